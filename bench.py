@@ -1,0 +1,221 @@
+"""Benchmark: shared-prefix decode attention (HBM GB/s) and extend attention
+(TFLOP/s) at the Llama-3-8B attention-layer shape, on one MI355X.
+
+A step is one pass of the hot path over one batch: the KV append of the
+step's new tokens, then attention for every query row (grouped prefix
+phase, suffix phase and the in-kernel log-sum-exp merge).  Inputs are
+resident in HBM before timing starts.
+
+Primary line (``value``): decode-8B -- Hq 32 / Hkv 8 / d 128, 4 agent
+prefixes x 2048 tokens, 64 decode requests (16 per agent, suffix U[64, 512]),
+1M-token (65,536-page) pool, pages scattered.  value = unique KV bytes per
+step (each prefix once + every suffix) / step time.  The step rotates over
+replicas of the batch on disjoint pages of the same pool so that the timed
+working set exceeds the 256 MB last-level cache.
+
+``extend``: extend-8B -- 3 prefixes x 4096, 32 requests with suffix
+U[256, 2048] prefilled against their agent's prefix; TFLOP/s over the
+causal-exact flop count.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-extend]
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+BF16_PEAK_TFLOPS = 2516.6      # MI355X dense bf16 MFMA, published
+METRIC = "shared-prefix decode attn HBM GB/s; extend attn TFLOP/s (8B layer shape)"
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def timed_steps(fn_step, fn_attn, steps, warmup, torch):
+    """Run warmup + timed steps; returns (ms per step, mean ms of the
+    attention call measured with events on the launch stream)."""
+    for i in range(warmup):
+        fn_step(i)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        fn_step(i, ev[i], stream)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3 / steps
+    attn = sum(a.elapsed_time(b) for a, b in ev) / steps
+    return wall, attn
+
+
+def bench_decode(args, torch, B, RN, W):
+    b = W.config_batch(2)
+    hv = W.host_values_fast(b, 2002)
+    ds = RN.DeviceStep(b, hv)
+    reps = W.replicas(b, args.replicas, 77)
+    # Replicas hold the same page contents at other pages (device copies).
+    src = torch.from_numpy(b.used_pages()).cuda()
+    plans = [ds.plan]
+    for rb in reps[1:]:
+        dst = torch.from_numpy(rb.used_pages()).cuda()
+        ds.k_pool.view(torch.int16).index_copy_(0, dst, ds.k_pool.view(torch.int16).index_select(0, src))
+        ds.v_pool.view(torch.int16).index_copy_(0, dst, ds.v_pool.view(torch.int16).index_select(0, src))
+        plans.append(B.plan_from_batch(ds.pool, rb, B.PFX_MODE_DECODE).upload())
+    torch.cuda.synchronize()
+
+    def step(i, ev=None, stream=None):
+        plan = plans[i % len(plans)]
+        B.pfx_append_kv(ds.pool, plan, ds.k_new, ds.v_new)
+        if ev is not None:
+            ev[0].record(stream)
+        B.pfx_attention(ds.pool, plan, ds.q, ds.o, ds.lse)
+        if ev is not None:
+            ev[1].record(stream)
+
+    ms, attn_ms = timed_steps(step, None, args.steps, args.warmup, torch)
+    B.pfx_sync_check()
+    u = b.unique_kv_bytes()
+    st = ds.plan.stats()
+    return dict(batch=b, hv=hv, ms=ms, attn_ms=attn_ms, unique_bytes=u, replicas=len(plans), stats=st)
+
+
+def bench_extend(args, torch, B, RN, W):
+    b = W.config_batch(3)
+    hv = W.host_values_fast(b, 2003)
+    ds = RN.DeviceStep(b, hv, poison=False)
+    torch.cuda.synchronize()
+
+    def step(i, ev=None, stream=None):
+        B.pfx_append_kv(ds.pool, ds.plan, ds.k_new, ds.v_new)
+        if ev is not None:
+            ev[0].record(stream)
+        B.pfx_attention(ds.pool, ds.plan, ds.q, ds.o, ds.lse)
+        if ev is not None:
+            ev[1].record(stream)
+
+    steps = max(3, args.steps // 4)
+    ms, attn_ms = timed_steps(step, None, steps, max(1, args.warmup // 4), torch)
+    B.pfx_sync_check()
+    return dict(ms=ms, attn_ms=attn_ms, flops=b.attention_flops(), steps=steps)
+
+
+def cpu_baseline(res, W):
+    """The fp64 oracle on a bounded sample of the decode step, on this host."""
+    import numpy as np
+
+    import oracle
+
+    b, hv = res["batch"], res["hv"]
+    cores = len(os.sched_getaffinity(0))
+    index = {int(p): i for i, p in enumerate(hv.pages)}
+    pp = [np.array([index[int(p)] for p in pl]) for pl in b.prefix_pages]
+    sp = [np.array([index[int(p)] for p in pl]) for pl in b.suffix_pages]
+    kp, vp = oracle.append_kv(hv.k_pages, hv.v_pages, sp, b.suffix_len, b.n_rows, hv.k_new, hv.v_new)
+    t0 = time.perf_counter()
+    done = 0
+    nbytes = 0
+    tau = b.num_kv_heads * b.head_dim * 4
+    for r in range(len(b.agent)):
+        oracle.prefix_shared_attention(kp, vp, pp, b.prefix_len, b.agent, sp, b.suffix_len, b.n_rows, hv.q,
+                                       b.num_q_heads, rows={r: [0]})
+        done += 1
+        # bytes the request reads: its agent's prefix (shared, counted once per
+        # request here as the oracle re-reads it) is not unique work, so count
+        # the unique share: suffix + prefix / requests-per-agent
+        a = int(b.agent[r])
+        share = int(b.prefix_len[a]) / int(np.sum(b.agent == a))
+        nbytes += (int(b.suffix_len[r]) + share) * tau
+        if time.perf_counter() - t0 > 20.0:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": round(nbytes / dt / 1e9, 4), "unit": "GB/s", "cores": cores, "kind": "oracle",
+            "sample": f"{done} of {len(b.agent)} decode requests of the decode-8B step (all 32 heads each), "
+                      f"fp64 numpy oracle, {dt:.1f} s; unique-KV-byte share per request"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--replicas", type=int, default=10)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-extend", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}), flush=True)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2608_25523_amd import binding as B
+    from paper_2608_25523_amd import runner as RN
+    from paper_2608_25523_amd import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    log("decode-8B: building inputs")
+    dec = bench_decode(args, torch, B, RN, W)
+    log(f"decode-8B: {dec['ms'] * 1e3:.1f} us/step, attention {dec['attn_ms'] * 1e3:.1f} us")
+    ext = None
+    if not args.no_extend:
+        log("extend-8B: building inputs")
+        ext = bench_extend(args, torch, B, RN, W)
+        log(f"extend-8B: {ext['ms']:.3f} ms/step, attention {ext['attn_ms']:.3f} ms")
+    cpu = None
+    if not args.no_cpu:
+        log("cpu baseline (oracle)")
+        cpu = cpu_baseline(dec, W)
+
+    u = dec["unique_bytes"]
+    value = u / (dec["ms"] * 1e-3) / 1e9
+    achieved = u / (dec["attn_ms"] * 1e-3) / 1e9
+    st = dec["stats"]
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(dec["ms"], 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) bf16; lengths per the workload recipe)",
+        "config": {"workload": "decode-8B: Hq32/Hkv8/d128, 4 prefixes x 2048, 64 decode reqs (16/agent, "
+                               "suffix U[64,512]), 65536-page pool, random placement",
+                   "unique_kv_bytes": u, "replicas": dec["replicas"], "items": st.num_items,
+                   "prefix_items": st.num_prefix_items, "suffix_items": st.num_suffix_items},
+        "roofline": {"bound": "hbm", "kernel": "attn_kernel (pfx_attention)",
+                     "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "attn_us": round(dec["attn_ms"] * 1e3, 3)},
+        "cpu_baseline": cpu,
+    }
+    if ext is not None:
+        tf = ext["flops"] / (ext["attn_ms"] * 1e-3) / 1e12
+        out["extend"] = {
+            "workload": "extend-8B: Hq32/Hkv8/d128, 3 prefixes x 4096, 32 reqs suffix U[256,2048]",
+            "value": round(ext["flops"] / (ext["ms"] * 1e-3) / 1e12, 2), "unit": "TFLOP/s",
+            "ms_per_step": round(ext["ms"], 4), "steps": ext["steps"],
+            "roofline": {"bound": "mfma", "kernel": "attn_kernel (pfx_attention)", "achieved": round(tf, 2),
+                         "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(tf / BF16_PEAK_TFLOPS, 4),
+                         "traffic": None, "flops": ext["flops"]},
+        }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

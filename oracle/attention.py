@@ -81,20 +81,17 @@ def gather_tokens(pool, page_ids: Sequence[int], length: int) -> np.ndarray:
 
     ``pool[p]`` must return the bf16 bits of page p, shaped [Hkv][PAGE][d]
     (a numpy array [num_pages][Hkv][PAGE][d] works, so does a dict of pages).
-    Token j lives in page ``page_ids[j // PAGE]`` at slot ``j % PAGE``.  The
-    loop walks tokens one at a time so the mapping is visible by eye.
+    Token j lives in page ``page_ids[j // PAGE]`` at slot ``j % PAGE``; the
+    loop walks the pages in order and takes the slots each one holds.
     Returns float64 [length][Hkv][d].
     """
-    if length == 0:
-        probe = np.asarray(pool[page_ids[0]]) if len(page_ids) else None
-        hkv = probe.shape[0] if probe is not None else 0
-        d = probe.shape[2] if probe is not None else 0
-        return np.zeros((0, hkv, d))
     first = np.asarray(pool[page_ids[0]])
     out = np.empty((length, first.shape[0], first.shape[2]), dtype=np.float64)
-    for j in range(length):
-        page = np.asarray(pool[page_ids[j // PAGE_SIZE]])
-        out[j] = bf16_bits_to_f64(page[:, j % PAGE_SIZE, :])
+    for i in range(pages_needed(length)):
+        page = np.asarray(pool[page_ids[i]])                # [Hkv][PAGE][d]
+        lo = i * PAGE_SIZE
+        hi = min(lo + PAGE_SIZE, length)
+        out[lo:hi] = bf16_bits_to_f64(page[:, :hi - lo, :]).transpose(1, 0, 2)
     return out
 
 

@@ -1,0 +1,96 @@
+// Internal layout shared by the host plan builder (pfx_plan.cpp) and the
+// device code (pfx_kernels.hip).  Not part of the public interface.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/pfx_attn.h"
+
+namespace pfx {
+
+// Columns of one MFMA tile: the query side of a 16x16x32 bf16 product.
+constexpr int kTileCols = 16;
+// Largest number of 16-column blocks one wave carries (64 query columns).
+constexpr int kMaxBlocks = 4;
+// Keys processed per inner step (two 16-token pages).
+constexpr int kStepKeys = 32;
+// Waves per workgroup; they split an item's key steps between them.
+constexpr int kWaves = 4;
+
+enum ItemKind : int32_t { kPrefixItem = 0, kSuffixItem = 1, kExtendItem = 2 };
+
+// One unit of device work, run by one workgroup.  Its query columns are
+// row_count tokens (row_tok[row_begin ...]) times the G query heads of KV
+// head kv_head.  Keys come from up to two segments of the plan's page list:
+//   segment 0 (no mask):  keys [s0_kbeg, s0_kend) of the list at s0_page_off;
+//   segment 1 (causal):   keys [s1_kbeg, s1_kend) of the list at s1_page_off,
+//                         key k visible to token t iff k <= t + causal_base.
+// out_slot < 0: final output rows; otherwise partial slot out_slot of every
+// request the item covers.
+struct alignas(16) Item {
+  int32_t kv_head;
+  int32_t row_begin;
+  int32_t row_count;
+  int32_t nblk;
+  int32_t s0_page_off, s0_kbeg, s0_kend;
+  int32_t s1_page_off, s1_kbeg, s1_kend;
+  int32_t causal_base;
+  int32_t out_slot;
+  int32_t kind;
+  int32_t req;  // request of a suffix/extend item, -1 for prefix items
+  int32_t pad0, pad1;
+};
+static_assert(sizeof(Item) == 64, "Item is 16 int32");
+
+// Per-request bookkeeping on the device.
+struct ReqInfo {
+  int32_t q_start;    // first query row
+  int32_t n;          // query rows
+  int32_t nparts;     // partial results to merge (1: written directly)
+  int32_t part_base;  // first partial row: (part_base + slot * n + i) for row i
+};
+
+// Device pointers into an uploaded workspace.
+struct DevPlan {
+  const Item* items;
+  const int32_t* row_tok;
+  const int32_t* page_list;
+  const int32_t* tok_req;
+  const ReqInfo* req;
+  const int32_t* tok_slot;  // page * 16 + slot of every new token (append)
+  int32_t* counters;        // [num_reqs * hkv], zero between launches
+  float* o_part;            // [num_part_rows][hq][d]
+  float* l_part;            // [num_part_rows][hq]
+};
+
+}  // namespace pfx
+
+struct pfx_plan {
+  int32_t num_pages = 0, hkv = 0, d = 0, hq = 0, group = 0, mode = 0;
+  int32_t num_reqs = 0, num_tokens = 0;
+  int32_t n_items_wide = 0;  // items[0, n_items_wide): more than one 16-column block
+  std::vector<pfx::Item> items;
+  std::vector<int32_t> row_tok, page_list, tok_req, tok_slot;
+  std::vector<pfx::ReqInfo> req;
+  int64_t num_part_rows = 0;
+  int32_t n_prefix_items = 0, n_suffix_items = 0, n_extend_items = 0;
+  int32_t pages_needed = 0;
+  // byte offsets inside the workspace
+  size_t off_items = 0, off_row_tok = 0, off_page_list = 0, off_tok_req = 0, off_req = 0,
+         off_tok_slot = 0, off_counters = 0, off_opart = 0, off_lpart = 0, total_bytes = 0,
+         blob_bytes = 0;
+  std::vector<unsigned char> blob;  // host image of [0, off_counters)
+  void* dev_ws = nullptr;
+  size_t dev_ws_bytes = 0;
+};
+
+namespace pfx {
+// Thread-local error text, set by every failing entry point.
+int fail(int code, const char* fmt, ...);
+void clear_error();
+pfx::DevPlan dev_plan(const pfx_plan* p);
+}  // namespace pfx

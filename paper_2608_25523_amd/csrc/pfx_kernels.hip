@@ -1,0 +1,706 @@
+// Device side of libpfxattn: kernels for gfx950 (CDNA4) and the entry points
+// that launch them.
+//
+// Attention layout on the MFMA units (v_mfma_f32_16x16x32_bf16, wave64):
+//   S^T = K Q^T     A = 16 keys x 32 head dims (one page of one KV head per
+//                   tile), B = 32 head dims x 16 query columns; each lane
+//                   ends up holding 4 scores of one query column.
+//   O^T = V^T P^T   A = 16 head dims x 32 keys, B = 32 keys x 16 columns,
+//                   taken straight from the lane's own scores, so the
+//                   online-softmax statistics of a column never leave the
+//                   four lanes that own it.
+// V is read from the pool with the keys as the contiguous direction of
+// neither operand; each lane loads 8 keys x (D/16) dims and transposes them
+// in registers with byte permutes.
+//
+// Work is a list of items (see pfx_internal.h).  A workgroup of four waves
+// runs one item: the waves take its 32-key steps round-robin, each with the
+// full set of query columns, and combine their softmax states through LDS.
+// An item whose keys are only part of a row's keys (a prefix chunk, a
+// suffix chunk) writes a partial result; the last item to finish for a
+// (request, KV head) merges all of its partials (log-sum-exp merge) and
+// writes the final row.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+
+#include "pfx_internal.h"
+
+namespace pfx {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+// Lazy rescaling: the running maximum is only raised when a new score
+// exceeds it by more than this (log2 units), so exp2 arguments stay <= 8.
+constexpr float kRescaleSlack = 8.0f;
+// Finite "minus infinity" for the running maximum: exp2(score - kNegBig) of a
+// masked score (-inf) is still 0, and no inf - inf can arise.
+constexpr float kNegBig = -1.0e30f;
+
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  f32x2 v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// V chunk held by one lane for one key: D/16 bf16 values.
+template <int D> struct VecCH;
+template <> struct VecCH<128> { typedef u32x4 T; static constexpr int dwords = 4; };
+template <> struct VecCH<64> { typedef u32x2 T; static constexpr int dwords = 2; };
+
+template <int D>
+struct KVRegs {
+  static constexpr int KS = D / 32;
+  u32x4 k[2][KS];                    // [tile][k-step]: key (lane & 15), dims 32s + 8*(lane>>4) .. +7
+  typename VecCH<D>::T v[2][4];      // [tile][i]: key 4*(lane>>4) + i, dims (D/16)*(lane&15) .. +D/16-1
+};
+
+struct AttnArgs {
+  const uint16_t* kpool;
+  const uint16_t* vpool;
+  const uint16_t* q;
+  uint16_t* o;
+  float* lse;
+  DevPlan plan;
+  int32_t item_base;
+  int32_t hq, hkv, group, group_shift;
+  float scale_log2;  // sm_scale * log2(e)
+};
+
+// Geometry of one 32-key step of an item.
+struct StepPos {
+  const int32_t* pages;  // page list of the segment
+  int32_t k0, kend;      // first key of the step, end of the segment
+  bool causal;           // segment 1
+};
+
+__device__ __forceinline__ StepPos step_pos(const Item& it, const int32_t* page_list, int st, int s0_steps) {
+  StepPos p;
+  if (st < s0_steps) {
+    p.pages = page_list + it.s0_page_off;
+    p.k0 = it.s0_kbeg + st * kStepKeys;
+    p.kend = it.s0_kend;
+    p.causal = false;
+  } else {
+    p.pages = page_list + it.s1_page_off;
+    p.k0 = it.s1_kbeg + (st - s0_steps) * kStepKeys;
+    p.kend = it.s1_kend;
+    p.causal = true;
+  }
+  return p;
+}
+
+template <int D>
+__device__ __forceinline__ void load_kv(KVRegs<D>& r, const AttnArgs& a, const StepPos& p, int h, int col,
+                                        int grp) {
+  constexpr int KS = D / 32;
+  constexpr int CH = D / 16;
+  const int page0 = p.pages[p.k0 >> 4];
+  const bool has1 = p.k0 + 16 < p.kend;
+  const int page1 = has1 ? p.pages[(p.k0 >> 4) + 1] : page0;
+  const size_t head_elems = size_t(16) * D;
+  const size_t b0 = (size_t(page0) * a.hkv + h) * head_elems;
+  const size_t b1 = (size_t(page1) * a.hkv + h) * head_elems;
+  const uint16_t* k0p = a.kpool + b0 + col * D + 8 * grp;
+  const uint16_t* k1p = a.kpool + b1 + col * D + 8 * grp;
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    r.k[0][s] = *reinterpret_cast<const u32x4*>(k0p + 32 * s);
+    r.k[1][s] = *reinterpret_cast<const u32x4*>(k1p + 32 * s);
+  }
+  const uint16_t* v0p = a.vpool + b0 + (4 * grp) * D + CH * col;
+  const uint16_t* v1p = a.vpool + b1 + (4 * grp) * D + CH * col;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    r.v[0][i] = *reinterpret_cast<const typename VecCH<D>::T*>(v0p + i * D);
+    r.v[1][i] = *reinterpret_cast<const typename VecCH<D>::T*>(v1p + i * D);
+  }
+}
+
+// bf16 element e (0..D/16-1) of a lane's V chunk, as the low 16 bits.
+template <int D>
+__device__ __forceinline__ uint32_t v_elem_pair(const typename VecCH<D>::T& a, const typename VecCH<D>::T& b,
+                                                int e) {
+  // Pack element e of key a (low half) with element e of key b (high half).
+  const uint32_t wa = a[e >> 1], wb = b[e >> 1];
+  return (e & 1) ? __builtin_amdgcn_perm(wb, wa, 0x07060302u) : __builtin_amdgcn_perm(wb, wa, 0x05040100u);
+}
+
+template <int D, int QB>
+struct WaveState {
+  static constexpr int CH = D / 16;
+  f32x4 acc[QB][CH];  // O^T: lane holds dims CH*(4*grp + i) + jj of its column, [jj][i]
+  float m[QB];        // running max (log2 units), same in the 4 lanes of a column
+  float l[QB];        // this lane's share of the running sum
+};
+
+template <int D, int QB>
+__device__ __forceinline__ void compute_step(WaveState<D, QB>& ws, KVRegs<D>& r, const bf16x8 (&qf)[QB][D / 32],
+                                             const int (&lim)[QB], const StepPos& p, int nblk, int grp,
+                                             float scale_log2) {
+  constexpr int KS = D / 32;
+  constexpr int CH = D / 16;
+  const bool tail = p.k0 + kStepKeys > p.kend;
+  if (tail) {
+    // Keys past the end of the segment: zero their V (the slots may hold
+    // anything) -- their probabilities are forced to 0 below.
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (p.k0 + 16 * t + 4 * grp + i >= p.kend) r.v[t][i] = typename VecCH<D>::T{};
+  }
+  // V^T operands: vt[jj] holds dim CH*col + jj of the 8 keys this lane owns.
+  bf16x8 vt[CH];
+#pragma unroll
+  for (int jj = 0; jj < CH; ++jj) {
+    u32x4 w;
+    w[0] = v_elem_pair<D>(r.v[0][0], r.v[0][1], jj);
+    w[1] = v_elem_pair<D>(r.v[0][2], r.v[0][3], jj);
+    w[2] = v_elem_pair<D>(r.v[1][0], r.v[1][1], jj);
+    w[3] = v_elem_pair<D>(r.v[1][2], r.v[1][3], jj);
+    vt[jj] = __builtin_bit_cast(bf16x8, w);
+  }
+  const bool need_mask = tail || p.causal;
+#pragma unroll
+  for (int b = 0; b < QB; ++b) {
+    if (b >= nblk) break;
+    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, r.k[0][s]), qf[b][s], s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, r.k[1][s]), qf[b][s], s1, 0, 0, 0);
+    }
+    float x[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      x[i] = s0[i] * scale_log2;
+      x[4 + i] = s1[i] * scale_log2;
+    }
+    if (need_mask) {
+      const int lim_b = p.causal ? lim[b] : 0x7fffffff;
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int key = p.k0 + 16 * t + 4 * grp + i;
+          if (key >= p.kend || key > lim_b) x[4 * t + i] = -INFINITY;
+        }
+    }
+    float mx = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const bool raise = mx > ws.m[b] + kRescaleSlack;
+    if (__any(raise)) {
+      const float mnew = raise ? mx : ws.m[b];
+      const float alpha = fast_exp2(ws.m[b] - mnew);
+      ws.l[b] *= alpha;
+#pragma unroll
+      for (int jj = 0; jj < CH; ++jj) ws.acc[b][jj] *= alpha;
+      ws.m[b] = mnew;
+    }
+    float pr[8];
+    float psum = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      pr[j] = fast_exp2(x[j] - ws.m[b]);
+      psum += pr[j];
+    }
+    ws.l[b] += psum;
+    u32x4 pw;
+    pw[0] = pack_bf16(pr[0], pr[1]);
+    pw[1] = pack_bf16(pr[2], pr[3]);
+    pw[2] = pack_bf16(pr[4], pr[5]);
+    pw[3] = pack_bf16(pr[6], pr[7]);
+    const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
+#pragma unroll
+    for (int jj = 0; jj < CH; ++jj)
+      ws.acc[b][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt[jj], pb, ws.acc[b][jj], 0, 0, 0);
+  }
+}
+
+// Merge `nparts` partial results for 8 consecutive dims of one row:
+//   lse = ln sum_k exp(lse_k),  O = sum_k exp(lse_k - lse) O_k.
+// o_row points at dims d0..d0+7 of partial 0; partial k is o_stride floats
+// further on; lse_k is at l_row[k * l_stride].
+__device__ __forceinline__ void merge_row8(const float* o_row, size_t o_stride, const float* l_row, size_t l_stride,
+                                           int nparts, uint16_t* out8, float* lse_out) {
+  float mx = -INFINITY;
+  for (int k = 0; k < nparts; ++k) mx = fmaxf(mx, l_row[k * l_stride]);
+  float z = 0.f;
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int k = 0; k < nparts; ++k) {
+    const float w = fast_exp2((l_row[k * l_stride] - mx) * kLog2e);
+    z += w;
+    const f32x4 a = *reinterpret_cast<const f32x4*>(o_row + k * o_stride);
+    const f32x4 b = *reinterpret_cast<const f32x4*>(o_row + k * o_stride + 4);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      acc[e] += w * a[e];
+      acc[4 + e] += w * b[e];
+    }
+  }
+  const float inv = 1.0f / z;
+  u32x4 ow;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) ow[e] = pack_bf16(acc[2 * e] * inv, acc[2 * e + 1] * inv);
+  *reinterpret_cast<u32x4*>(out8) = ow;
+  if (lse_out) *lse_out = mx + logf(z);
+}
+
+// Merge every partial of (request r, KV head h) into the final rows.
+template <int D>
+__device__ void merge_request(const AttnArgs& a, int r, int h) {
+  const ReqInfo ri = a.plan.req[r];
+  const int G = a.group;
+  constexpr int SL = D / 8;  // 8-dim slices per row
+  const int rows = ri.n * G;
+  for (int t = threadIdx.x; t < rows * SL; t += blockDim.x) {
+    const int x = t / SL, sl = t - x * SL;
+    const int i = x >> a.group_shift, g = x & (G - 1);
+    const int qh = h * G + g;
+    const size_t prow = size_t(ri.part_base) + i;
+    const float* orow = a.plan.o_part + (prow * a.hq + qh) * D + sl * 8;
+    const float* lrow = a.plan.l_part + prow * a.hq + qh;
+    const size_t tok = size_t(ri.q_start) + i;
+    uint16_t* out = a.o + (tok * a.hq + qh) * D + sl * 8;
+    float* lo = (a.lse && sl == 0) ? a.lse + tok * a.hq + qh : nullptr;
+    merge_row8(orow, size_t(ri.n) * a.hq * D, lrow, size_t(ri.n) * a.hq, ri.nparts, out, lo);
+  }
+}
+
+template <int D, int QB>
+__global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
+  constexpr int KS = D / 32;
+  constexpr int CH = D / 16;
+  constexpr int NCOL = QB * kTileCols;
+  // Cross-wave combination buffers.
+  __shared__ float red_o[kWaves][NCOL][D + 4];
+  __shared__ float red_m[kWaves][NCOL];
+  __shared__ float red_l[kWaves][NCOL];
+  __shared__ int last_req[64];
+  __shared__ int n_last;
+
+  const Item it = a.plan.items[a.item_base + blockIdx.x];
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int col = lane & 15, grp = lane >> 4;
+  const int h = it.kv_head;
+  const int G = a.group;
+  const int nblk = it.nblk;
+
+  // Query operands and causal limits of this lane's columns.
+  bf16x8 qf[QB][KS];
+  int lim[QB];
+#pragma unroll
+  for (int b = 0; b < QB; ++b) {
+    const int c = b * kTileCols + col;
+    int j = c >> a.group_shift;
+    const int g = c & (G - 1);
+    if (j >= it.row_count) j = 0;  // padding column: a copy of the first token, never stored
+    const int tok = a.plan.row_tok[it.row_begin + j];
+    lim[b] = tok + it.causal_base;
+    if (b < nblk) {
+      const uint16_t* qp = a.q + (size_t(tok) * a.hq + h * G + g) * D + 8 * grp;
+#pragma unroll
+      for (int s = 0; s < KS; ++s) qf[b][s] = *reinterpret_cast<const bf16x8*>(qp + 32 * s);
+    } else {
+#pragma unroll
+      for (int s = 0; s < KS; ++s) qf[b][s] = bf16x8{};
+    }
+  }
+
+  WaveState<D, QB> ws;
+#pragma unroll
+  for (int b = 0; b < QB; ++b) {
+    ws.m[b] = kNegBig;
+    ws.l[b] = 0.f;
+#pragma unroll
+    for (int jj = 0; jj < CH; ++jj) ws.acc[b][jj] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  const int s0_steps = (it.s0_kend - it.s0_kbeg + kStepKeys - 1) / kStepKeys;
+  const int s1_steps = (it.s1_kend - it.s1_kbeg + kStepKeys - 1) / kStepKeys;
+  const int nsteps = s0_steps + s1_steps;
+
+  // Two register buffers: the next step's K/V is in flight while the
+  // current one is multiplied.
+  KVRegs<D> bufA, bufB;
+  int st = wave;
+  if (st < nsteps) load_kv<D>(bufA, a, step_pos(it, a.plan.page_list, st, s0_steps), h, col, grp);
+  while (st < nsteps) {
+    int nst = st + kWaves;
+    if (nst < nsteps) load_kv<D>(bufB, a, step_pos(it, a.plan.page_list, nst, s0_steps), h, col, grp);
+    compute_step<D, QB>(ws, bufA, qf, lim, step_pos(it, a.plan.page_list, st, s0_steps), nblk, grp, a.scale_log2);
+    st = nst;
+    if (st >= nsteps) break;
+    nst = st + kWaves;
+    if (nst < nsteps) load_kv<D>(bufA, a, step_pos(it, a.plan.page_list, nst, s0_steps), h, col, grp);
+    compute_step<D, QB>(ws, bufB, qf, lim, step_pos(it, a.plan.page_list, st, s0_steps), nblk, grp, a.scale_log2);
+    st = nst;
+  }
+
+  // Per-wave state to LDS: unnormalised O, max and the column's sum.
+#pragma unroll
+  for (int b = 0; b < QB; ++b) {
+    if (b >= nblk) break;
+    float l = ws.l[b];
+    l += __shfl_xor(l, 16);
+    l += __shfl_xor(l, 32);
+    const int c = b * kTileCols + col;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int jj = 0; jj < CH; ++jj) red_o[wave][c][CH * (4 * grp + i) + jj] = ws.acc[b][jj][i];
+    if (grp == 0) {
+      red_m[wave][c] = ws.m[b];
+      red_l[wave][c] = l;
+    }
+  }
+  __syncthreads();
+
+  // Combine the waves: each thread owns one column and a slice of dims.
+  const int ncols = nblk * kTileCols;
+  constexpr int TPC = 256 / NCOL;      // threads per column
+  constexpr int SLICE = D / TPC;       // dims per thread (multiple of 8)
+  const bool partial = it.out_slot >= 0;
+  {
+    const int c = threadIdx.x / TPC;
+    const int d0 = (threadIdx.x - c * TPC) * SLICE;
+    const int j = c >> a.group_shift;
+    if (c < ncols && j < it.row_count) {
+      const int g = c & (G - 1);
+      const int qh = h * G + g;
+      float mx = kNegBig;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) mx = fmaxf(mx, red_m[w][c]);
+      float wgt[kWaves];
+      float z = 0.f;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        wgt[w] = fast_exp2(red_m[w][c] - mx);
+        z += wgt[w] * red_l[w][c];
+      }
+      // A row can see none of a chunk's keys (a multi-row decode request whose
+      // last suffix chunk starts after its first row): O = 0, LSE = -inf,
+      // which the merge weighs with exp(-inf) = 0.
+      const float inv = z > 0.f ? 1.0f / z : 0.f;
+      const float lse_nat = z > 0.f ? (mx + log2f(z)) * kLn2 : -INFINITY;
+      const int tok = a.plan.row_tok[it.row_begin + j];
+      if (!partial) {
+        uint16_t* out = a.o + (size_t(tok) * a.hq + qh) * D + d0;
+        constexpr int UNIT = SLICE >= 8 ? 8 : 4;
+#pragma unroll
+        for (int e = 0; e < SLICE; e += UNIT) {
+          float v[UNIT];
+#pragma unroll
+          for (int u = 0; u < UNIT; ++u) {
+            float s = 0.f;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) s += wgt[w] * red_o[w][c][d0 + e + u];
+            v[u] = s * inv;
+          }
+          if constexpr (UNIT == 8) {
+            u32x4 ow = {pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]), pack_bf16(v[4], v[5]), pack_bf16(v[6], v[7])};
+            *reinterpret_cast<u32x4*>(out + e) = ow;
+          } else {
+            u32x2 ow = {pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3])};
+            *reinterpret_cast<u32x2*>(out + e) = ow;
+          }
+        }
+        if (a.lse && d0 == 0) a.lse[size_t(tok) * a.hq + qh] = lse_nat;
+      } else {
+        const int r = a.plan.tok_req[tok];
+        const ReqInfo ri = a.plan.req[r];
+        const size_t prow = size_t(ri.part_base) + size_t(it.out_slot) * ri.n + (tok - ri.q_start);
+        float* out = a.plan.o_part + (prow * a.hq + qh) * D + d0;
+#pragma unroll
+        for (int e = 0; e < SLICE; e += 4) {
+          f32x4 v;
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            float s = 0.f;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) s += wgt[w] * red_o[w][c][d0 + e + u];
+            v[u] = s * inv;
+          }
+          *reinterpret_cast<f32x4*>(out + e) = v;
+        }
+        if (d0 == 0) a.plan.l_part[prow * a.hq + qh] = lse_nat;
+      }
+    }
+  }
+  if (!partial) return;
+
+  // Arrival: make the partial rows visible device-wide, then count this
+  // item once per (request, KV head) it covers.  The last arrival merges.
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) n_last = 0;
+  __syncthreads();
+  if (threadIdx.x < it.row_count) {
+    const int tok = a.plan.row_tok[it.row_begin + threadIdx.x];
+    const int r = a.plan.tok_req[tok];
+    const ReqInfo ri = a.plan.req[r];
+    if (tok == ri.q_start) {
+      const int old = atomicAdd(a.plan.counters + size_t(r) * a.hkv + h, 1);
+      if (old == ri.nparts - 1) {
+        const int slot = atomicAdd(&n_last, 1);
+        last_req[slot] = r;
+      }
+    }
+  }
+  __syncthreads();
+  const int nl = n_last;
+  if (nl == 0) return;
+  __threadfence();
+  for (int k = 0; k < nl; ++k) {
+    const int r = last_req[k];
+    merge_request<D>(a, r, h);
+    if (threadIdx.x == 0) atomicExch(a.plan.counters + size_t(r) * a.hkv + h, 0);
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void merge_states_kernel(const float* o_parts, const float* lse_parts, int nparts,
+                                                           int rows, uint16_t* o, float* lse) {
+  constexpr int SL = D / 8;
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= rows * SL) return;
+  const int x = t / SL, sl = t - x * SL;
+  merge_row8(o_parts + size_t(x) * D + sl * 8, size_t(rows) * D, lse_parts + x, size_t(rows), nparts,
+             o + size_t(x) * D + sl * 8, (lse && sl == 0) ? lse + x : nullptr);
+}
+
+// One thread per 16-byte chunk of a new token's K or V row.
+template <int D>
+__global__ __launch_bounds__(256) void append_kernel(const uint16_t* k_new, const uint16_t* v_new, uint16_t* kpool,
+                                                     uint16_t* vpool, const int32_t* tok_slot, int tokens, int hkv) {
+  constexpr int CPR = D / 8;  // chunks per (token, head)
+  const size_t per = size_t(tokens) * hkv * CPR;
+  const size_t idx = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (idx >= 2 * per) return;
+  const bool is_v = idx >= per;
+  const size_t e = is_v ? idx - per : idx;
+  const int c = int(e % CPR);
+  const size_t th = e / CPR;
+  const int hh = int(th % hkv);
+  const int t = int(th / hkv);
+  const int slot = tok_slot[t];
+  const size_t dst = ((size_t(slot >> 4) * hkv + hh) * 16 + (slot & 15)) * D + 8 * c;
+  const size_t src = (size_t(t) * hkv + hh) * D + 8 * c;
+  const uint16_t* s = is_v ? v_new : k_new;
+  uint16_t* d = is_v ? vpool : kpool;
+  *reinterpret_cast<u32x4*>(d + dst) = *reinterpret_cast<const u32x4*>(s + src);
+}
+
+// grid (chunks of a page, pages, 2 for K/V); pairs[2i] = dst page, pairs[2i+1] = src page.
+__global__ __launch_bounds__(256) void page_copy_kernel(const u32x4* src_k, const u32x4* src_v, u32x4* dst_k,
+                                                        u32x4* dst_v, const int32_t* pairs, size_t page_vecs) {
+  const size_t v = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (v >= page_vecs) return;
+  const int i = blockIdx.y;
+  const size_t dp = size_t(pairs[2 * i]), sp = size_t(pairs[2 * i + 1]);
+  if (blockIdx.z == 0)
+    dst_k[dp * page_vecs + v] = src_k[sp * page_vecs + v];
+  else
+    dst_v[dp * page_vecs + v] = src_v[sp * page_vecs + v];
+}
+
+__global__ void zero_kernel(int32_t* p, size_t n) {
+  const size_t i = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+
+static int hip_fail(hipError_t e, const char* what) {
+  return fail(PFX_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+static int check_launch(const char* what) {
+  hipError_t e = hipGetLastError();
+  return e == hipSuccess ? PFX_OK : hip_fail(e, what);
+}
+
+static int check_pool_matches(const pfx_pool* pool, const pfx_plan* p, const char* who) {
+  if (!pool) return fail(PFX_EINVAL, "%s: pool is NULL", who);
+  if (!p) return fail(PFX_EINVAL, "%s: plan is NULL", who);
+  if (pool->page_size != PFX_PAGE_SIZE || pool->num_kv_heads != p->hkv || pool->head_dim != p->d ||
+      pool->num_pages != p->num_pages)
+    return fail(PFX_EINVAL, "%s: pool shape differs from the one the plan was built for", who);
+  if (!pool->k_pages || !pool->v_pages) return fail(PFX_EINVAL, "%s: pool pointers are NULL", who);
+  if (!p->dev_ws) return fail(PFX_EINVAL, "%s: plan has not been uploaded", who);
+  return PFX_OK;
+}
+
+template <int D, int QB>
+static void launch_attn(const AttnArgs& a, int n, hipStream_t s) {
+  hipLaunchKernelGGL((attn_kernel<D, QB>), dim3(n), dim3(256), 0, s, a);
+}
+
+}  // namespace pfx
+
+using namespace pfx;
+
+extern "C" int pfx_plan_upload(pfx_plan* p, void* ws, size_t bytes, void* stream) {
+  if (!p || !ws) return fail(PFX_EINVAL, "pfx_plan_upload: NULL argument");
+  if (reinterpret_cast<uintptr_t>(ws) % 256) return fail(PFX_EINVAL, "pfx_plan_upload: workspace not 256-byte aligned");
+  if (bytes < p->total_bytes)
+    return fail(PFX_ENOMEM, "pfx_plan_upload: workspace has %zu bytes, plan needs %zu", bytes, p->total_bytes);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (p->blob_bytes) {
+    hipError_t e = hipMemcpyAsync(ws, p->blob.data(), p->blob_bytes, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return hip_fail(e, "pfx_plan_upload: hipMemcpyAsync");
+  }
+  const size_t nc = size_t(p->num_reqs) * p->hkv;
+  if (nc) {
+    int32_t* c = reinterpret_cast<int32_t*>(static_cast<unsigned char*>(ws) + p->off_counters);
+    hipLaunchKernelGGL(zero_kernel, dim3((nc + 255) / 256), dim3(256), 0, s, c, nc);
+    int rc = check_launch("pfx_plan_upload: zero_kernel");
+    if (rc) return rc;
+  }
+  p->dev_ws = ws;
+  p->dev_ws_bytes = bytes;
+  return PFX_OK;
+}
+
+extern "C" int pfx_append_kv(const pfx_pool* pool, const pfx_plan* p, const void* k_new, const void* v_new,
+                             void* stream) {
+  int rc = check_pool_matches(pool, p, "pfx_append_kv");
+  if (rc) return rc;
+  if (p->num_tokens == 0) return PFX_OK;
+  if (!k_new || !v_new) return fail(PFX_EINVAL, "pfx_append_kv: k_new or v_new is NULL");
+  const DevPlan dp = dev_plan(p);
+  const size_t total = 2 * size_t(p->num_tokens) * p->hkv * (p->d / 8);
+  const dim3 grid((total + 255) / 256);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  auto kn = static_cast<const uint16_t*>(k_new);
+  auto vn = static_cast<const uint16_t*>(v_new);
+  auto kp = static_cast<uint16_t*>(pool->k_pages);
+  auto vp = static_cast<uint16_t*>(pool->v_pages);
+  if (p->d == 128)
+    hipLaunchKernelGGL(append_kernel<128>, grid, dim3(256), 0, s, kn, vn, kp, vp, dp.tok_slot, p->num_tokens, p->hkv);
+  else
+    hipLaunchKernelGGL(append_kernel<64>, grid, dim3(256), 0, s, kn, vn, kp, vp, dp.tok_slot, p->num_tokens, p->hkv);
+  return check_launch("pfx_append_kv");
+}
+
+extern "C" int pfx_attention(const pfx_pool* pool, const pfx_plan* p, const void* q, void* o, float* lse,
+                             float sm_scale, void* stream) {
+  int rc = check_pool_matches(pool, p, "pfx_attention");
+  if (rc) return rc;
+  if (p->items.empty()) return PFX_OK;
+  if (!q || !o) return fail(PFX_EINVAL, "pfx_attention: q or o is NULL");
+  if (!(sm_scale > 0.f)) sm_scale = 1.0f / sqrtf(float(p->d));
+  AttnArgs a;
+  a.kpool = static_cast<const uint16_t*>(pool->k_pages);
+  a.vpool = static_cast<const uint16_t*>(pool->v_pages);
+  a.q = static_cast<const uint16_t*>(q);
+  a.o = static_cast<uint16_t*>(o);
+  a.lse = lse;
+  a.plan = dev_plan(p);
+  a.hq = p->hq;
+  a.hkv = p->hkv;
+  a.group = p->group;
+  a.group_shift = __builtin_ctz(static_cast<unsigned>(p->group));
+  a.scale_log2 = sm_scale * kLog2e;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int n_wide = p->n_items_wide;
+  const int n_narrow = static_cast<int>(p->items.size()) - n_wide;
+  if (n_wide) {
+    a.item_base = 0;
+    if (p->d == 128) launch_attn<128, 4>(a, n_wide, s); else launch_attn<64, 4>(a, n_wide, s);
+    if ((rc = check_launch("pfx_attention (wide items)"))) return rc;
+  }
+  if (n_narrow) {
+    a.item_base = n_wide;
+    if (p->d == 128) launch_attn<128, 1>(a, n_narrow, s); else launch_attn<64, 1>(a, n_narrow, s);
+    if ((rc = check_launch("pfx_attention (narrow items)"))) return rc;
+  }
+  return PFX_OK;
+}
+
+extern "C" int pfx_merge_states(const float* o_parts, const float* lse_parts, int32_t num_parts, int32_t rows,
+                                int32_t head_dim, void* o, float* lse, void* stream) {
+  if (!o_parts || !lse_parts || !o) return fail(PFX_EINVAL, "pfx_merge_states: NULL argument");
+  if (head_dim != 64 && head_dim != 128) return fail(PFX_EUNSUPPORTED, "pfx_merge_states: head_dim %d", head_dim);
+  if (num_parts < 1 || num_parts > 4096) return fail(PFX_ERANGE, "pfx_merge_states: num_parts %d", num_parts);
+  if (rows < 0) return fail(PFX_ERANGE, "pfx_merge_states: rows %d", rows);
+  if (rows == 0) return PFX_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const size_t threads = size_t(rows) * (head_dim / 8);
+  const dim3 grid((threads + 255) / 256);
+  if (head_dim == 128)
+    hipLaunchKernelGGL(merge_states_kernel<128>, grid, dim3(256), 0, s, o_parts, lse_parts, num_parts, rows,
+                       static_cast<uint16_t*>(o), lse);
+  else
+    hipLaunchKernelGGL(merge_states_kernel<64>, grid, dim3(256), 0, s, o_parts, lse_parts, num_parts, rows,
+                       static_cast<uint16_t*>(o), lse);
+  return check_launch("pfx_merge_states");
+}
+
+extern "C" size_t pfx_page_copy_workspace_bytes(int32_t n) { return n <= 0 ? 256 : (size_t(n) * 8 + 255) & ~size_t(255); }
+
+extern "C" int pfx_page_copy(const pfx_pool* dst, const pfx_pool* src, const int32_t* dst_pages,
+                             const int32_t* src_pages, int32_t n, void* ws, size_t ws_bytes, void* stream) {
+  if (!dst || !src) return fail(PFX_EINVAL, "pfx_page_copy: pool descriptor is NULL");
+  if (n < 0) return fail(PFX_ERANGE, "pfx_page_copy: n %d < 0", n);
+  if (n == 0) return PFX_OK;
+  if (!dst_pages || !src_pages || !ws) return fail(PFX_EINVAL, "pfx_page_copy: NULL argument");
+  if (dst->page_size != PFX_PAGE_SIZE || src->page_size != PFX_PAGE_SIZE)
+    return fail(PFX_EUNSUPPORTED, "pfx_page_copy: page_size must be %d", PFX_PAGE_SIZE);
+  if (dst->num_kv_heads != src->num_kv_heads || dst->head_dim != src->head_dim || dst->num_kv_heads < 1 ||
+      dst->head_dim < 8 || dst->head_dim % 8)
+    return fail(PFX_EINVAL, "pfx_page_copy: source and destination page formats differ");
+  if (!dst->k_pages || !dst->v_pages || !src->k_pages || !src->v_pages)
+    return fail(PFX_EINVAL, "pfx_page_copy: page pointers are NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % 256) return fail(PFX_EINVAL, "pfx_page_copy: workspace not 256-byte aligned");
+  if (ws_bytes < pfx_page_copy_workspace_bytes(n))
+    return fail(PFX_ENOMEM, "pfx_page_copy: workspace has %zu bytes, needs %zu", ws_bytes,
+                pfx_page_copy_workspace_bytes(n));
+  std::vector<int32_t> pairs(2 * size_t(n));
+  std::vector<uint8_t> seen(dst->num_pages, 0);
+  for (int32_t i = 0; i < n; ++i) {
+    if (dst_pages[i] < 0 || dst_pages[i] >= dst->num_pages)
+      return fail(PFX_ERANGE, "pfx_page_copy: dst_pages[%d] = %d outside [0, %d)", i, dst_pages[i], dst->num_pages);
+    if (src_pages[i] < 0 || src_pages[i] >= src->num_pages)
+      return fail(PFX_ERANGE, "pfx_page_copy: src_pages[%d] = %d outside [0, %d)", i, src_pages[i], src->num_pages);
+    if (seen[dst_pages[i]]) return fail(PFX_EINVAL, "pfx_page_copy: destination page %d repeated", dst_pages[i]);
+    seen[dst_pages[i]] = 1;
+    pairs[2 * i] = dst_pages[i];
+    pairs[2 * i + 1] = src_pages[i];
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = hipMemcpyAsync(ws, pairs.data(), pairs.size() * 4, hipMemcpyHostToDevice, s);
+  if (e != hipSuccess) return hip_fail(e, "pfx_page_copy: hipMemcpyAsync");
+  const size_t page_bytes = size_t(dst->num_kv_heads) * PFX_PAGE_SIZE * dst->head_dim * 2;
+  const size_t page_vecs = page_bytes / 16;
+  // gridDim.y is limited to 65535: launch the page list in slices.
+  for (int32_t at = 0; at < n; at += 65535) {
+    const int32_t cnt = std::min<int32_t>(65535, n - at);
+    const dim3 grid((page_vecs + 255) / 256, cnt, 2);
+    hipLaunchKernelGGL(page_copy_kernel, grid, dim3(256), 0, s, static_cast<const u32x4*>(src->k_pages),
+                       static_cast<const u32x4*>(src->v_pages), static_cast<u32x4*>(dst->k_pages),
+                       static_cast<u32x4*>(dst->v_pages), static_cast<const int32_t*>(ws) + 2 * size_t(at),
+                       page_vecs);
+    int rc = check_launch("pfx_page_copy");
+    if (rc) return rc;
+  }
+  return PFX_OK;
+}
+
+extern "C" int pfx_sync_check(void* stream) {
+  hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "pfx_sync_check");
+  e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "pfx_sync_check");
+  return PFX_OK;
+}

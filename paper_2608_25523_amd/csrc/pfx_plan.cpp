@@ -1,0 +1,498 @@
+// Host side of the library: errors, the page allocator, validation and the
+// plan builder.  No HIP calls live here, so this file also builds with g++
+// for host-only sanitizer runs.
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+
+#include "pfx_internal.h"
+
+namespace pfx {
+
+static thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+void clear_error() { g_err.clear(); }
+
+static size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+static int64_t pages_for(int64_t tokens) { return (tokens + PFX_PAGE_SIZE - 1) / PFX_PAGE_SIZE; }
+
+DevPlan dev_plan(const pfx_plan* p) {
+  unsigned char* base = static_cast<unsigned char*>(p->dev_ws);
+  DevPlan d;
+  d.items = reinterpret_cast<const Item*>(base + p->off_items);
+  d.row_tok = reinterpret_cast<const int32_t*>(base + p->off_row_tok);
+  d.page_list = reinterpret_cast<const int32_t*>(base + p->off_page_list);
+  d.tok_req = reinterpret_cast<const int32_t*>(base + p->off_tok_req);
+  d.req = reinterpret_cast<const ReqInfo*>(base + p->off_req);
+  d.tok_slot = reinterpret_cast<const int32_t*>(base + p->off_tok_slot);
+  d.counters = reinterpret_cast<int32_t*>(base + p->off_counters);
+  d.o_part = reinterpret_cast<float*>(base + p->off_opart);
+  d.l_part = reinterpret_cast<float*>(base + p->off_lpart);
+  return d;
+}
+
+}  // namespace pfx
+
+using pfx::fail;
+
+extern "C" int pfx_version(void) { return PFX_VERSION; }
+
+extern "C" const char* pfx_last_error(void) { return pfx::g_err.c_str(); }
+
+// ---------------------------------------------------------------------------
+// Page allocator
+// ---------------------------------------------------------------------------
+
+struct pfx_alloc {
+  int32_t num_pages = 0;
+  std::vector<int32_t> free_list;  // back() is handed out next
+  std::vector<uint8_t> used;
+};
+
+extern "C" int pfx_alloc_create(int32_t num_pages, pfx_alloc** out) {
+  if (!out) return fail(PFX_EINVAL, "pfx_alloc_create: out is NULL");
+  *out = nullptr;
+  if (num_pages < 0) return fail(PFX_ERANGE, "pfx_alloc_create: num_pages %d < 0", num_pages);
+  pfx_alloc* a = new (std::nothrow) pfx_alloc;
+  if (!a) return fail(PFX_ENOMEM, "pfx_alloc_create: host allocation failed");
+  a->num_pages = num_pages;
+  a->free_list.resize(num_pages);
+  for (int32_t i = 0; i < num_pages; ++i) a->free_list[i] = num_pages - 1 - i;
+  a->used.assign(num_pages, 0);
+  *out = a;
+  return PFX_OK;
+}
+
+extern "C" int pfx_alloc_pages(pfx_alloc* a, int32_t n, int32_t* out_ids) {
+  if (!a) return fail(PFX_EINVAL, "pfx_alloc_pages: allocator is NULL");
+  if (n < 0) return fail(PFX_ERANGE, "pfx_alloc_pages: n %d < 0", n);
+  if (n > 0 && !out_ids) return fail(PFX_EINVAL, "pfx_alloc_pages: out_ids is NULL");
+  if (static_cast<size_t>(n) > a->free_list.size())
+    return fail(PFX_ENOMEM, "pfx_alloc_pages: %d pages requested, %zu free", n, a->free_list.size());
+  for (int32_t i = 0; i < n; ++i) {
+    int32_t id = a->free_list.back();
+    a->free_list.pop_back();
+    a->used[id] = 1;
+    out_ids[i] = id;
+  }
+  return PFX_OK;
+}
+
+extern "C" int pfx_free_pages(pfx_alloc* a, const int32_t* ids, int32_t n) {
+  if (!a) return fail(PFX_EINVAL, "pfx_free_pages: allocator is NULL");
+  if (n < 0) return fail(PFX_ERANGE, "pfx_free_pages: n %d < 0", n);
+  if (n > 0 && !ids) return fail(PFX_EINVAL, "pfx_free_pages: ids is NULL");
+  std::vector<uint8_t> seen;
+  for (int32_t i = 0; i < n; ++i) {
+    int32_t id = ids[i];
+    if (id < 0 || id >= a->num_pages) return fail(PFX_EINVAL, "pfx_free_pages: id %d out of range", id);
+    if (!a->used[id]) return fail(PFX_EINVAL, "pfx_free_pages: page %d is not allocated", id);
+    if (seen.empty()) seen.assign(a->num_pages, 0);
+    if (seen[id]) return fail(PFX_EINVAL, "pfx_free_pages: page %d freed twice", id);
+    seen[id] = 1;
+  }
+  for (int32_t i = 0; i < n; ++i) {
+    a->used[ids[i]] = 0;
+    a->free_list.push_back(ids[i]);
+  }
+  return PFX_OK;
+}
+
+extern "C" int pfx_alloc_num_free(const pfx_alloc* a, int32_t* out) {
+  if (!a || !out) return fail(PFX_EINVAL, "pfx_alloc_num_free: NULL argument");
+  *out = static_cast<int32_t>(a->free_list.size());
+  return PFX_OK;
+}
+
+extern "C" void pfx_alloc_destroy(pfx_alloc* a) { delete a; }
+
+// ---------------------------------------------------------------------------
+// Plan
+// ---------------------------------------------------------------------------
+
+namespace {
+
+constexpr int32_t kDefaultPrefixChunk = 512;
+constexpr int32_t kDefaultSuffixChunk = 512;
+
+int check_pool_shape(const pfx_pool* pool, const char* who) {
+  if (!pool) return fail(PFX_EINVAL, "%s: pool is NULL", who);
+  if (pool->page_size != PFX_PAGE_SIZE)
+    return fail(PFX_EUNSUPPORTED, "%s: page_size %d (only %d is supported)", who, pool->page_size,
+                PFX_PAGE_SIZE);
+  if (pool->head_dim != 64 && pool->head_dim != 128)
+    return fail(PFX_EUNSUPPORTED, "%s: head_dim %d (64 or 128 supported)", who, pool->head_dim);
+  if (pool->num_kv_heads < 1) return fail(PFX_EINVAL, "%s: num_kv_heads %d < 1", who, pool->num_kv_heads);
+  if (pool->num_pages < 0) return fail(PFX_ERANGE, "%s: num_pages %d < 0", who, pool->num_pages);
+  return PFX_OK;
+}
+
+bool is_group_supported(int32_t g) { return g == 1 || g == 2 || g == 4 || g == 8 || g == 16; }
+
+}  // namespace
+
+extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt, const pfx_batch* b,
+                               int32_t hq, int32_t mode, const pfx_plan_opts* opts, pfx_plan** out) {
+  using namespace pfx;
+  if (!out) return fail(PFX_EINVAL, "pfx_plan_create: out is NULL");
+  *out = nullptr;
+  int rc = check_pool_shape(pool, "pfx_plan_create");
+  if (rc) return rc;
+  if (!pt || !b) return fail(PFX_EINVAL, "pfx_plan_create: prefix table or batch is NULL");
+  const int32_t hkv = pool->num_kv_heads;
+  if (hq < 1 || hq % hkv != 0)
+    return fail(PFX_EINVAL, "pfx_plan_create: num_q_heads %d is not a multiple of num_kv_heads %d", hq, hkv);
+  const int32_t G = hq / hkv;
+  if (!is_group_supported(G))
+    return fail(PFX_EUNSUPPORTED, "pfx_plan_create: query group %d (1, 2, 4, 8 or 16 supported)", G);
+  if (mode != PFX_MODE_EXTEND && mode != PFX_MODE_DECODE && mode != PFX_MODE_MIXED)
+    return fail(PFX_EINVAL, "pfx_plan_create: mode %d", mode);
+  int32_t pchunk = kDefaultPrefixChunk, schunk = kDefaultSuffixChunk;
+  if (opts) {
+    for (int i = 0; i < 6; ++i)
+      if (opts->reserved[i]) return fail(PFX_EINVAL, "pfx_plan_create: opts.reserved[%d] != 0", i);
+    if (opts->prefix_chunk < 0 || opts->prefix_chunk % kStepKeys)
+      return fail(PFX_EINVAL, "pfx_plan_create: prefix_chunk %d is not a multiple of %d", opts->prefix_chunk,
+                  kStepKeys);
+    if (opts->suffix_chunk < 0 || opts->suffix_chunk % kStepKeys)
+      return fail(PFX_EINVAL, "pfx_plan_create: suffix_chunk %d is not a multiple of %d", opts->suffix_chunk,
+                  kStepKeys);
+    if (opts->prefix_chunk) pchunk = opts->prefix_chunk;
+    if (opts->suffix_chunk) schunk = opts->suffix_chunk;
+  }
+
+  // ---- prefix table ----
+  const int32_t A = pt->num_agents;
+  if (A < 0) return fail(PFX_ERANGE, "pfx_plan_create: num_agents %d < 0", A);
+  if (A > 0 && (!pt->page_indptr || !pt->prefix_len))
+    return fail(PFX_EINVAL, "pfx_plan_create: prefix table arrays are NULL");
+  if (A > 0 && pt->page_indptr[0] != 0) return fail(PFX_EINVAL, "pfx_plan_create: page_indptr[0] != 0");
+  for (int32_t a = 0; a < A; ++a) {
+    if (pt->prefix_len[a] < 0) return fail(PFX_ERANGE, "pfx_plan_create: prefix_len[%d] = %d", a, pt->prefix_len[a]);
+    int64_t cnt = int64_t(pt->page_indptr[a + 1]) - pt->page_indptr[a];
+    if (cnt != pages_for(pt->prefix_len[a]))
+      return fail(PFX_EINVAL, "pfx_plan_create: agent %d has %lld pages for %d tokens (need %lld)", a,
+                  (long long)cnt, pt->prefix_len[a], (long long)pages_for(pt->prefix_len[a]));
+  }
+  if (A > 0 && pt->page_indptr[A] > 0 && !pt->page_ids)
+    return fail(PFX_EINVAL, "pfx_plan_create: page_ids is NULL");
+
+  // ---- batch ----
+  const int32_t R = b->num_reqs;
+  if (R < 0) return fail(PFX_ERANGE, "pfx_plan_create: num_reqs %d < 0", R);
+  if (R > 0 && (!b->agent || !b->suffix_indptr || !b->suffix_len || !b->q_indptr))
+    return fail(PFX_EINVAL, "pfx_plan_create: batch arrays are NULL");
+  if (R > 0 && (b->suffix_indptr[0] != 0 || b->q_indptr[0] != 0))
+    return fail(PFX_EINVAL, "pfx_plan_create: suffix_indptr[0] and q_indptr[0] must be 0");
+  int64_t total_tokens = 0;
+  for (int32_t r = 0; r < R; ++r) {
+    int32_t L = b->suffix_len[r];
+    if (L < 0) return fail(PFX_ERANGE, "pfx_plan_create: suffix_len[%d] = %d", r, L);
+    int64_t cnt = int64_t(b->suffix_indptr[r + 1]) - b->suffix_indptr[r];
+    if (cnt != pages_for(L))
+      return fail(PFX_EINVAL, "pfx_plan_create: request %d has %lld suffix pages for %d tokens", r, (long long)cnt, L);
+    int64_t n = int64_t(b->q_indptr[r + 1]) - b->q_indptr[r];
+    if (n < 0) return fail(PFX_EINVAL, "pfx_plan_create: q_indptr decreases at request %d", r);
+    if (n > L) return fail(PFX_ERANGE, "pfx_plan_create: request %d has %lld query rows but suffix_len %d", r, (long long)n, L);
+    if (mode == PFX_MODE_DECODE && n > 1)
+      return fail(PFX_EINVAL, "pfx_plan_create: decode mode but request %d has %lld query rows", r, (long long)n);
+    int32_t a = b->agent[r];
+    if (a < -1 || a >= A) return fail(PFX_ERANGE, "pfx_plan_create: agent[%d] = %d (num_agents %d)", r, a, A);
+    total_tokens += n;
+  }
+  if (total_tokens > (int64_t(1) << 30)) return fail(PFX_ERANGE, "pfx_plan_create: too many query rows");
+  if (R > 0 && b->suffix_indptr[R] > 0 && !b->suffix_page_ids)
+    return fail(PFX_EINVAL, "pfx_plan_create: suffix_page_ids is NULL");
+
+  // ---- Sec. 3, Eq. (2): prefixes counted once, plus every request's own KV ----
+  std::vector<uint8_t> referenced(A, 0);
+  for (int32_t r = 0; r < R; ++r)
+    if (b->agent[r] >= 0) referenced[b->agent[r]] = 1;
+  int64_t need = 0;
+  for (int32_t a = 0; a < A; ++a)
+    if (referenced[a]) need += pages_for(pt->prefix_len[a]);
+  for (int32_t r = 0; r < R; ++r) need += pages_for(b->suffix_len[r]);
+  if (need > pool->num_pages)
+    return fail(PFX_ENOMEM, "pfx_plan_create: batch needs %lld pages (prefixes once + suffixes), pool has %d",
+                (long long)need, pool->num_pages);
+
+  // ---- page ids: in range and owned exactly once ----
+  std::vector<uint8_t> owner(pool->num_pages, 0);
+  auto claim = [&](int32_t id, const char* what, int32_t who) -> int {
+    if (id < 0 || id >= pool->num_pages)
+      return fail(PFX_ERANGE, "pfx_plan_create: %s %d uses page %d outside [0, %d)", what, who, id, pool->num_pages);
+    if (owner[id]) return fail(PFX_EINVAL, "pfx_plan_create: page %d is used twice (%s %d)", id, what, who);
+    owner[id] = 1;
+    return PFX_OK;
+  };
+  for (int32_t a = 0; a < A; ++a) {
+    if (!referenced[a]) continue;
+    for (int32_t i = pt->page_indptr[a]; i < pt->page_indptr[a + 1]; ++i)
+      if ((rc = claim(pt->page_ids[i], "agent", a))) return rc;
+  }
+  for (int32_t r = 0; r < R; ++r)
+    for (int32_t i = b->suffix_indptr[r]; i < b->suffix_indptr[r + 1]; ++i)
+      if ((rc = claim(b->suffix_page_ids[i], "request", r))) return rc;
+
+  // ---- build ----
+  pfx_plan* p = new (std::nothrow) pfx_plan;
+  if (!p) return fail(PFX_ENOMEM, "pfx_plan_create: host allocation failed");
+  p->num_pages = pool->num_pages;
+  p->hkv = hkv;
+  p->d = pool->head_dim;
+  p->hq = hq;
+  p->group = G;
+  p->mode = mode;
+  p->num_reqs = R;
+  p->num_tokens = static_cast<int32_t>(total_tokens);
+  p->pages_needed = static_cast<int32_t>(need);
+
+  std::vector<int32_t> prefix_off(A, -1), suffix_off(R, 0);
+  for (int32_t a = 0; a < A; ++a) {
+    if (!referenced[a]) continue;
+    prefix_off[a] = static_cast<int32_t>(p->page_list.size());
+    p->page_list.insert(p->page_list.end(), pt->page_ids + pt->page_indptr[a], pt->page_ids + pt->page_indptr[a + 1]);
+  }
+  for (int32_t r = 0; r < R; ++r) {
+    suffix_off[r] = static_cast<int32_t>(p->page_list.size());
+    p->page_list.insert(p->page_list.end(), b->suffix_page_ids + b->suffix_indptr[r],
+                        b->suffix_page_ids + b->suffix_indptr[r + 1]);
+  }
+  p->tok_req.resize(total_tokens);
+  p->tok_slot.resize(total_tokens);
+  p->req.resize(R);
+  for (int32_t r = 0; r < R; ++r) {
+    const int32_t q0 = b->q_indptr[r], n = b->q_indptr[r + 1] - q0, L = b->suffix_len[r];
+    p->req[r] = ReqInfo{q0, n, 0, 0};
+    for (int32_t i = 0; i < n; ++i) {
+      int32_t pos = L - n + i;
+      int32_t page = b->suffix_page_ids[b->suffix_indptr[r] + pos / PFX_PAGE_SIZE];
+      p->tok_req[q0 + i] = r;
+      p->tok_slot[q0 + i] = page * PFX_PAGE_SIZE + pos % PFX_PAGE_SIZE;
+    }
+  }
+
+  const int32_t max_cols = kTileCols * kMaxBlocks;
+  auto is_decode_class = [&](int32_t r) {
+    int32_t n = p->req[r].n;
+    return n >= 1 && n * G <= kTileCols;
+  };
+  auto nchunks = [](int32_t len, int32_t chunk) { return len <= 0 ? 0 : (len + chunk - 1) / chunk; };
+  auto blocks_for = [&](int32_t tokens) { return (tokens * G + kTileCols - 1) / kTileCols; };
+
+  std::vector<Item> items;
+  std::vector<int32_t> prefix_chunks(R, 0);
+
+  // Grouped decode over each agent's prefix: the agent's decode rows are
+  // packed into items of up to 64 query columns; every prefix chunk is read
+  // once per (row block, KV head) and shared by all the rows in the block.
+  for (int32_t a = 0; a < A; ++a) {
+    if (!referenced[a]) continue;
+    const int32_t P = pt->prefix_len[a];
+    std::vector<int32_t> members;
+    for (int32_t r = 0; r < R; ++r)
+      if (b->agent[r] == a && is_decode_class(r)) members.push_back(r);
+    if (members.empty() || P == 0) continue;
+    const int32_t nc = nchunks(P, pchunk);
+    struct RowBlock { int32_t begin, tokens; };
+    std::vector<RowBlock> blocks;
+    int32_t cols = max_cols;  // forces a new block at the first member
+    for (int32_t r : members) {
+      int32_t n = p->req[r].n;
+      if (cols + n * G > max_cols) {
+        blocks.push_back(RowBlock{static_cast<int32_t>(p->row_tok.size()), 0});
+        cols = 0;
+      }
+      for (int32_t i = 0; i < n; ++i) p->row_tok.push_back(p->req[r].q_start + i);
+      blocks.back().tokens += n;
+      cols += n * G;
+      prefix_chunks[r] = nc;
+    }
+    for (int32_t c = 0; c < nc; ++c)
+      for (int32_t h = 0; h < hkv; ++h)
+        for (const RowBlock& rb : blocks) {
+          Item it{};
+          it.kv_head = h;
+          it.row_begin = rb.begin;
+          it.row_count = rb.tokens;
+          it.nblk = blocks_for(rb.tokens);
+          it.s0_page_off = prefix_off[a];
+          it.s0_kbeg = c * pchunk;
+          it.s0_kend = std::min(P, (c + 1) * pchunk);
+          it.s1_page_off = 0;
+          it.s1_kbeg = it.s1_kend = 0;
+          it.causal_base = 0;
+          it.out_slot = c;
+          it.kind = kPrefixItem;
+          it.req = -1;
+          items.push_back(it);
+          ++p->n_prefix_items;
+        }
+  }
+
+  // Decode rows against each request's own suffix, in chunks.
+  int64_t part_rows = 0;
+  for (int32_t r = 0; r < R; ++r) {
+    if (!is_decode_class(r)) continue;
+    const ReqInfo ri = p->req[r];
+    const int32_t L = b->suffix_len[r];
+    const int32_t ns = nchunks(L, schunk);
+    const int32_t nparts = prefix_chunks[r] + ns;
+    p->req[r].nparts = nparts;
+    if (nparts > 1) {
+      p->req[r].part_base = static_cast<int32_t>(part_rows);
+      part_rows += int64_t(nparts) * ri.n;
+    }
+    const int32_t rb = static_cast<int32_t>(p->row_tok.size());
+    for (int32_t i = 0; i < ri.n; ++i) p->row_tok.push_back(ri.q_start + i);
+    for (int32_t j = 0; j < ns; ++j)
+      for (int32_t h = 0; h < hkv; ++h) {
+        Item it{};
+        it.kv_head = h;
+        it.row_begin = rb;
+        it.row_count = ri.n;
+        it.nblk = 1;
+        it.s0_page_off = 0;
+        it.s0_kbeg = it.s0_kend = 0;
+        it.s1_page_off = suffix_off[r];
+        it.s1_kbeg = j * schunk;
+        it.s1_kend = std::min(L, (j + 1) * schunk);
+        it.causal_base = L - ri.n - ri.q_start;
+        it.out_slot = nparts > 1 ? prefix_chunks[r] + j : -1;
+        it.kind = kSuffixItem;
+        it.req = r;
+        items.push_back(it);
+        ++p->n_suffix_items;
+      }
+  }
+
+  // Extend rows: blocks of up to 64 query columns of one request, over the
+  // whole prefix (no mask) then the suffix (causal).  Written directly.
+  for (int32_t r = 0; r < R; ++r) {
+    const ReqInfo ri = p->req[r];
+    if (ri.n == 0 || is_decode_class(r)) continue;
+    p->req[r].nparts = 1;
+    const int32_t a = b->agent[r];
+    const int32_t P = a >= 0 ? pt->prefix_len[a] : 0;
+    const int32_t L = b->suffix_len[r];
+    const int32_t per = max_cols / G;
+    for (int32_t i0 = 0; i0 < ri.n; i0 += per) {
+      const int32_t i1 = std::min(ri.n, i0 + per);
+      const int32_t rbeg = static_cast<int32_t>(p->row_tok.size());
+      for (int32_t i = i0; i < i1; ++i) p->row_tok.push_back(ri.q_start + i);
+      for (int32_t h = 0; h < hkv; ++h) {
+        Item it{};
+        it.kv_head = h;
+        it.row_begin = rbeg;
+        it.row_count = i1 - i0;
+        it.nblk = blocks_for(i1 - i0);
+        it.s0_page_off = P > 0 ? prefix_off[a] : 0;
+        it.s0_kbeg = 0;
+        it.s0_kend = P;
+        it.s1_page_off = suffix_off[r];
+        it.s1_kbeg = 0;
+        it.s1_kend = L - ri.n + i1;
+        it.causal_base = L - ri.n - ri.q_start;
+        it.out_slot = -1;
+        it.kind = kExtendItem;
+        it.req = r;
+        items.push_back(it);
+        ++p->n_extend_items;
+      }
+    }
+  }
+  if (part_rows > (int64_t(1) << 31) / std::max(1, hq))
+    return delete p, fail(PFX_ERANGE, "pfx_plan_create: too many partial rows");
+  p->num_part_rows = part_rows;
+
+  // Wide items (several 16-column blocks) first, narrow ones after; inside
+  // each class the longest key ranges go first so the tail stays short.
+  auto cost = [](const Item& it) { return (it.s0_kend - it.s0_kbeg) + (it.s1_kend - it.s1_kbeg); };
+  std::stable_sort(items.begin(), items.end(), [&](const Item& x, const Item& y) {
+    bool wx = x.nblk > 1, wy = y.nblk > 1;
+    if (wx != wy) return wx;
+    return cost(x) > cost(y);
+  });
+  p->n_items_wide = static_cast<int32_t>(std::count_if(items.begin(), items.end(), [](const Item& it) { return it.nblk > 1; }));
+  p->items = std::move(items);
+
+  // ---- workspace layout ----
+  size_t off = 0;
+  p->off_items = off;      off = align256(off + p->items.size() * sizeof(Item));
+  p->off_row_tok = off;    off = align256(off + p->row_tok.size() * 4);
+  p->off_page_list = off;  off = align256(off + p->page_list.size() * 4);
+  p->off_tok_req = off;    off = align256(off + p->tok_req.size() * 4);
+  p->off_req = off;        off = align256(off + p->req.size() * sizeof(ReqInfo));
+  p->off_tok_slot = off;   off = align256(off + p->tok_slot.size() * 4);
+  p->blob_bytes = off;
+  p->off_counters = off;   off = align256(off + size_t(R) * hkv * 4);
+  p->off_opart = off;      off = align256(off + size_t(part_rows) * hq * p->d * 4);
+  p->off_lpart = off;      off = align256(off + size_t(part_rows) * hq * 4);
+  p->total_bytes = std::max<size_t>(off, 256);
+
+  p->blob.assign(p->blob_bytes, 0);
+  auto put = [&](size_t at, const void* src, size_t bytes) {
+    if (bytes) std::memcpy(p->blob.data() + at, src, bytes);
+  };
+  put(p->off_items, p->items.data(), p->items.size() * sizeof(Item));
+  put(p->off_row_tok, p->row_tok.data(), p->row_tok.size() * 4);
+  put(p->off_page_list, p->page_list.data(), p->page_list.size() * 4);
+  put(p->off_tok_req, p->tok_req.data(), p->tok_req.size() * 4);
+  put(p->off_req, p->req.data(), p->req.size() * sizeof(ReqInfo));
+  put(p->off_tok_slot, p->tok_slot.data(), p->tok_slot.size() * 4);
+
+  *out = p;
+  return PFX_OK;
+}
+
+extern "C" int pfx_plan_workspace_bytes(const pfx_plan* p, size_t* bytes) {
+  if (!p || !bytes) return fail(PFX_EINVAL, "pfx_plan_workspace_bytes: NULL argument");
+  *bytes = p->total_bytes;
+  return PFX_OK;
+}
+
+extern "C" int pfx_plan_get_stats(const pfx_plan* p, pfx_plan_stats* s) {
+  if (!p || !s) return fail(PFX_EINVAL, "pfx_plan_get_stats: NULL argument");
+  s->num_requests = p->num_reqs;
+  s->num_tokens = p->num_tokens;
+  s->num_items = static_cast<int32_t>(p->items.size());
+  s->num_prefix_items = p->n_prefix_items;
+  s->num_suffix_items = p->n_suffix_items;
+  s->num_extend_items = p->n_extend_items;
+  s->num_partial_rows = static_cast<int32_t>(p->num_part_rows);
+  s->pages_needed = p->pages_needed;
+  s->workspace_bytes = static_cast<int64_t>(p->total_bytes);
+  return PFX_OK;
+}
+
+extern "C" int pfx_plan_export(const pfx_plan* p, int32_t which, int32_t* out, int64_t cap, int64_t* count) {
+  if (!p || !count) return fail(PFX_EINVAL, "pfx_plan_export: NULL argument");
+  const int32_t* src = nullptr;
+  int64_t n = 0;
+  switch (which) {
+    case 0: src = reinterpret_cast<const int32_t*>(p->items.data()); n = int64_t(p->items.size()) * 16; break;
+    case 1: src = p->row_tok.data(); n = int64_t(p->row_tok.size()); break;
+    case 2: src = p->page_list.data(); n = int64_t(p->page_list.size()); break;
+    default: return fail(PFX_EINVAL, "pfx_plan_export: which = %d", which);
+  }
+  *count = n;
+  if (cap > 0 && !out) return fail(PFX_EINVAL, "pfx_plan_export: out is NULL");
+  int64_t m = std::min(n, std::max<int64_t>(cap, 0));
+  if (m) std::memcpy(out, src, size_t(m) * 4);
+  return PFX_OK;
+}
+
+extern "C" void pfx_plan_destroy(pfx_plan* p) { delete p; }

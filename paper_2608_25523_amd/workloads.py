@@ -317,3 +317,33 @@ def host_values_fast(batch: Batch, seed: int) -> HostValues:
     kn = _normal_bf16(rng, (t, hkv, d))
     vn = _normal_bf16(rng, (t, hkv, d))
     return HostValues(pages, kp, vp, q, kn, vn)
+
+
+def replicas(batch: Batch, count: int, seed: int) -> list:
+    """``count`` copies of a batch's lengths and agents whose pages are
+    pairwise disjoint within the same pool (replica 0 is ``batch`` itself).
+    Used to rotate the benchmark over a working set larger than the GPU's
+    last-level cache."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    used = set(int(p) for p in batch.used_pages())
+    free = np.array([p for p in range(batch.num_pages) if p not in used], np.int32)
+    free = free[rng.permutation(len(free))]
+    out = [batch]
+    at = 0
+    per = len(batch.used_pages())
+    for _ in range(count - 1):
+        if at + per > len(free):
+            break
+        take = free[at:at + per]
+        at += per
+        k = 0
+        pp, sp = [], []
+        for pl in batch.prefix_pages:
+            pp.append(take[k:k + len(pl)].copy())
+            k += len(pl)
+        for pl in batch.suffix_pages:
+            sp.append(take[k:k + len(pl)].copy())
+            k += len(pl)
+        out.append(Batch(batch.num_q_heads, batch.num_kv_heads, batch.head_dim, batch.num_pages, batch.prefix_len,
+                         pp, batch.agent, batch.suffix_len, batch.n_rows, sp, dict(batch.meta, replica=len(out))))
+    return out

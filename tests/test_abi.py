@@ -1,0 +1,288 @@
+"""Host-side tests of the C interface: no GPU needed (no kernel is launched).
+
+The library is loaded, every function the header declares is exported, the
+allocator and the plan builder are exercised, every validation error code is
+reached, and the work list is checked to cover each visible (query row,
+head, key) triple exactly once.
+"""
+
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2608_25523_amd import binding as B
+from paper_2608_25523_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "pfx_attn.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pfx_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    names = header_functions()
+    assert len(names) >= 19
+    lib = C.CDLL(B.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(B.EXPORTED)
+
+
+def test_version_and_error_text():
+    assert B.pfx_version() == 10000
+    with pytest.raises(B.PfxError):
+        B.Allocator(-1)
+    assert "num_pages" in B.pfx_last_error()
+
+
+def test_allocator_is_lifo_and_checks():
+    a = B.Allocator(5)
+    assert list(a.alloc(3)) == [0, 1, 2]
+    assert a.num_free() == 2
+    a.free([1, 0])
+    assert list(a.alloc(2)) == [0, 1]          # last freed comes back first
+    with pytest.raises(B.PfxError) as e:
+        a.alloc(4)
+    assert e.value.code == B.PFX_ENOMEM
+    assert a.num_free() == 2                    # nothing handed out on failure
+    for bad in ([7], [3], [0, 0]):
+        with pytest.raises(B.PfxError) as e:
+            a.free(bad)
+        assert e.value.code == B.PFX_EINVAL
+    assert a.num_free() == 2
+
+
+def small_batch(**over):
+    kw = dict(num_q_heads=8, num_kv_heads=2, head_dim=64, num_pages=64, prefix_len=[40, 17],
+              agent=[0, 1, 0, -1, 1], suffix_len=[5, 20, 33, 3, 16], n_rows=[1, 1, 33, 3, 2])
+    kw.update(over)
+    return W.make_batch(11, **kw)
+
+
+def plan_for(batch, pool=None, mode=B.PFX_MODE_MIXED, **kw):
+    pool = pool or B.make_pool(batch.num_pages, batch.num_kv_heads, batch.head_dim)
+    return B.plan_from_batch(pool, batch, mode, **kw)
+
+
+def expect_error(code, fn):
+    with pytest.raises(B.PfxError) as e:
+        fn()
+    assert e.value.code == code, str(e.value)
+    return str(e.value)
+
+
+def raw_create(batch, pind=None, pids=None, plen=None, agent=None, sind=None, sids=None, slen=None, qind=None,
+               hq=None, mode=B.PFX_MODE_MIXED, pool=None, **kw):
+    a_pind, a_pids, a_plen = batch.prefix_csr()
+    a_sind, a_sids = batch.suffix_csr()
+    pool = pool or B.make_pool(batch.num_pages, batch.num_kv_heads, batch.head_dim)
+    return B.pfx_plan_create(pool,
+                             a_pind if pind is None else pind, a_pids if pids is None else pids,
+                             a_plen if plen is None else plen, batch.agent if agent is None else agent,
+                             a_sind if sind is None else sind, a_sids if sids is None else sids,
+                             batch.suffix_len if slen is None else slen,
+                             batch.q_indptr() if qind is None else qind,
+                             batch.num_q_heads if hq is None else hq, mode, **kw)
+
+
+def test_plan_validation_error_codes():
+    b = small_batch()
+    raw_create(b)  # valid
+    pool = lambda **o: B.pfx_pool(o.get("n", 64), o.get("ps", 16), o.get("hkv", 2), o.get("d", 64), None, None)
+    expect_error(B.PFX_EUNSUPPORTED, lambda: raw_create(b, pool=pool(ps=32)))
+    expect_error(B.PFX_EUNSUPPORTED, lambda: raw_create(b, pool=pool(d=96)))
+    expect_error(B.PFX_EINVAL, lambda: raw_create(b, hq=7))                    # Hq % Hkv != 0
+    expect_error(B.PFX_EUNSUPPORTED, lambda: raw_create(b, hq=6))              # G = 3
+    expect_error(B.PFX_EINVAL, lambda: raw_create(b, mode=7))
+    expect_error(B.PFX_EINVAL, lambda: raw_create(b, mode=B.PFX_MODE_DECODE))  # request with 33 rows
+    expect_error(B.PFX_EINVAL, lambda: raw_create(b, prefix_chunk=48))
+    # Eq. (2): pool of 10 pages cannot hold 3 + 2 prefix pages and 1+2+3+1+1 suffix pages
+    msg = expect_error(B.PFX_ENOMEM, lambda: raw_create(b, pool=pool(n=12)))
+    assert "13 pages" in msg
+    sids = b.suffix_csr()[1].copy()
+    sids[0] = 64
+    expect_error(B.PFX_ERANGE, lambda: raw_create(b, sids=sids))               # page id out of range
+    sids = b.suffix_csr()[1].copy()
+    sids[1] = b.prefix_pages[0][0]
+    expect_error(B.PFX_EINVAL, lambda: raw_create(b, sids=sids))               # prefix page reused as suffix
+    sids = b.suffix_csr()[1].copy()
+    sids[2] = sids[1]
+    expect_error(B.PFX_EINVAL, lambda: raw_create(b, sids=sids))               # page owned twice
+    expect_error(B.PFX_ERANGE, lambda: raw_create(b, agent=[0, 2, 0, -1, 1]))  # no agent 2
+    expect_error(B.PFX_ERANGE, lambda: raw_create(b, agent=[0, 1, 0, -2, 1]))
+    slen = b.suffix_len.copy(); slen[3] = 2
+    expect_error(B.PFX_ERANGE, lambda: raw_create(b, slen=slen))               # 3 rows but L = 2
+    slen = b.suffix_len.copy(); slen[0] = 40
+    expect_error(B.PFX_EINVAL, lambda: raw_create(b, slen=slen))               # page count != ceil(L/16)
+    plen = np.array([40, 33], np.int32)
+    expect_error(B.PFX_EINVAL, lambda: raw_create(b, plen=plen))
+    qind = b.q_indptr().copy(); qind[0] = 1
+    expect_error(B.PFX_EINVAL, lambda: raw_create(b, qind=qind))
+    plen = np.array([40, -1], np.int32)
+    expect_error(B.PFX_ERANGE, lambda: raw_create(b, plen=plen))
+
+
+def test_unreferenced_agent_pages_are_ignored():
+    # Agent 1 has no request: its (possibly stale) pages are not validated or counted.
+    b = small_batch(agent=[0, 0, 0, -1, 0])
+    _, pids, _ = b.prefix_csr()
+    pids = pids.copy()
+    pids[-1] = 10_000
+    p = raw_create(b, pids=pids)
+    assert p.stats().pages_needed == 3 + (1 + 2 + 3 + 1 + 1)
+
+
+def test_empty_batch_and_zero_row_requests():
+    b = small_batch(agent=[], suffix_len=[], n_rows=[])
+    p = plan_for(b)
+    s = p.stats()
+    assert (s.num_items, s.num_tokens, s.num_requests) == (0, 0, 0)
+    b = small_batch(n_rows=[0, 0, 0, 0, 0])
+    s = plan_for(b).stats()
+    assert s.num_items == 0 and s.num_requests == 5
+
+
+def enumerate_coverage(plan, batch):
+    """Count, from the exported work list, how often each (token, q head,
+    logical key) triple is attended, and by how many partial slots."""
+    items = plan.export(0)
+    row_tok = plan.export(1)
+    page_list = plan.export(2)
+    G = batch.group
+    q_indptr = batch.q_indptr()
+    tok_req = np.repeat(np.arange(len(batch.agent)), batch.n_rows)
+    counts = {}
+    slots = {}
+    for it in items:
+        (h, rb, rc, nblk, s0p, s0b, s0e, s1p, s1b, s1e, cbase, slot, kind, req, _, _) = it
+        assert 1 <= nblk <= 4 and rc * G <= nblk * 16 and (rc * G > (nblk - 1) * 16)
+        for j in range(rc):
+            tok = int(row_tok[rb + j])
+            r = int(tok_req[tok])
+            a = int(batch.agent[r])
+            plen = int(batch.prefix_len[a]) if a >= 0 else 0
+            n, L = int(batch.n_rows[r]), int(batch.suffix_len[r])
+            pos_in_suffix = L - n + (tok - q_indptr[r])
+            for g in range(G):
+                qh = h * G + g
+                for k in range(s0b, s0e):
+                    page = int(page_list[s0p + k // 16])
+                    assert page == int(batch.prefix_pages[a][k // 16])
+                    counts[(tok, qh, k)] = counts.get((tok, qh, k), 0) + 1
+                for k in range(s1b, s1e):
+                    page = int(page_list[s1p + k // 16])
+                    assert page == int(batch.suffix_pages[r][k // 16])
+                    if k <= tok + cbase:
+                        assert tok + cbase == pos_in_suffix
+                        counts[(tok, qh, plen + k)] = counts.get((tok, qh, plen + k), 0) + 1
+                slots.setdefault((tok, qh), set()).add(int(slot))
+    return counts, slots
+
+
+@pytest.mark.parametrize("case", ["small", "small_chunks", "g1", "g16", "decode_only"])
+def test_plan_covers_every_visible_key_once(case):
+    if case == "small":
+        b, kw = small_batch(), {}
+    elif case == "small_chunks":
+        b, kw = small_batch(prefix_len=[100, 17], suffix_len=[70, 20, 33, 3, 40]), dict(prefix_chunk=32, suffix_chunk=32)
+    elif case == "g1":
+        b, kw = small_batch(num_q_heads=2), {}
+    elif case == "g16":
+        b, kw = small_batch(num_q_heads=32, n_rows=[1, 1, 33, 1, 1]), dict(prefix_chunk=32)
+    else:
+        agents = np.arange(70) % 3 - 1
+        b = W.make_batch(5, num_q_heads=8, num_kv_heads=2, head_dim=128, num_pages=512, prefix_len=[64, 300],
+                         agent=agents, suffix_len=(np.arange(70) % 40) + 1, n_rows=np.ones(70, np.int32))
+        kw = dict(prefix_chunk=64, suffix_chunk=32)
+    p = plan_for(b, **kw)
+    counts, slots = enumerate_coverage(p, b)
+    G = b.group
+    q_indptr = b.q_indptr()
+    expected = 0
+    for r in range(len(b.agent)):
+        a = int(b.agent[r])
+        plen = int(b.prefix_len[a]) if a >= 0 else 0
+        n, L = int(b.n_rows[r]), int(b.suffix_len[r])
+        for i in range(n):
+            tok = int(q_indptr[r]) + i
+            vis = plen + L - n + i + 1
+            for qh in range(b.num_q_heads):
+                for k in range(vis):
+                    assert counts.get((tok, qh, k), 0) == 1, (tok, qh, k)
+                expected += vis
+    assert sum(counts.values()) == expected            # nothing invisible is attended
+    # Each row's partial slots are 0 .. nparts-1 (or the single direct slot -1).
+    for (tok, qh), ss in slots.items():
+        assert ss == {-1} or ss == set(range(len(ss))), (tok, qh, ss)
+
+
+def test_plan_is_deterministic_and_placement_independent():
+    b = W.config_batch(2)
+    p1, p2 = plan_for(b), plan_for(b)
+    np.testing.assert_array_equal(p1.export(0), p2.export(0))
+    # Same lengths, different page placement: same work list apart from page ids.
+    b2 = W.make_batch(777, num_q_heads=b.num_q_heads, num_kv_heads=b.num_kv_heads, head_dim=b.head_dim,
+                      num_pages=b.num_pages, prefix_len=b.prefix_len, agent=b.agent, suffix_len=b.suffix_len,
+                      n_rows=b.n_rows)
+    p3 = plan_for(b2)
+    np.testing.assert_array_equal(p1.export(0), p3.export(0))
+    np.testing.assert_array_equal(p1.export(1), p3.export(1))
+    assert not np.array_equal(p1.export(2), p3.export(2))
+
+
+def test_config_plans_build_and_group_prefixes():
+    for cfg in (1, 2, 3, 4, 5):
+        b = W.config_batch(cfg)
+        s = plan_for(b).stats()
+        assert s.num_tokens == b.num_tokens
+        assert s.pages_needed <= b.num_pages
+        if cfg == 2:
+            # 4 agents x 8 KV heads x 4 chunks of 512 keys, one 64-column row block each
+            assert s.num_prefix_items == 4 * 8 * 4
+            assert s.num_suffix_items == 64 * 8
+            assert s.num_extend_items == 0
+        if cfg == 3:
+            assert s.num_prefix_items == 0 and s.num_suffix_items == 0
+            assert s.num_extend_items == sum((int(n) + 15) // 16 for n in b.n_rows) * 8
+
+
+def test_upload_rejects_small_workspace_without_gpu_work():
+    b = small_batch()
+    p = plan_for(b)
+    need = p.workspace_bytes()
+    rc = B.LIB.pfx_plan_upload(p.h, C.c_void_p(256), need - 1, None)
+    assert rc == B.PFX_ENOMEM
+    rc = B.LIB.pfx_plan_upload(p.h, C.c_void_p(100), need, None)
+    assert rc == B.PFX_EINVAL
+
+
+def test_device_calls_validate_before_launch():
+    b = small_batch()
+    pool = B.make_pool(b.num_pages, b.num_kv_heads, b.head_dim)
+    p = plan_for(b, pool=pool)
+    # not uploaded yet -> EINVAL, nothing launched
+    rc = B.LIB.pfx_attention(C.byref(pool), p.h, None, None, None, C.c_float(0), None)
+    assert rc == B.PFX_EINVAL
+    other = B.pfx_pool(b.num_pages, 16, b.num_kv_heads, 128, 1, 1)
+    assert B.LIB.pfx_append_kv(C.byref(other), p.h, None, None, None) == B.PFX_EINVAL
+    assert "shape" in B.pfx_last_error()
+    assert B.LIB.pfx_merge_states(None, None, 1, 1, 128, None, None, None) == B.PFX_EINVAL
+    assert B.LIB.pfx_merge_states(C.c_void_p(8), C.c_void_p(8), 0, 1, 128, C.c_void_p(8), None, None) == B.PFX_ERANGE
+    src = B.pfx_pool(4, 16, 2, 64, 8, 8)
+    dst = B.pfx_pool(6, 16, 2, 64, 8, 8)
+    ids = (C.c_int32 * 2)(0, 6)
+    srcs = (C.c_int32 * 2)(0, 1)
+    ws = C.c_void_p(256)
+    assert B.LIB.pfx_page_copy(C.byref(dst), C.byref(src), ids, srcs, 2, ws, 4096, None) == B.PFX_ERANGE
+    ids = (C.c_int32 * 2)(3, 3)
+    assert B.LIB.pfx_page_copy(C.byref(dst), C.byref(src), ids, srcs, 2, ws, 4096, None) == B.PFX_EINVAL
+    ids = (C.c_int32 * 2)(3, 4)
+    assert B.LIB.pfx_page_copy(C.byref(dst), C.byref(src), ids, srcs, 2, ws, 16, None) == B.PFX_ENOMEM
+    bad = B.pfx_pool(6, 16, 2, 128, 8, 8)
+    assert B.LIB.pfx_page_copy(C.byref(bad), C.byref(src), ids, srcs, 2, ws, 4096, None) == B.PFX_EINVAL

@@ -1,0 +1,332 @@
+"""GPU parity: the HIP path through the C interface against the fp64 oracle.
+
+Every test here needs an MI355X and the built library; the binding fails
+loudly without it.  Each test prints the case it is about to run.
+"""
+
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+import oracle  # noqa: E402
+from paper_2608_25523_amd import binding as B  # noqa: E402
+from paper_2608_25523_amd import runner as RN  # noqa: E402
+from paper_2608_25523_amd import workloads as W  # noqa: E402
+import parity as PT  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+def announce(msg):
+    print(f"\n[gpu-case] {msg}", flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    yield
+    torch.cuda.synchronize()
+
+
+def run_and_check(batch, hv, label, rows=None, host_resident=(), check_pages=True, **kw):
+    announce(f"{label}: tokens={batch.num_tokens} reqs={len(batch.agent)} Hq={batch.num_q_heads} "
+             f"Hkv={batch.num_kv_heads} d={batch.head_dim} pool={batch.num_pages} {kw}")
+    ds = RN.DeviceStep(batch, hv, host_resident=host_resident, **kw)
+    ds.gather_evicted()
+    ds.step()
+    B.pfx_sync_check()
+    o_bits, lse = ds.outputs()
+    exp_k, exp_v = PT.expected_pools(batch, hv)
+    if check_pages:
+        gk, gv = ds.read_pages(hv.pages)
+        assert np.array_equal(gk, exp_k), f"{label}: K pool differs from the oracle's append"
+        assert np.array_equal(gv, exp_v), f"{label}: V pool differs from the oracle's append"
+    o_ref, l_ref = PT.reference(batch, hv, (exp_k, exp_v), rows=rows)
+    res = PT.compare(batch, o_bits, lse, o_ref, l_ref, label)
+    announce(f"{label}: max_abs={res[0]:.2e} rel={res[1]:.2e} lse={res[2]:.2e}")
+    return ds, o_bits, lse
+
+
+# --------------------------------------------------------------------------- merge and copy
+
+@pytest.mark.parametrize("d,parts,rows", [(128, 1, 7), (128, 3, 50), (64, 37, 33), (128, 200, 5)])
+def test_merge_states_matches_oracle(d, parts, rows):
+    announce(f"merge d={d} parts={parts} rows={rows}")
+    rng = np.random.default_rng(parts * 100 + rows)
+    o_parts = rng.standard_normal((parts, rows, d)).astype(np.float32)
+    lse_parts = (rng.standard_normal((parts, rows)) * 4).astype(np.float32)
+    lse_parts[0, 0] = -np.inf if parts > 1 else lse_parts[0, 0]      # a part that saw no keys
+    o_parts[0, 0] = 0.0 if parts > 1 else o_parts[0, 0]
+    o = torch.empty((rows, d), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((rows,), dtype=torch.float32, device="cuda")
+    B.pfx_merge_states(torch.from_numpy(o_parts).cuda(), torch.from_numpy(lse_parts).cuda(), o, lse)
+    B.pfx_sync_check()
+    ro, rl = oracle.merge_partials([p.astype(np.float64) for p in o_parts], [l.astype(np.float64) for l in lse_parts])
+    got = oracle.bf16_bits_to_f64(RN.to_host_bits(o))
+    assert np.max(np.abs(got - ro)) <= 2 ** -8 * np.max(np.abs(ro)) + 1e-6
+    assert np.max(np.abs(lse.cpu().numpy() - rl)) <= 1e-5 * (1 + np.max(np.abs(rl)))
+
+
+def test_page_copy_bit_exact_all_directions():
+    announce("page copy: device->device, host->device, device->host")
+    rng = np.random.default_rng(5)
+    hkv, d = 8, 128
+    src = rng.integers(0, 65535, size=(40, hkv, 16, d), dtype=np.uint16)
+    dst0 = rng.integers(0, 65535, size=(100, hkv, 16, d), dtype=np.uint16)
+    dst_pages = rng.permutation(100)[:25].astype(np.int32)
+    src_pages = rng.integers(0, 40, size=25).astype(np.int32)
+    want = oracle.page_copy(dst0, src, dst_pages, src_pages)
+    ws = torch.empty(B.pfx_page_copy_workspace_bytes(25) + 256, dtype=torch.uint8, device="cuda")
+    d_src = RN.to_device_bits(src)
+    d_dst = RN.to_device_bits(dst0)
+    # device -> device (K and V given the same arrays for simplicity, then distinct)
+    h_v = torch.from_numpy(src[::-1].copy().view(np.int16)).view(torch.bfloat16).pin_memory()
+    d_dst_v = RN.to_device_bits(dst0)
+    B.pfx_page_copy(B.make_pool(100, hkv, d, d_dst, d_dst_v), B.make_pool(40, hkv, d, d_src, h_v),
+                    dst_pages, src_pages, ws)
+    B.pfx_sync_check()
+    assert np.array_equal(RN.to_host_bits(d_dst), want)
+    want_v = oracle.page_copy(dst0, src[::-1].copy(), dst_pages, src_pages)
+    assert np.array_equal(RN.to_host_bits(d_dst_v), want_v)
+    # device -> pinned host (eviction)
+    h_dst = torch.from_numpy(dst0.view(np.int16).copy()).view(torch.bfloat16).pin_memory()
+    h_dst_v = torch.from_numpy(dst0.view(np.int16).copy()).view(torch.bfloat16).pin_memory()
+    B.pfx_page_copy(B.make_pool(100, hkv, d, h_dst, h_dst_v), B.make_pool(40, hkv, d, d_src, d_src),
+                    dst_pages, src_pages, ws)
+    B.pfx_sync_check()
+    assert np.array_equal(h_dst.view(torch.int16).numpy().view(np.uint16), want)
+    assert np.array_equal(h_dst_v.view(torch.int16).numpy().view(np.uint16), want)
+
+
+# --------------------------------------------------------------------------- small batches
+
+SMALL_CASES = [
+    # (seed, Hq, Hkv, d, prefix_len, reqs [(agent, L, n)], opts)
+    (1, 8, 2, 64, [40, 17], [(0, 5, 1), (1, 20, 1), (0, 33, 33), (-1, 3, 3), (1, 16, 2)], {}),
+    (2, 32, 8, 128, [100, 0, 37], [(0, 70, 1), (2, 1, 1), (1, 40, 40), (0, 65, 1), (2, 17, 4), (-1, 31, 1)],
+     dict(prefix_chunk=32, suffix_chunk=32)),
+    (3, 16, 16, 128, [64], [(0, 90, 90), (0, 1, 1), (0, 48, 1)], {}),                 # G = 1
+    (4, 16, 1, 64, [300], [(0, 9, 1), (0, 200, 1), (0, 40, 40), (-1, 5, 1)], dict(prefix_chunk=64)),  # G = 16
+    (5, 64, 8, 128, [129, 500], [(i % 2, 10 + 7 * i, 1) for i in range(20)] + [(1, 77, 2)], dict(suffix_chunk=64)),
+    (6, 32, 8, 128, [16], [(0, 1, 0), (0, 33, 1), (-1, 64, 64)], {}),                 # a request with no rows
+]
+
+
+@pytest.mark.parametrize("case", SMALL_CASES, ids=[f"small{c[0]}" for c in SMALL_CASES])
+def test_small_batches(case):
+    seed, hq, hkv, d, plen, reqs, opts = case
+    b = W.make_batch(seed, num_q_heads=hq, num_kv_heads=hkv, head_dim=d, num_pages=256, prefix_len=plen,
+                     agent=[r[0] for r in reqs], suffix_len=[r[1] for r in reqs], n_rows=[r[2] for r in reqs])
+    hv = W.host_values(b, seed + 50)
+    run_and_check(b, hv, f"small{seed}", **opts)
+
+
+def test_many_partials_merge_in_kernel():
+    """Long prefix cut into 32-key chunks: 40+ partials per row merged by the
+    last-arriving workgroup."""
+    b = W.make_batch(9, num_q_heads=32, num_kv_heads=8, head_dim=128, num_pages=1024, prefix_len=[1300, 700],
+                     agent=[i % 2 for i in range(40)], suffix_len=[100 + 13 * i for i in range(40)],
+                     n_rows=[1] * 40)
+    hv = W.host_values_fast(b, 10)
+    run_and_check(b, hv, "many-partials", prefix_chunk=32, suffix_chunk=64)
+
+
+# --------------------------------------------------------------------------- the five workloads
+
+def test_config1_extend_then_16_decode_steps():
+    b = W.config_batch(1)
+    hv = W.host_values(b, 2001)
+    ds, o_bits, lse = run_and_check(b, hv, "config1-extend", check_pages=True)
+    # 16 greedy decode steps: one new page per request at step 0, then one token per step.
+    alloc_free = sorted(set(range(b.num_pages)) - set(int(p) for p in b.used_pages()))
+    extra = alloc_free[:len(b.agent)]
+    pool_k, pool_v = PT.expected_pools(b, hv)
+    pages = list(hv.pages) + extra
+    # The decode steps reuse the same device pool; the oracle follows with its own append.
+    index = {int(p): i for i, p in enumerate(pages)}
+    kp = np.concatenate([pool_k, np.full((len(extra),) + pool_k.shape[1:], W.POISON_BF16, np.uint16)])
+    vp = np.concatenate([pool_v, np.full_like(kp[len(pool_k):], W.POISON_BF16)])
+    rng = np.random.Generator(np.random.PCG64(3001))
+    for step in range(16):
+        sb = W.tiny_decode_step(b, step, extra)
+        q = W.bf16_round(rng.standard_normal((4, 8, 64), dtype=np.float32))
+        kn = W.bf16_round(rng.standard_normal((4, 2, 64), dtype=np.float32))
+        vn = W.bf16_round(rng.standard_normal((4, 2, 64), dtype=np.float32))
+        pool = ds.pool
+        plan = B.plan_from_batch(pool, sb, B.PFX_MODE_DECODE).upload()
+        qd, knd, vnd = RN.to_device_bits(q), RN.to_device_bits(kn), RN.to_device_bits(vn)
+        o = torch.empty((4, 8, 64), dtype=torch.bfloat16, device="cuda")
+        l = torch.empty((4, 8), dtype=torch.float32, device="cuda")
+        B.pfx_append_kv(pool, plan, knd, vnd)
+        B.pfx_attention(pool, plan, qd, o, l)
+        B.pfx_sync_check()
+        sp = [np.array([index[int(p)] for p in pl]) for pl in sb.suffix_pages]
+        pp = [np.array([index[int(p)] for p in pl]) for pl in sb.prefix_pages]
+        kp, vp = oracle.append_kv(kp, vp, sp, sb.suffix_len, sb.n_rows, kn, vn)
+        gk, gv = ds.read_pages(pages)
+        assert np.array_equal(gk, kp) and np.array_equal(gv, vp), f"decode step {step}: pool differs"
+        ro, rl = oracle.prefix_shared_attention(kp, vp, pp, sb.prefix_len, sb.agent, sp, sb.suffix_len, sb.n_rows,
+                                                q, 8)
+        PT.compare(sb, RN.to_host_bits(o), l.cpu().numpy(), ro, rl, f"config1 decode step {step}")
+
+
+def relocate(batch, hv, seed):
+    """Same logical content at a different page placement."""
+    nb = W.make_batch(seed, num_q_heads=batch.num_q_heads, num_kv_heads=batch.num_kv_heads,
+                      head_dim=batch.head_dim, num_pages=batch.num_pages, prefix_len=batch.prefix_len,
+                      agent=batch.agent, suffix_len=batch.suffix_len, n_rows=batch.n_rows)
+    old = {int(p): i for i, p in enumerate(hv.pages)}
+    mapping = {}
+    for a in range(len(batch.prefix_pages)):
+        for x, y in zip(batch.prefix_pages[a], nb.prefix_pages[a]):
+            mapping[int(y)] = old[int(x)]
+    for r in range(len(batch.suffix_pages)):
+        for x, y in zip(batch.suffix_pages[r], nb.suffix_pages[r]):
+            mapping[int(y)] = old[int(x)]
+    pages = np.array(sorted(mapping), np.int64)
+    src = np.array([mapping[int(p)] for p in pages])
+    return nb, W.HostValues(pages, hv.k_pages[src], hv.v_pages[src], hv.q, hv.k_new, hv.v_new)
+
+
+def test_config2_decode_deterministic_and_placement_invariant():
+    b = W.config_batch(2)
+    hv = W.host_values_fast(b, 2002)
+    ds, o1, l1 = run_and_check(b, hv, "config2")
+    ds.attention()
+    B.pfx_sync_check()
+    o2, l2 = ds.outputs()
+    assert np.array_equal(o1, o2) and np.array_equal(l1, l2), "rerun is not bit-identical"
+    del ds
+    nb, nhv = relocate(b, hv, 4242)
+    announce("config2 relocated")
+    ds2 = RN.DeviceStep(nb, nhv)
+    ds2.step()
+    B.pfx_sync_check()
+    o3, l3 = ds2.outputs()
+    assert np.array_equal(o1, o3) and np.array_equal(l1, l3), "placement changed the result bits"
+
+
+def sample_rows(batch, rng, per=16):
+    rows = {}
+    for r in range(len(batch.agent)):
+        n = int(batch.n_rows[r])
+        if n == 0:
+            continue
+        L = int(batch.suffix_len[r])
+        cand = {0, n - 1}
+        for i in range(n):                      # rows on page boundaries of the suffix
+            if (L - n + i) % 16 in (0, 15):
+                cand.add(i)
+        cand = sorted(cand)
+        pick = set(rng.choice(cand, size=min(len(cand), per // 2), replace=False).tolist())
+        pick |= set(rng.integers(0, n, size=per // 2).tolist())
+        pick |= {0, n - 1}
+        rows[r] = sorted(pick)
+    return rows
+
+
+def test_config3_extend_sampled_rows():
+    b = W.config_batch(3)
+    hv = W.host_values_fast(b, 2003)
+    rows = sample_rows(b, np.random.default_rng(3))
+    run_and_check(b, hv, "config3", rows=rows)
+
+
+def test_config3_shape_small_full():
+    """Config 3's shape with shorter lengths, every row checked."""
+    b = W.make_batch(33, num_q_heads=32, num_kv_heads=8, head_dim=128, num_pages=4096, prefix_len=[700, 1024, 33],
+                     agent=[0, 1, 2, 0, 1, 2, -1], suffix_len=[256, 300, 17, 129, 64, 200, 90],
+                     n_rows=[256, 300, 17, 129, 64, 200, 90])
+    hv = W.host_values_fast(b, 34)
+    run_and_check(b, hv, "config3-small")
+
+
+def test_config4_gather_evicted_then_decode():
+    b = W.config_batch(4)
+    hv = W.host_values_fast(b, 2004)
+    evicted = [int(a) for a in b.meta["evicted"]]
+    run_and_check(b, hv, "config4", host_resident=evicted)
+
+
+@pytest.mark.timeout(600)
+def test_config5_80_layers_sampled():
+    """70B-like mixed batch over 80 layers with independent pools (device-drawn
+    values); layer 0 and one seeded layer fully on decode rows and 16 rows per
+    extend request, 10% of decode requests on the other layers."""
+    b = W.config_batch(5)
+    layers = int(b.meta["layers"])
+    hkv, d, hq = b.num_kv_heads, b.head_dim, b.num_q_heads
+    announce(f"config5: {layers} layers, pool {b.num_pages} pages/layer, tokens {b.num_tokens}")
+    gen = torch.Generator(device="cuda")
+    shape = (b.num_pages, hkv, 16, d)
+    # Each layer's pool: the same device-drawn N(0,1) pages rotated by a
+    # layer-specific page offset, so every layer holds different data while
+    # 200 GB are filled at copy speed.
+    gen.manual_seed(50_000)
+    base_k = torch.randn(shape, dtype=torch.bfloat16, device="cuda", generator=gen)
+    base_v = torch.randn(shape, dtype=torch.bfloat16, device="cuda", generator=gen)
+    pools_k, pools_v = [], []
+    for layer in range(layers):
+        pools_k.append(torch.roll(base_k, shifts=977 * layer + 1, dims=0))
+        pools_v.append(torch.roll(base_v, shifts=1489 * layer + 3, dims=0))
+    del base_k, base_v
+    gen.manual_seed(5)
+    t = b.num_tokens
+    q = torch.randn((t, hq, d), dtype=torch.bfloat16, device="cuda", generator=gen)
+    kn = torch.randn((t, hkv, d), dtype=torch.bfloat16, device="cuda", generator=gen)
+    vn = torch.randn((t, hkv, d), dtype=torch.bfloat16, device="cuda", generator=gen)
+    o = torch.empty((t, hq, d), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((t, hq), dtype=torch.float32, device="cuda")
+    pool0 = B.make_pool(b.num_pages, hkv, d, pools_k[0], pools_v[0])
+    plan = B.plan_from_batch(pool0, b, B.PFX_MODE_MIXED).upload()
+    rng = np.random.default_rng(55)
+    full_layers = {0, int(rng.integers(1, layers))}
+    ext = [r for r in range(len(b.agent)) if b.n_rows[r] > 1]
+    dec = [r for r in range(len(b.agent)) if b.n_rows[r] == 1]
+    q_bits = RN.to_host_bits(q)
+    kn_bits, vn_bits = RN.to_host_bits(kn), RN.to_host_bits(vn)
+    for layer in range(layers):
+        pool = B.make_pool(b.num_pages, hkv, d, pools_k[layer], pools_v[layer])
+        B.pfx_append_kv(pool, plan, kn, vn)
+        B.pfx_attention(pool, plan, q, o, lse)
+        if layer not in full_layers and layer % 8 != 3:
+            continue
+        B.pfx_sync_check()
+        if layer in full_layers:
+            rows = {r: [0] for r in dec}
+            rows.update({r: v for r, v in sample_rows(b, rng, per=16).items() if r in ext})
+        else:
+            rows = {int(r): [0] for r in rng.choice(dec, size=len(dec) // 10, replace=False)}
+        need = set()
+        for r in rows:
+            a = int(b.agent[r])
+            need.update(int(p) for p in b.prefix_pages[a])
+            need.update(int(p) for p in b.suffix_pages[r])
+        pages = np.array(sorted(need), np.int64)
+        idx = torch.from_numpy(pages).cuda()
+        kp = pools_k[layer].view(torch.int16).index_select(0, idx).cpu().numpy().view(np.uint16)
+        vp = pools_v[layer].view(torch.int16).index_select(0, idx).cpu().numpy().view(np.uint16)
+        index = {int(p): i for i, p in enumerate(pages)}
+        pp = [np.array([index.get(int(p), 0) for p in pl]) for pl in b.prefix_pages]
+        sp = [np.array([index.get(int(p), 0) for p in pl]) for pl in b.suffix_pages]
+        # append bit-exactness on the sampled requests' new-token slots
+        q_indptr = b.q_indptr()
+        for r in list(rows)[:20]:
+            n, L = int(b.n_rows[r]), int(b.suffix_len[r])
+            for i in (0, n - 1):
+                pos = L - n + i
+                pg = sp[r][pos // 16]
+                assert np.array_equal(kp[pg, :, pos % 16], kn_bits[q_indptr[r] + i])
+                assert np.array_equal(vp[pg, :, pos % 16], vn_bits[q_indptr[r] + i])
+        ro, rl = oracle.prefix_shared_attention(kp, vp, pp, b.prefix_len, b.agent, sp, b.suffix_len, b.n_rows,
+                                                q_bits, hq, rows=rows)
+        res = PT.compare(b, RN.to_host_bits(o), lse.cpu().numpy(), ro, rl, f"config5 layer {layer}")
+        announce(f"config5 layer {layer}: rows={sum(len(v) for v in rows.values())} max_abs={res[0]:.2e} "
+                 f"rel={res[1]:.2e}")
+    del pools_k, pools_v
+    torch.cuda.empty_cache()
