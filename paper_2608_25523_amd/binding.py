@@ -73,6 +73,12 @@ class pfx_plan_stats(C.Structure):
 
 
 def _load():
+    # torch bundles its own HIP runtime with the same soname as the system
+    # one.  Loading torch first makes this library bind to that same runtime,
+    # so one process never holds two HIP runtimes (the second would find no
+    # device).
+    import torch  # noqa: F401
+
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2608_25523_amd.build` "
                           "(there is no CPU fallback)")

@@ -20,6 +20,8 @@ FLAGS = [
     "-O3",
     "-std=c++17",
     "-fPIC",
+    # Code-object v5: accepted by both the system runtime and the one torch bundles.
+    "-mcode-object-version=5",
     "-shared",
     # Packed-FP32 VALU ops are kept out of the device code.
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -29,8 +29,10 @@ enum ItemKind : int32_t { kPrefixItem = 0, kSuffixItem = 1, kExtendItem = 2 };
 //   segment 0 (no mask):  keys [s0_kbeg, s0_kend) of the list at s0_page_off;
 //   segment 1 (causal):   keys [s1_kbeg, s1_kend) of the list at s1_page_off,
 //                         key k visible to token t iff k <= t + causal_base.
-// out_slot < 0: final output rows; otherwise partial slot out_slot of every
-// request the item covers.
+// out_slot >= 0: partial slot out_slot of every request the item covers
+// (phase A).  out_slot < 0: final rows -- directly (extend items), or, for a
+// request's last suffix chunk (phase B), after merging the request's
+// phase-A partials.
 struct alignas(16) Item {
   int32_t kv_head;
   int32_t row_begin;
@@ -50,8 +52,8 @@ static_assert(sizeof(Item) == 64, "Item is 16 int32");
 struct ReqInfo {
   int32_t q_start;    // first query row
   int32_t n;          // query rows
-  int32_t nparts;     // partial results to merge (1: written directly)
-  int32_t part_base;  // first partial row: (part_base + slot * n + i) for row i
+  int32_t nparts;     // partial results written in phase A (0: none)
+  int32_t part_base;  // partial row of (slot, row i): part_base + slot * n + i
 };
 
 // Device pointers into an uploaded workspace.
@@ -62,7 +64,6 @@ struct DevPlan {
   const int32_t* tok_req;
   const ReqInfo* req;
   const int32_t* tok_slot;  // page * 16 + slot of every new token (append)
-  int32_t* counters;        // [num_reqs * hkv], zero between launches
   float* o_part;            // [num_part_rows][hq][d]
   float* l_part;            // [num_part_rows][hq]
 };
@@ -72,7 +73,7 @@ struct DevPlan {
 struct pfx_plan {
   int32_t num_pages = 0, hkv = 0, d = 0, hq = 0, group = 0, mode = 0;
   int32_t num_reqs = 0, num_tokens = 0;
-  int32_t n_items_wide = 0;  // items[0, n_items_wide): more than one 16-column block
+  int32_t n_items_a = 0;  // items[0, n_items_a): phase A; the rest: phase B
   std::vector<pfx::Item> items;
   std::vector<int32_t> row_tok, page_list, tok_req, tok_slot;
   std::vector<pfx::ReqInfo> req;
@@ -81,9 +82,8 @@ struct pfx_plan {
   int32_t pages_needed = 0;
   // byte offsets inside the workspace
   size_t off_items = 0, off_row_tok = 0, off_page_list = 0, off_tok_req = 0, off_req = 0,
-         off_tok_slot = 0, off_counters = 0, off_opart = 0, off_lpart = 0, total_bytes = 0,
-         blob_bytes = 0;
-  std::vector<unsigned char> blob;  // host image of [0, off_counters)
+         off_tok_slot = 0, off_opart = 0, off_lpart = 0, total_bytes = 0, blob_bytes = 0;
+  std::vector<unsigned char> blob;  // host image of [0, blob_bytes)
   void* dev_ws = nullptr;
   size_t dev_ws_bytes = 0;
 };

@@ -13,13 +13,16 @@
 // neither operand; each lane loads 8 keys x (D/16) dims and transposes them
 // in registers with byte permutes.
 //
-// Work is a list of items (see pfx_internal.h).  A workgroup of four waves
-// runs one item: the waves take its 32-key steps round-robin, each with the
-// full set of query columns, and combine their softmax states through LDS.
-// An item whose keys are only part of a row's keys (a prefix chunk, a
-// suffix chunk) writes a partial result; the last item to finish for a
-// (request, KV head) merges all of its partials (log-sum-exp merge) and
-// writes the final row.
+// Work is a list of items (see pfx_internal.h), run in two stream-ordered
+// launches.  Phase A: a workgroup of four waves runs one item -- the waves
+// take its 32-key steps round-robin, each with all of the item's query
+// columns, and combine their softmax states through LDS; the item writes
+// either final rows (extend) or a partial result over its key range (a
+// prefix chunk shared by an agent's decode rows, or an early suffix chunk).
+// Phase B: one wave per (decode request, KV head) streams the last suffix
+// chunk and merges the request's phase-A partials in registers
+// (log-sum-exp merge) before writing the final rows.  The launch boundary
+// orders the two phases, so no atomics or device-wide fences are needed.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -78,35 +81,56 @@ struct AttnArgs {
 
 // Geometry of one 32-key step of an item.
 struct StepPos {
-  const int32_t* pages;  // page list of the segment
+  int32_t list_off;      // offset of the segment's page list in the plan's page list
   int32_t k0, kend;      // first key of the step, end of the segment
-  bool causal;           // segment 1
+  int32_t seg;           // 0: prefix (no mask), 1: suffix (causal)
 };
 
-__device__ __forceinline__ StepPos step_pos(const Item& it, const int32_t* page_list, int st, int s0_steps) {
+__device__ __forceinline__ StepPos step_pos(const Item& it, int st, int s0_steps) {
   StepPos p;
   if (st < s0_steps) {
-    p.pages = page_list + it.s0_page_off;
+    p.list_off = it.s0_page_off;
     p.k0 = it.s0_kbeg + st * kStepKeys;
     p.kend = it.s0_kend;
-    p.causal = false;
+    p.seg = 0;
   } else {
-    p.pages = page_list + it.s1_page_off;
+    p.list_off = it.s1_page_off;
     p.k0 = it.s1_kbeg + (st - s0_steps) * kStepKeys;
     p.kend = it.s1_kend;
-    p.causal = true;
+    p.seg = 1;
   }
   return p;
 }
 
+// 64 consecutive page ids of a segment, one per lane, so a step finds its
+// pages with v_readlane instead of a dependent scalar load.
+struct PageWindow {
+  int32_t vpage;  // lane i: page id at list position base + i
+  int32_t seg;    // segment held (-1: none)
+  int32_t base;
+};
+
+__device__ __forceinline__ void window_for(PageWindow& w, const int32_t* page_list, const StepPos& p, int lane) {
+  const int pos = p.k0 >> 4;  // even: steps start on 32-key boundaries
+  if (p.seg != w.seg || pos < w.base || pos + 1 >= w.base + 64) {
+    const int npages = (p.kend + 15) >> 4;
+    w.seg = p.seg;
+    w.base = pos;
+    w.vpage = (pos + lane < npages) ? page_list[p.list_off + pos + lane] : 0;
+  }
+}
+
 template <int D>
-__device__ __forceinline__ void load_kv(KVRegs<D>& r, const AttnArgs& a, const StepPos& p, int h, int col,
-                                        int grp) {
+__device__ __forceinline__ void load_kv(KVRegs<D>& r, const AttnArgs& a, PageWindow& w, const StepPos& p, int h,
+                                        int lane) {
   constexpr int KS = D / 32;
   constexpr int CH = D / 16;
-  const int page0 = p.pages[p.k0 >> 4];
+  const int col = lane & 15, grp = lane >> 4;
+  window_for(w, a.plan.page_list, p, lane);
+  const int pos = (p.k0 >> 4) - w.base;
+  const int page0 = __builtin_amdgcn_readlane(w.vpage, pos);
   const bool has1 = p.k0 + 16 < p.kend;
-  const int page1 = has1 ? p.pages[(p.k0 >> 4) + 1] : page0;
+  const int page1 = has1 ? __builtin_amdgcn_readlane(w.vpage, pos + 1) : page0;
   const size_t head_elems = size_t(16) * D;
   const size_t b0 = (size_t(page0) * a.hkv + h) * head_elems;
   const size_t b1 = (size_t(page1) * a.hkv + h) * head_elems;
@@ -135,6 +159,18 @@ __device__ __forceinline__ uint32_t v_elem_pair(const typename VecCH<D>::T& a, c
   return (e & 1) ? __builtin_amdgcn_perm(wb, wa, 0x07060302u) : __builtin_amdgcn_perm(wb, wa, 0x05040100u);
 }
 
+// V^T operand jj: dim CH*col + jj of the 8 keys this lane owns (tile 0 keys
+// 4*grp..+3, then tile 1 keys 4*grp..+3), built with byte permutes.
+template <int D>
+__device__ __forceinline__ bf16x8 v_operand(const KVRegs<D>& r, int jj) {
+  u32x4 w;
+  w[0] = v_elem_pair<D>(r.v[0][0], r.v[0][1], jj);
+  w[1] = v_elem_pair<D>(r.v[0][2], r.v[0][3], jj);
+  w[2] = v_elem_pair<D>(r.v[1][0], r.v[1][1], jj);
+  w[3] = v_elem_pair<D>(r.v[1][2], r.v[1][3], jj);
+  return __builtin_bit_cast(bf16x8, w);
+}
+
 template <int D, int QB>
 struct WaveState {
   static constexpr int CH = D / 16;
@@ -159,18 +195,7 @@ __device__ __forceinline__ void compute_step(WaveState<D, QB>& ws, KVRegs<D>& r,
       for (int i = 0; i < 4; ++i)
         if (p.k0 + 16 * t + 4 * grp + i >= p.kend) r.v[t][i] = typename VecCH<D>::T{};
   }
-  // V^T operands: vt[jj] holds dim CH*col + jj of the 8 keys this lane owns.
-  bf16x8 vt[CH];
-#pragma unroll
-  for (int jj = 0; jj < CH; ++jj) {
-    u32x4 w;
-    w[0] = v_elem_pair<D>(r.v[0][0], r.v[0][1], jj);
-    w[1] = v_elem_pair<D>(r.v[0][2], r.v[0][3], jj);
-    w[2] = v_elem_pair<D>(r.v[1][0], r.v[1][1], jj);
-    w[3] = v_elem_pair<D>(r.v[1][2], r.v[1][3], jj);
-    vt[jj] = __builtin_bit_cast(bf16x8, w);
-  }
-  const bool need_mask = tail || p.causal;
+  const bool need_mask = tail || p.seg == 1;
 #pragma unroll
   for (int b = 0; b < QB; ++b) {
     if (b >= nblk) break;
@@ -187,7 +212,7 @@ __device__ __forceinline__ void compute_step(WaveState<D, QB>& ws, KVRegs<D>& r,
       x[4 + i] = s1[i] * scale_log2;
     }
     if (need_mask) {
-      const int lim_b = p.causal ? lim[b] : 0x7fffffff;
+      const int lim_b = p.seg == 1 ? lim[b] : 0x7fffffff;
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -224,7 +249,7 @@ __device__ __forceinline__ void compute_step(WaveState<D, QB>& ws, KVRegs<D>& r,
     const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
 #pragma unroll
     for (int jj = 0; jj < CH; ++jj)
-      ws.acc[b][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt[jj], pb, ws.acc[b][jj], 0, 0, 0);
+      ws.acc[b][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v_operand<D>(r, jj), pb, ws.acc[b][jj], 0, 0, 0);
   }
 }
 
@@ -257,27 +282,6 @@ __device__ __forceinline__ void merge_row8(const float* o_row, size_t o_stride, 
   if (lse_out) *lse_out = mx + logf(z);
 }
 
-// Merge every partial of (request r, KV head h) into the final rows.
-template <int D>
-__device__ void merge_request(const AttnArgs& a, int r, int h) {
-  const ReqInfo ri = a.plan.req[r];
-  const int G = a.group;
-  constexpr int SL = D / 8;  // 8-dim slices per row
-  const int rows = ri.n * G;
-  for (int t = threadIdx.x; t < rows * SL; t += blockDim.x) {
-    const int x = t / SL, sl = t - x * SL;
-    const int i = x >> a.group_shift, g = x & (G - 1);
-    const int qh = h * G + g;
-    const size_t prow = size_t(ri.part_base) + i;
-    const float* orow = a.plan.o_part + (prow * a.hq + qh) * D + sl * 8;
-    const float* lrow = a.plan.l_part + prow * a.hq + qh;
-    const size_t tok = size_t(ri.q_start) + i;
-    uint16_t* out = a.o + (tok * a.hq + qh) * D + sl * 8;
-    float* lo = (a.lse && sl == 0) ? a.lse + tok * a.hq + qh : nullptr;
-    merge_row8(orow, size_t(ri.n) * a.hq * D, lrow, size_t(ri.n) * a.hq, ri.nparts, out, lo);
-  }
-}
-
 template <int D, int QB>
 __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   constexpr int KS = D / 32;
@@ -287,8 +291,6 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   __shared__ float red_o[kWaves][NCOL][D + 4];
   __shared__ float red_m[kWaves][NCOL];
   __shared__ float red_l[kWaves][NCOL];
-  __shared__ int last_req[64];
-  __shared__ int n_last;
 
   const Item it = a.plan.items[a.item_base + blockIdx.x];
   const int wave = threadIdx.x >> 6;
@@ -335,17 +337,18 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   // Two register buffers: the next step's K/V is in flight while the
   // current one is multiplied.
   KVRegs<D> bufA, bufB;
+  PageWindow win{0, -1, 0};
   int st = wave;
-  if (st < nsteps) load_kv<D>(bufA, a, step_pos(it, a.plan.page_list, st, s0_steps), h, col, grp);
+  if (st < nsteps) load_kv<D>(bufA, a, win, step_pos(it, st, s0_steps), h, lane);
   while (st < nsteps) {
     int nst = st + kWaves;
-    if (nst < nsteps) load_kv<D>(bufB, a, step_pos(it, a.plan.page_list, nst, s0_steps), h, col, grp);
-    compute_step<D, QB>(ws, bufA, qf, lim, step_pos(it, a.plan.page_list, st, s0_steps), nblk, grp, a.scale_log2);
+    if (nst < nsteps) load_kv<D>(bufB, a, win, step_pos(it, nst, s0_steps), h, lane);
+    compute_step<D, QB>(ws, bufA, qf, lim, step_pos(it, st, s0_steps), nblk, grp, a.scale_log2);
     st = nst;
     if (st >= nsteps) break;
     nst = st + kWaves;
-    if (nst < nsteps) load_kv<D>(bufA, a, step_pos(it, a.plan.page_list, nst, s0_steps), h, col, grp);
-    compute_step<D, QB>(ws, bufB, qf, lim, step_pos(it, a.plan.page_list, st, s0_steps), nblk, grp, a.scale_log2);
+    if (nst < nsteps) load_kv<D>(bufA, a, win, step_pos(it, nst, s0_steps), h, lane);
+    compute_step<D, QB>(ws, bufB, qf, lim, step_pos(it, st, s0_steps), nblk, grp, a.scale_log2);
     st = nst;
   }
 
@@ -439,35 +442,106 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
       }
     }
   }
-  if (!partial) return;
+}
 
-  // Arrival: make the partial rows visible device-wide, then count this
-  // item once per (request, KV head) it covers.  The last arrival merges.
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) n_last = 0;
-  __syncthreads();
-  if (threadIdx.x < it.row_count) {
-    const int tok = a.plan.row_tok[it.row_begin + threadIdx.x];
-    const int r = a.plan.tok_req[tok];
-    const ReqInfo ri = a.plan.req[r];
-    if (tok == ri.q_start) {
-      const int old = atomicAdd(a.plan.counters + size_t(r) * a.hkv + h, 1);
-      if (old == ri.nparts - 1) {
-        const int slot = atomicAdd(&n_last, 1);
-        last_req[slot] = r;
+// Phase B: one wave per (decode request, KV head): the request's last suffix
+// chunk, merged with the partials phase A wrote for the same rows.
+template <int D>
+__global__ __launch_bounds__(64, 2) void attn_final_kernel(AttnArgs a) {
+  constexpr int KS = D / 32;
+  constexpr int CH = D / 16;
+  const Item it = a.plan.items[a.item_base + blockIdx.x];
+  const int lane = threadIdx.x;
+  const int col = lane & 15, grp = lane >> 4;
+  const int h = it.kv_head;
+  const int G = a.group;
+  int j = col >> a.group_shift;
+  const int g = col & (G - 1);
+  const bool valid = j < it.row_count;
+  if (!valid) j = 0;
+  const int tok = a.plan.row_tok[it.row_begin + j];
+  const int qh = h * G + g;
+  bf16x8 qf[1][KS];
+  int lim[1] = {tok + it.causal_base};
+  {
+    const uint16_t* qp = a.q + (size_t(tok) * a.hq + qh) * D + 8 * grp;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) qf[0][s] = *reinterpret_cast<const bf16x8*>(qp + 32 * s);
+  }
+  WaveState<D, 1> ws;
+  ws.m[0] = kNegBig;
+  ws.l[0] = 0.f;
+#pragma unroll
+  for (int jj = 0; jj < CH; ++jj) ws.acc[0][jj] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int s0_steps = (it.s0_kend - it.s0_kbeg + kStepKeys - 1) / kStepKeys;
+  const int s1_steps = (it.s1_kend - it.s1_kbeg + kStepKeys - 1) / kStepKeys;
+  const int nsteps = s0_steps + s1_steps;
+  KVRegs<D> bufA, bufB;
+  PageWindow win{0, -1, 0};
+  int st = 0;
+  if (st < nsteps) load_kv<D>(bufA, a, win, step_pos(it, st, s0_steps), h, lane);
+  while (st < nsteps) {
+    if (st + 1 < nsteps) load_kv<D>(bufB, a, win, step_pos(it, st + 1, s0_steps), h, lane);
+    compute_step<D, 1>(ws, bufA, qf, lim, step_pos(it, st, s0_steps), 1, grp, a.scale_log2);
+    if (++st >= nsteps) break;
+    if (st + 1 < nsteps) load_kv<D>(bufA, a, win, step_pos(it, st + 1, s0_steps), h, lane);
+    compute_step<D, 1>(ws, bufB, qf, lim, step_pos(it, st, s0_steps), 1, grp, a.scale_log2);
+    ++st;
+  }
+
+  float l = ws.l[0];
+  l += __shfl_xor(l, 16);
+  l += __shfl_xor(l, 32);
+  // This wave's own result in log2 units, then the phase-A partials.
+  const float own = l > 0.f ? ws.m[0] + log2f(l) : -INFINITY;
+  const float inv_l = l > 0.f ? 1.0f / l : 0.f;
+  float o[4 * CH];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int jj = 0; jj < CH; ++jj) o[CH * i + jj] = ws.acc[0][jj][i] * inv_l;
+  const int r = a.plan.tok_req[tok];
+  const ReqInfo ri = a.plan.req[r];
+  float lse2 = own;
+  if (ri.nparts > 0) {
+    const size_t i_row = size_t(tok - ri.q_start);
+    float mx = own;
+    for (int s = 0; s < ri.nparts; ++s) {
+      const size_t prow = size_t(ri.part_base) + size_t(s) * ri.n + i_row;
+      mx = fmaxf(mx, a.plan.l_part[prow * a.hq + qh] * kLog2e);
+    }
+    float z = fast_exp2(own - mx);
+#pragma unroll
+    for (int e = 0; e < 4 * CH; ++e) o[e] *= z;
+    for (int s = 0; s < ri.nparts; ++s) {
+      const size_t prow = size_t(ri.part_base) + size_t(s) * ri.n + i_row;
+      const float w = fast_exp2(a.plan.l_part[prow * a.hq + qh] * kLog2e - mx);
+      z += w;
+      const float* op = a.plan.o_part + (prow * a.hq + qh) * D + 4 * CH * grp;
+#pragma unroll
+      for (int e = 0; e < 4 * CH; e += 4) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(op + e);
+        o[e] += w * v[0];
+        o[e + 1] += w * v[1];
+        o[e + 2] += w * v[2];
+        o[e + 3] += w * v[3];
       }
     }
+    const float inv = 1.0f / z;
+#pragma unroll
+    for (int e = 0; e < 4 * CH; ++e) o[e] *= inv;
+    lse2 = mx + log2f(z);
   }
-  __syncthreads();
-  const int nl = n_last;
-  if (nl == 0) return;
-  __threadfence();
-  for (int k = 0; k < nl; ++k) {
-    const int r = last_req[k];
-    merge_request<D>(a, r, h);
-    if (threadIdx.x == 0) atomicExch(a.plan.counters + size_t(r) * a.hkv + h, 0);
+  if (!valid) return;
+  uint16_t* out = a.o + (size_t(tok) * a.hq + qh) * D + 4 * CH * grp;
+#pragma unroll
+  for (int e = 0; e < 4 * CH; e += 8) {
+    u32x4 w = {pack_bf16(o[e], o[e + 1]), pack_bf16(o[e + 2], o[e + 3]), pack_bf16(o[e + 4], o[e + 5]),
+               pack_bf16(o[e + 6], o[e + 7])};
+    *reinterpret_cast<u32x4*>(out + e) = w;
   }
+  if (a.lse && grp == 0) a.lse[size_t(tok) * a.hq + qh] = lse2 * kLn2;
 }
 
 template <int D>
@@ -516,11 +590,6 @@ __global__ __launch_bounds__(256) void page_copy_kernel(const u32x4* src_k, cons
     dst_v[dp * page_vecs + v] = src_v[sp * page_vecs + v];
 }
 
-__global__ void zero_kernel(int32_t* p, size_t n) {
-  const size_t i = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i < n) p[i] = 0;
-}
-
 static int hip_fail(hipError_t e, const char* what) {
   return fail(PFX_EHIP, "%s: %s", what, hipGetErrorString(e));
 }
@@ -541,9 +610,16 @@ static int check_pool_matches(const pfx_pool* pool, const pfx_plan* p, const cha
   return PFX_OK;
 }
 
-template <int D, int QB>
-static void launch_attn(const AttnArgs& a, int n, hipStream_t s) {
-  hipLaunchKernelGGL((attn_kernel<D, QB>), dim3(n), dim3(256), 0, s, a);
+template <int D>
+static void launch_phases(AttnArgs a, int n_a, int n_b, hipStream_t s) {
+  if (n_a) {
+    a.item_base = 0;
+    hipLaunchKernelGGL((attn_kernel<D, kMaxBlocks>), dim3(n_a), dim3(256), 0, s, a);
+  }
+  if (n_b) {
+    a.item_base = n_a;
+    hipLaunchKernelGGL((attn_final_kernel<D>), dim3(n_b), dim3(64), 0, s, a);
+  }
 }
 
 }  // namespace pfx
@@ -559,13 +635,6 @@ extern "C" int pfx_plan_upload(pfx_plan* p, void* ws, size_t bytes, void* stream
   if (p->blob_bytes) {
     hipError_t e = hipMemcpyAsync(ws, p->blob.data(), p->blob_bytes, hipMemcpyHostToDevice, s);
     if (e != hipSuccess) return hip_fail(e, "pfx_plan_upload: hipMemcpyAsync");
-  }
-  const size_t nc = size_t(p->num_reqs) * p->hkv;
-  if (nc) {
-    int32_t* c = reinterpret_cast<int32_t*>(static_cast<unsigned char*>(ws) + p->off_counters);
-    hipLaunchKernelGGL(zero_kernel, dim3((nc + 255) / 256), dim3(256), 0, s, c, nc);
-    int rc = check_launch("pfx_plan_upload: zero_kernel");
-    if (rc) return rc;
   }
   p->dev_ws = ws;
   p->dev_ws_bytes = bytes;
@@ -613,19 +682,10 @@ extern "C" int pfx_attention(const pfx_pool* pool, const pfx_plan* p, const void
   a.group_shift = __builtin_ctz(static_cast<unsigned>(p->group));
   a.scale_log2 = sm_scale * kLog2e;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const int n_wide = p->n_items_wide;
-  const int n_narrow = static_cast<int>(p->items.size()) - n_wide;
-  if (n_wide) {
-    a.item_base = 0;
-    if (p->d == 128) launch_attn<128, 4>(a, n_wide, s); else launch_attn<64, 4>(a, n_wide, s);
-    if ((rc = check_launch("pfx_attention (wide items)"))) return rc;
-  }
-  if (n_narrow) {
-    a.item_base = n_wide;
-    if (p->d == 128) launch_attn<128, 1>(a, n_narrow, s); else launch_attn<64, 1>(a, n_narrow, s);
-    if ((rc = check_launch("pfx_attention (narrow items)"))) return rc;
-  }
-  return PFX_OK;
+  const int n_a = p->n_items_a;
+  const int n_b = static_cast<int>(p->items.size()) - n_a;
+  if (p->d == 128) launch_phases<128>(a, n_a, n_b, s); else launch_phases<64>(a, n_a, n_b, s);
+  return check_launch("pfx_attention");
 }
 
 extern "C" int pfx_merge_states(const float* o_parts, const float* lse_parts, int32_t num_parts, int32_t rows,

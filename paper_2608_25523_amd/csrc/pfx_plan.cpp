@@ -38,7 +38,6 @@ DevPlan dev_plan(const pfx_plan* p) {
   d.tok_req = reinterpret_cast<const int32_t*>(base + p->off_tok_req);
   d.req = reinterpret_cast<const ReqInfo*>(base + p->off_req);
   d.tok_slot = reinterpret_cast<const int32_t*>(base + p->off_tok_slot);
-  d.counters = reinterpret_cast<int32_t*>(base + p->off_counters);
   d.o_part = reinterpret_cast<float*>(base + p->off_opart);
   d.l_part = reinterpret_cast<float*>(base + p->off_lpart);
   return d;
@@ -343,16 +342,20 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
         }
   }
 
-  // Decode rows against each request's own suffix, in chunks.
+  // Decode rows against each request's own suffix, in chunks.  Every chunk
+  // but the last is a phase-A item writing a partial; the last chunk is the
+  // request's phase-B item, which merges all of the row's partials (prefix
+  // chunks and earlier suffix chunks) with its own state and writes the row.
   int64_t part_rows = 0;
+  std::vector<Item> final_items;
   for (int32_t r = 0; r < R; ++r) {
     if (!is_decode_class(r)) continue;
     const ReqInfo ri = p->req[r];
     const int32_t L = b->suffix_len[r];
     const int32_t ns = nchunks(L, schunk);
-    const int32_t nparts = prefix_chunks[r] + ns;
+    const int32_t nparts = prefix_chunks[r] + ns - 1;  // written in phase A
     p->req[r].nparts = nparts;
-    if (nparts > 1) {
+    if (nparts > 0) {
       p->req[r].part_base = static_cast<int32_t>(part_rows);
       part_rows += int64_t(nparts) * ri.n;
     }
@@ -371,10 +374,15 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
         it.s1_kbeg = j * schunk;
         it.s1_kend = std::min(L, (j + 1) * schunk);
         it.causal_base = L - ri.n - ri.q_start;
-        it.out_slot = nparts > 1 ? prefix_chunks[r] + j : -1;
         it.kind = kSuffixItem;
         it.req = r;
-        items.push_back(it);
+        if (j + 1 < ns) {
+          it.out_slot = prefix_chunks[r] + j;
+          items.push_back(it);
+        } else {
+          it.out_slot = -1;
+          final_items.push_back(it);
+        }
         ++p->n_suffix_items;
       }
   }
@@ -384,7 +392,7 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   for (int32_t r = 0; r < R; ++r) {
     const ReqInfo ri = p->req[r];
     if (ri.n == 0 || is_decode_class(r)) continue;
-    p->req[r].nparts = 1;
+    p->req[r].nparts = 0;
     const int32_t a = b->agent[r];
     const int32_t P = a >= 0 ? pt->prefix_len[a] : 0;
     const int32_t L = b->suffix_len[r];
@@ -418,15 +426,17 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
     return delete p, fail(PFX_ERANGE, "pfx_plan_create: too many partial rows");
   p->num_part_rows = part_rows;
 
-  // Wide items (several 16-column blocks) first, narrow ones after; inside
-  // each class the longest key ranges go first so the tail stays short.
-  auto cost = [](const Item& it) { return (it.s0_kend - it.s0_kbeg) + (it.s1_kend - it.s1_kbeg); };
-  std::stable_sort(items.begin(), items.end(), [&](const Item& x, const Item& y) {
-    bool wx = x.nblk > 1, wy = y.nblk > 1;
-    if (wx != wy) return wx;
-    return cost(x) > cost(y);
-  });
-  p->n_items_wide = static_cast<int32_t>(std::count_if(items.begin(), items.end(), [](const Item& it) { return it.nblk > 1; }));
+  // Phase A (four-wave workgroups): longest key ranges first so the tail
+  // stays short.  Phase B (one-wave workgroups) runs after phase A on the
+  // same stream, so every partial it merges is complete and visible.
+  auto cost = [](const Item& it) {
+    return int64_t(it.s0_kend - it.s0_kbeg + it.s1_kend - it.s1_kbeg) * (it.nblk + 1);
+  };
+  auto by_cost = [&](const Item& x, const Item& y) { return cost(x) > cost(y); };
+  std::stable_sort(items.begin(), items.end(), by_cost);
+  std::stable_sort(final_items.begin(), final_items.end(), by_cost);
+  p->n_items_a = static_cast<int32_t>(items.size());
+  items.insert(items.end(), final_items.begin(), final_items.end());
   p->items = std::move(items);
 
   // ---- workspace layout ----
@@ -438,7 +448,6 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   p->off_req = off;        off = align256(off + p->req.size() * sizeof(ReqInfo));
   p->off_tok_slot = off;   off = align256(off + p->tok_slot.size() * 4);
   p->blob_bytes = off;
-  p->off_counters = off;   off = align256(off + size_t(R) * hkv * 4);
   p->off_opart = off;      off = align256(off + size_t(part_rows) * hq * p->d * 4);
   p->off_lpart = off;      off = align256(off + size_t(part_rows) * hq * 4);
   p->total_bytes = std::max<size_t>(off, 256);

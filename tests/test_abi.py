@@ -181,7 +181,7 @@ def enumerate_coverage(plan, batch):
                     if k <= tok + cbase:
                         assert tok + cbase == pos_in_suffix
                         counts[(tok, qh, plen + k)] = counts.get((tok, qh, plen + k), 0) + 1
-                slots.setdefault((tok, qh), set()).add(int(slot))
+                slots.setdefault((tok, qh), []).append(int(slot))
     return counts, slots
 
 
@@ -217,9 +217,17 @@ def test_plan_covers_every_visible_key_once(case):
                     assert counts.get((tok, qh, k), 0) == 1, (tok, qh, k)
                 expected += vis
     assert sum(counts.values()) == expected            # nothing invisible is attended
-    # Each row's partial slots are 0 .. nparts-1 (or the single direct slot -1).
+    # Each row has exactly one item writing its final value (slot -1); any
+    # other items write partial slots 0 .. k-1, each once.
+    items = p.export(0)
+    n_a = len(items) - sum(1 for it in items if it[11] < 0 and it[12] == 1)
     for (tok, qh), ss in slots.items():
-        assert ss == {-1} or ss == set(range(len(ss))), (tok, qh, ss)
+        assert ss.count(-1) == 1, (tok, qh, ss)
+        parts = sorted(x for x in ss if x >= 0)
+        assert parts == list(range(len(parts))), (tok, qh, ss)
+    # Phase B (final suffix chunks of decode rows) comes after every phase-A item.
+    kinds = [(int(it[11]) < 0 and int(it[12]) == 1) for it in items]
+    assert kinds == sorted(kinds)
 
 
 def test_plan_is_deterministic_and_placement_independent():

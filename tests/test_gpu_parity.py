@@ -129,7 +129,7 @@ def test_small_batches(case):
 def test_many_partials_merge_in_kernel():
     """Long prefix cut into 32-key chunks: 40+ partials per row merged by the
     last-arriving workgroup."""
-    b = W.make_batch(9, num_q_heads=32, num_kv_heads=8, head_dim=128, num_pages=1024, prefix_len=[1300, 700],
+    b = W.make_batch(9, num_q_heads=32, num_kv_heads=8, head_dim=128, num_pages=2048, prefix_len=[1300, 700],
                      agent=[i % 2 for i in range(40)], suffix_len=[100 + 13 * i for i in range(40)],
                      n_rows=[1] * 40)
     hv = W.host_values_fast(b, 10)
