@@ -14,12 +14,16 @@ namespace pfx {
 
 // Columns of one MFMA tile: the query side of a 16x16x32 bf16 product.
 constexpr int kTileCols = 16;
-// Largest number of 16-column blocks one wave carries (64 query columns).
-constexpr int kMaxBlocks = 4;
+// Waves per phase-A workgroup; each owns 16 (decode) or 32 (extend) columns.
+constexpr int kTileWaves = 4;
+// Query columns of a phase-A item: decode prefix pieces and early suffix
+// chunks, and extend blocks.
+constexpr int kDecodeTileCols = kTileWaves * 16;
+constexpr int kExtendTileCols = kTileWaves * 32;
+// Page ids one phase-A item may reference (its LDS page table).
+constexpr int kMaxTilePages = 1024;
 // Keys processed per inner step (two 16-token pages).
 constexpr int kStepKeys = 32;
-// Waves per workgroup; they split an item's key steps between them.
-constexpr int kWaves = 4;
 
 enum ItemKind : int32_t { kPrefixItem = 0, kSuffixItem = 1, kExtendItem = 2 };
 
@@ -73,7 +77,9 @@ struct DevPlan {
 struct pfx_plan {
   int32_t num_pages = 0, hkv = 0, d = 0, hq = 0, group = 0, mode = 0;
   int32_t num_reqs = 0, num_tokens = 0;
-  int32_t n_items_a = 0;  // items[0, n_items_a): phase A; the rest: phase B
+  // items[0, n_tile1): phase A, 16 columns per wave; then n_tile2 phase-A
+  // items with 32 columns per wave (extend); the rest: phase B.
+  int32_t n_tile1 = 0, n_tile2 = 0;
   std::vector<pfx::Item> items;
   std::vector<int32_t> row_tok, page_list, tok_req, tok_slot;
   std::vector<pfx::ReqInfo> req;

@@ -13,12 +13,12 @@
 // neither operand; each lane loads 8 keys x (D/16) dims and transposes them
 // in registers with byte permutes.
 //
-// Work is a list of items (see pfx_internal.h), run in two stream-ordered
-// launches.  Phase A: a workgroup of four waves runs one item -- the waves
-// take its 32-key steps round-robin, each with all of the item's query
-// columns, and combine their softmax states through LDS; the item writes
-// either final rows (extend) or a partial result over its key range (a
-// prefix chunk shared by an agent's decode rows, or an early suffix chunk).
+// Work is a list of items (see pfx_internal.h), run in stream-ordered
+// launches.  Phase A: a workgroup of four waves runs one item; the item's
+// K/V streams once through an LDS ring and every wave multiplies it against
+// its own query columns (16 or 32 of them); the item writes either final
+// rows (extend) or a partial result over its key range (a prefix chunk
+// shared by an agent's decode rows, or an early suffix chunk).
 // Phase B: one wave per (decode request, KV head) streams the last suffix
 // chunk and merges the request's phase-A partials in registers
 // (log-sum-exp merge) before writing the final rows.  The launch boundary
@@ -282,36 +282,228 @@ __device__ __forceinline__ void merge_row8(const float* o_row, size_t o_stride, 
   if (lse_out) *lse_out = mx + logf(z);
 }
 
-template <int D, int QB>
-__global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
+// ---------------------------------------------------------------------------
+// Phase A: LDS-staged tiles shared by the four waves of a workgroup.
+//
+// A step's K/V (two 16-token pages of one KV head, K and V) is copied from
+// the pool straight into LDS with global_load_lds_dwordx4 -- no registers
+// involved -- through a ring of kStages buffers, so kStages - 1 steps are in
+// flight while one is consumed.  Each wave loads one quarter of a step (one
+// page of K or of V) and consumes all of it for its own query columns; a
+// barrier per step publishes the stage and frees the one to be refilled.
+// Inside a page tile the 16-byte chunk c of token t sits at slot
+// t * chunks + (c ^ t): the MFMA operand reads (16 tokens at one chunk, or
+// one token's 16 chunks) then fall in 16 different bank groups.
+// ---------------------------------------------------------------------------
+constexpr int kStages = 4;
+
+template <int D>
+struct TileGeom {
+  static constexpr int chunks = D / 8;                 // 16-byte chunks per token row
+  static constexpr int page_bytes = 16 * D * 2;        // one (page, KV head) block
+  static constexpr int stage_bytes = 4 * page_bytes;   // K tile 0, K tile 1, V tile 0, V tile 1
+  static constexpr int loads_per_wave = page_bytes / 1024;
+};
+
+__device__ __forceinline__ int swizzled_slot(int t, int c, int chunks) { return t * chunks + (c ^ (t & (chunks - 1))); }
+
+// Wait until at most n of this wave's vector-memory operations are pending.
+__device__ __forceinline__ void wait_vmcnt(int n) {
+  // s_waitcnt encoding on gfx9: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] at [15:14].
+#define PFX_VMCNT(N) __builtin_amdgcn_s_waitcnt(((N) & 15) | (7 << 4) | (15 << 8) | (((N) >> 4) << 14))
+  switch (n) {
+    case 0: PFX_VMCNT(0); break;
+    case 1: PFX_VMCNT(1); break;
+    case 2: PFX_VMCNT(2); break;
+    case 3: PFX_VMCNT(3); break;
+    case 4: PFX_VMCNT(4); break;
+    case 5: PFX_VMCNT(5); break;
+    case 6: PFX_VMCNT(6); break;
+    case 7: PFX_VMCNT(7); break;
+    default: PFX_VMCNT(8); break;
+  }
+#undef PFX_VMCNT
+}
+
+typedef __attribute__((address_space(3))) unsigned char* lds_bytes;
+
+// Copy 16 bytes per lane from global memory into LDS at lds_addr + 16 * lane
+// (global_load_lds_dwordx4; M0 holds the wave-uniform LDS address).  Issued
+// through asm so the compiler's wait insertion does not treat every later
+// LDS read as dependent on every copy in flight: completion is awaited
+// explicitly with wait_vmcnt before the barrier that publishes a stage.
+// M0 is otherwise unused by these kernels (tests/test_build_checks.py checks
+// the generated code for that).
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void copy16_to_lds(const void* src, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds_addr) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+__device__ __forceinline__ uint32_t lds_address(const unsigned char* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_bytes)(p)));
+}
+
+// Issue this wave's share of step st into a stage buffer.
+template <int D>
+__device__ __forceinline__ void issue_tile(unsigned char* stage, const AttnArgs& a, const Item& it, const int* ptab,
+                                           int p0n, int st, int s0_steps, int h, int wave, int lane) {
+  using TG = TileGeom<D>;
+  const StepPos p = step_pos(it, st, s0_steps);
+  const int t = wave & 1;
+  const bool is_v = wave >> 1;
+  const int seg_base = p.seg == 0 ? it.s0_kbeg : it.s1_kbeg;
+  int idx = (p.seg == 0 ? 0 : p0n) + ((p.k0 - seg_base) >> 4);
+  if (t == 1 && p.k0 + 16 < p.kend) idx += 1;  // a missing second page re-reads the first (masked later)
+  const int page = ptab[idx];
+  const uint16_t* base = (is_v ? a.vpool : a.kpool) + (size_t(page) * a.hkv + h) * (16 * D);
+  const uint32_t dst = lds_address(stage) + wave * TG::page_bytes;
+#pragma unroll
+  for (int j = 0; j < TG::loads_per_wave; ++j) {
+    const int q = 64 * j + lane;
+    const int tt = q / TG::chunks;
+    const int cc = (q % TG::chunks) ^ (tt & (TG::chunks - 1));
+    copy16_to_lds(base + tt * D + cc * 8, dst + 1024 * j);
+  }
+}
+
+// Read a stage into the register layout compute_step expects.
+template <int D>
+__device__ __forceinline__ void read_tile(KVRegs<D>& r, const unsigned char* stage, int col, int grp) {
+  using TG = TileGeom<D>;
+  constexpr int KS = D / 32;
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+      r.k[t][s] = *reinterpret_cast<const u32x4*>(stage + t * TG::page_bytes +
+                                                  16 * swizzled_slot(col, 4 * s + grp, TG::chunks));
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const unsigned char* vb = stage + (2 + t) * TG::page_bytes;
+      if constexpr (D == 128) {
+        r.v[t][i] = *reinterpret_cast<const u32x4*>(vb + 16 * swizzled_slot(4 * grp + i, col, TG::chunks));
+      } else {
+        r.v[t][i] = *reinterpret_cast<const u32x2*>(vb + 16 * swizzled_slot(4 * grp + i, col >> 1, TG::chunks) +
+                                                    8 * (col & 1));
+      }
+    }
+}
+
+// Normalise a wave's block and write it: final bf16 rows, or an fp32 partial.
+template <int D>
+__device__ __forceinline__ void write_block(const AttnArgs& a, const Item& it, const f32x4 (&acc)[D / 16], float m,
+                                            float l_lane, int c, int tok, int grp) {
+  constexpr int CH = D / 16;
+  float l = l_lane;
+  l += __shfl_xor(l, 16);
+  l += __shfl_xor(l, 32);
+  const int j = c >> a.group_shift;
+  if (j >= it.row_count) return;
+  const int g = c & (a.group - 1);
+  const int qh = it.kv_head * a.group + g;
+  const float inv = l > 0.f ? 1.0f / l : 0.f;
+  // A row can see none of a chunk's keys (a multi-row decode request whose
+  // later suffix chunk starts after its first row): O = 0, LSE = -inf,
+  // which the merge weighs with exp(-inf) = 0.
+  const float lse_nat = l > 0.f ? (m + log2f(l)) * kLn2 : -INFINITY;
+  if (it.out_slot < 0) {
+    uint16_t* out = a.o + (size_t(tok) * a.hq + qh) * D + 4 * CH * grp;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if constexpr (CH == 8) {
+        u32x4 w = {pack_bf16(acc[0][i] * inv, acc[1][i] * inv), pack_bf16(acc[2][i] * inv, acc[3][i] * inv),
+                   pack_bf16(acc[4][i] * inv, acc[5][i] * inv), pack_bf16(acc[6][i] * inv, acc[7][i] * inv)};
+        *reinterpret_cast<u32x4*>(out + CH * i) = w;
+      } else {
+        u32x2 w = {pack_bf16(acc[0][i] * inv, acc[1][i] * inv), pack_bf16(acc[2][i] * inv, acc[3][i] * inv)};
+        *reinterpret_cast<u32x2*>(out + CH * i) = w;
+      }
+    }
+    if (a.lse && grp == 0) a.lse[size_t(tok) * a.hq + qh] = lse_nat;
+  } else {
+    const int r = a.plan.tok_req[tok];
+    const ReqInfo ri = a.plan.req[r];
+    const size_t prow = size_t(ri.part_base) + size_t(it.out_slot) * ri.n + (tok - ri.q_start);
+    float* out = a.plan.o_part + (prow * a.hq + qh) * D + 4 * CH * grp;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int jj = 0; jj < CH; jj += 4) {
+        f32x4 v = {acc[jj][i] * inv, acc[jj + 1][i] * inv, acc[jj + 2][i] * inv, acc[jj + 3][i] * inv};
+        *reinterpret_cast<f32x4*>(out + CH * i + jj) = v;
+      }
+    if (grp == 0) a.plan.l_part[prow * a.hq + qh] = lse_nat;
+  }
+}
+
+// One step of a phase-A item: wait for this wave's copies of step st, meet
+// the other waves (stage st complete everywhere, stage st-1 consumed), refill
+// that freed stage with step st + kStages - 1, then multiply stage st.
+template <int D, int QBW>
+__device__ __forceinline__ void tile_step(WaveState<D, QBW>& ws, const bf16x8 (&qf)[QBW][D / 32], const int (&lim)[QBW],
+                                          const unsigned char* cur, unsigned char* refill, const AttnArgs& a,
+                                          const Item& it, const int* ptab, int p0n, int st, int s0_steps, int nsteps,
+                                          int nb, int h, int wave, int lane) {
+  using TG = TileGeom<D>;
+  const int ahead = nsteps - 1 - st < kStages - 2 ? nsteps - 1 - st : kStages - 2;
+  wait_vmcnt(ahead * TG::loads_per_wave);
+  __syncthreads();
+  if (st + kStages - 1 < nsteps) issue_tile<D>(refill, a, it, ptab, p0n, st + kStages - 1, s0_steps, h, wave, lane);
+  if (nb > 0) {
+    KVRegs<D> r;
+    read_tile<D>(r, cur, lane & 15, lane >> 4);
+    compute_step<D, QBW>(ws, r, qf, lim, step_pos(it, st, s0_steps), nb, lane >> 4, a.scale_log2);
+  }
+}
+
+template <int D, int QBW>
+__global__ __launch_bounds__(256, 2) void tile_kernel(AttnArgs a) {
+  using TG = TileGeom<D>;
   constexpr int KS = D / 32;
   constexpr int CH = D / 16;
-  constexpr int NCOL = QB * kTileCols;
-  // Cross-wave combination buffers.
-  __shared__ float red_o[kWaves][NCOL][D + 4];
-  __shared__ float red_m[kWaves][NCOL];
-  __shared__ float red_l[kWaves][NCOL];
+  __shared__ __attribute__((aligned(1024))) unsigned char ring0[TG::stage_bytes];
+  __shared__ __attribute__((aligned(1024))) unsigned char ring1[TG::stage_bytes];
+  __shared__ __attribute__((aligned(1024))) unsigned char ring2[TG::stage_bytes];
+  __shared__ __attribute__((aligned(1024))) unsigned char ring3[TG::stage_bytes];
+  __shared__ int ptab[kMaxTilePages];
+  static_assert(kStages == 4, "the step loop below is unrolled for four stages");
 
   const Item it = a.plan.items[a.item_base + blockIdx.x];
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
   const int h = it.kv_head;
   const int G = a.group;
-  const int nblk = it.nblk;
 
-  // Query operands and causal limits of this lane's columns.
-  bf16x8 qf[QB][KS];
-  int lim[QB];
+  // Page ids of both segments, staged once per item.
+  const int p0b = it.s0_kbeg >> 4;
+  const int p0n = it.s0_kend > it.s0_kbeg ? ((it.s0_kend + 15) >> 4) - p0b : 0;
+  const int p1b = it.s1_kbeg >> 4;
+  const int p1n = it.s1_kend > it.s1_kbeg ? ((it.s1_kend + 15) >> 4) - p1b : 0;
+  for (int i = threadIdx.x; i < p0n + p1n; i += 256)
+    ptab[i] = i < p0n ? a.plan.page_list[it.s0_page_off + p0b + i] : a.plan.page_list[it.s1_page_off + p1b + i - p0n];
+
+  // This wave's query columns: blocks wave*QBW .. wave*QBW + QBW - 1.
+  const int ncols = it.row_count * G;
+  int nb = (ncols - wave * QBW * kTileCols + kTileCols - 1) / kTileCols;
+  nb = nb < 0 ? 0 : (nb > QBW ? QBW : nb);
+  bf16x8 qf[QBW][KS];
+  int lim[QBW];
+  int tok_of[QBW];
 #pragma unroll
-  for (int b = 0; b < QB; ++b) {
-    const int c = b * kTileCols + col;
+  for (int b = 0; b < QBW; ++b) {
+    const int c = (wave * QBW + b) * kTileCols + col;
     int j = c >> a.group_shift;
     const int g = c & (G - 1);
-    if (j >= it.row_count) j = 0;  // padding column: a copy of the first token, never stored
+    if (j >= it.row_count) j = 0;
     const int tok = a.plan.row_tok[it.row_begin + j];
+    tok_of[b] = tok;
     lim[b] = tok + it.causal_base;
-    if (b < nblk) {
+    if (b < nb) {
       const uint16_t* qp = a.q + (size_t(tok) * a.hq + h * G + g) * D + 8 * grp;
 #pragma unroll
       for (int s = 0; s < KS; ++s) qf[b][s] = *reinterpret_cast<const bf16x8*>(qp + 32 * s);
@@ -320,127 +512,37 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
       for (int s = 0; s < KS; ++s) qf[b][s] = bf16x8{};
     }
   }
-
-  WaveState<D, QB> ws;
+  WaveState<D, QBW> ws;
 #pragma unroll
-  for (int b = 0; b < QB; ++b) {
+  for (int b = 0; b < QBW; ++b) {
     ws.m[b] = kNegBig;
     ws.l[b] = 0.f;
 #pragma unroll
     for (int jj = 0; jj < CH; ++jj) ws.acc[b][jj] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-
   const int s0_steps = (it.s0_kend - it.s0_kbeg + kStepKeys - 1) / kStepKeys;
   const int s1_steps = (it.s1_kend - it.s1_kbeg + kStepKeys - 1) / kStepKeys;
   const int nsteps = s0_steps + s1_steps;
+  __syncthreads();  // page table ready
 
-  // Two register buffers: the next step's K/V is in flight while the
-  // current one is multiplied.
-  KVRegs<D> bufA, bufB;
-  PageWindow win{0, -1, 0};
-  int st = wave;
-  if (st < nsteps) load_kv<D>(bufA, a, win, step_pos(it, st, s0_steps), h, lane);
-  while (st < nsteps) {
-    int nst = st + kWaves;
-    if (nst < nsteps) load_kv<D>(bufB, a, win, step_pos(it, nst, s0_steps), h, lane);
-    compute_step<D, QB>(ws, bufA, qf, lim, step_pos(it, st, s0_steps), nblk, grp, a.scale_log2);
-    st = nst;
-    if (st >= nsteps) break;
-    nst = st + kWaves;
-    if (nst < nsteps) load_kv<D>(bufA, a, win, step_pos(it, nst, s0_steps), h, lane);
-    compute_step<D, QB>(ws, bufB, qf, lim, step_pos(it, st, s0_steps), nblk, grp, a.scale_log2);
-    st = nst;
+  if (0 < nsteps) issue_tile<D>(ring0, a, it, ptab, p0n, 0, s0_steps, h, wave, lane);
+  if (1 < nsteps) issue_tile<D>(ring1, a, it, ptab, p0n, 1, s0_steps, h, wave, lane);
+  if (2 < nsteps) issue_tile<D>(ring2, a, it, ptab, p0n, 2, s0_steps, h, wave, lane);
+
+  for (int st = 0; st < nsteps; st += kStages) {
+    tile_step<D, QBW>(ws, qf, lim, ring0, ring3, a, it, ptab, p0n, st, s0_steps, nsteps, nb, h, wave, lane);
+    if (st + 1 >= nsteps) break;
+    tile_step<D, QBW>(ws, qf, lim, ring1, ring0, a, it, ptab, p0n, st + 1, s0_steps, nsteps, nb, h, wave, lane);
+    if (st + 2 >= nsteps) break;
+    tile_step<D, QBW>(ws, qf, lim, ring2, ring1, a, it, ptab, p0n, st + 2, s0_steps, nsteps, nb, h, wave, lane);
+    if (st + 3 >= nsteps) break;
+    tile_step<D, QBW>(ws, qf, lim, ring3, ring2, a, it, ptab, p0n, st + 3, s0_steps, nsteps, nb, h, wave, lane);
   }
 
-  // Per-wave state to LDS: unnormalised O, max and the column's sum.
 #pragma unroll
-  for (int b = 0; b < QB; ++b) {
-    if (b >= nblk) break;
-    float l = ws.l[b];
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
-    const int c = b * kTileCols + col;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int jj = 0; jj < CH; ++jj) red_o[wave][c][CH * (4 * grp + i) + jj] = ws.acc[b][jj][i];
-    if (grp == 0) {
-      red_m[wave][c] = ws.m[b];
-      red_l[wave][c] = l;
-    }
-  }
-  __syncthreads();
-
-  // Combine the waves: each thread owns one column and a slice of dims.
-  const int ncols = nblk * kTileCols;
-  constexpr int TPC = 256 / NCOL;      // threads per column
-  constexpr int SLICE = D / TPC;       // dims per thread (multiple of 8)
-  const bool partial = it.out_slot >= 0;
-  {
-    const int c = threadIdx.x / TPC;
-    const int d0 = (threadIdx.x - c * TPC) * SLICE;
-    const int j = c >> a.group_shift;
-    if (c < ncols && j < it.row_count) {
-      const int g = c & (G - 1);
-      const int qh = h * G + g;
-      float mx = kNegBig;
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) mx = fmaxf(mx, red_m[w][c]);
-      float wgt[kWaves];
-      float z = 0.f;
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) {
-        wgt[w] = fast_exp2(red_m[w][c] - mx);
-        z += wgt[w] * red_l[w][c];
-      }
-      // A row can see none of a chunk's keys (a multi-row decode request whose
-      // last suffix chunk starts after its first row): O = 0, LSE = -inf,
-      // which the merge weighs with exp(-inf) = 0.
-      const float inv = z > 0.f ? 1.0f / z : 0.f;
-      const float lse_nat = z > 0.f ? (mx + log2f(z)) * kLn2 : -INFINITY;
-      const int tok = a.plan.row_tok[it.row_begin + j];
-      if (!partial) {
-        uint16_t* out = a.o + (size_t(tok) * a.hq + qh) * D + d0;
-        constexpr int UNIT = SLICE >= 8 ? 8 : 4;
-#pragma unroll
-        for (int e = 0; e < SLICE; e += UNIT) {
-          float v[UNIT];
-#pragma unroll
-          for (int u = 0; u < UNIT; ++u) {
-            float s = 0.f;
-#pragma unroll
-            for (int w = 0; w < kWaves; ++w) s += wgt[w] * red_o[w][c][d0 + e + u];
-            v[u] = s * inv;
-          }
-          if constexpr (UNIT == 8) {
-            u32x4 ow = {pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]), pack_bf16(v[4], v[5]), pack_bf16(v[6], v[7])};
-            *reinterpret_cast<u32x4*>(out + e) = ow;
-          } else {
-            u32x2 ow = {pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3])};
-            *reinterpret_cast<u32x2*>(out + e) = ow;
-          }
-        }
-        if (a.lse && d0 == 0) a.lse[size_t(tok) * a.hq + qh] = lse_nat;
-      } else {
-        const int r = a.plan.tok_req[tok];
-        const ReqInfo ri = a.plan.req[r];
-        const size_t prow = size_t(ri.part_base) + size_t(it.out_slot) * ri.n + (tok - ri.q_start);
-        float* out = a.plan.o_part + (prow * a.hq + qh) * D + d0;
-#pragma unroll
-        for (int e = 0; e < SLICE; e += 4) {
-          f32x4 v;
-#pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            float s = 0.f;
-#pragma unroll
-            for (int w = 0; w < kWaves; ++w) s += wgt[w] * red_o[w][c][d0 + e + u];
-            v[u] = s * inv;
-          }
-          *reinterpret_cast<f32x4*>(out + e) = v;
-        }
-        if (d0 == 0) a.plan.l_part[prow * a.hq + qh] = lse_nat;
-      }
-    }
+  for (int b = 0; b < QBW; ++b) {
+    if (b >= nb) break;
+    write_block<D>(a, it, ws.acc[b], ws.m[b], ws.l[b], (wave * QBW + b) * kTileCols + col, tok_of[b], grp);
   }
 }
 
@@ -611,13 +713,18 @@ static int check_pool_matches(const pfx_pool* pool, const pfx_plan* p, const cha
 }
 
 template <int D>
-static void launch_phases(AttnArgs a, int n_a, int n_b, hipStream_t s) {
-  if (n_a) {
+static void launch_phases(AttnArgs a, const pfx_plan* p, hipStream_t s) {
+  if (p->n_tile1) {
     a.item_base = 0;
-    hipLaunchKernelGGL((attn_kernel<D, kMaxBlocks>), dim3(n_a), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((tile_kernel<D, 1>), dim3(p->n_tile1), dim3(256), 0, s, a);
   }
+  if (p->n_tile2) {
+    a.item_base = p->n_tile1;
+    hipLaunchKernelGGL((tile_kernel<D, 2>), dim3(p->n_tile2), dim3(256), 0, s, a);
+  }
+  const int n_b = static_cast<int>(p->items.size()) - p->n_tile1 - p->n_tile2;
   if (n_b) {
-    a.item_base = n_a;
+    a.item_base = p->n_tile1 + p->n_tile2;
     hipLaunchKernelGGL((attn_final_kernel<D>), dim3(n_b), dim3(64), 0, s, a);
   }
 }
@@ -682,9 +789,7 @@ extern "C" int pfx_attention(const pfx_pool* pool, const pfx_plan* p, const void
   a.group_shift = __builtin_ctz(static_cast<unsigned>(p->group));
   a.scale_log2 = sm_scale * kLog2e;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const int n_a = p->n_items_a;
-  const int n_b = static_cast<int>(p->items.size()) - n_a;
-  if (p->d == 128) launch_phases<128>(a, n_a, n_b, s); else launch_phases<64>(a, n_a, n_b, s);
+  if (p->d == 128) launch_phases<128>(a, p, s); else launch_phases<64>(a, p, s);
   return check_launch("pfx_attention");
 }
 

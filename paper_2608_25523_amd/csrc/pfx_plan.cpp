@@ -169,6 +169,8 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
     if (opts->suffix_chunk < 0 || opts->suffix_chunk % kStepKeys)
       return fail(PFX_EINVAL, "pfx_plan_create: suffix_chunk %d is not a multiple of %d", opts->suffix_chunk,
                   kStepKeys);
+    if (opts->prefix_chunk > kMaxTilePages * PFX_PAGE_SIZE || opts->suffix_chunk > kMaxTilePages * PFX_PAGE_SIZE)
+      return fail(PFX_EUNSUPPORTED, "pfx_plan_create: chunks are limited to %d keys", kMaxTilePages * PFX_PAGE_SIZE);
     if (opts->prefix_chunk) pchunk = opts->prefix_chunk;
     if (opts->suffix_chunk) schunk = opts->suffix_chunk;
   }
@@ -215,6 +217,18 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   if (total_tokens > (int64_t(1) << 30)) return fail(PFX_ERANGE, "pfx_plan_create: too many query rows");
   if (R > 0 && b->suffix_indptr[R] > 0 && !b->suffix_page_ids)
     return fail(PFX_EINVAL, "pfx_plan_create: suffix_page_ids is NULL");
+
+  // An extend row block streams its agent's whole prefix and its suffix in
+  // one workgroup whose page table holds kMaxTilePages ids.
+  for (int32_t r = 0; r < R; ++r) {
+    const int64_t n = int64_t(b->q_indptr[r + 1]) - b->q_indptr[r];
+    if (n * G <= kTileCols) continue;
+    const int32_t a = b->agent[r];
+    const int64_t pages = (a >= 0 ? pages_for(pt->prefix_len[a]) : 0) + pages_for(b->suffix_len[r]);
+    if (pages > kMaxTilePages)
+      return fail(PFX_EUNSUPPORTED, "pfx_plan_create: request %d extends over %lld pages (at most %d)", r,
+                  (long long)pages, kMaxTilePages);
+  }
 
   // ---- Sec. 3, Eq. (2): prefixes counted once, plus every request's own KV ----
   std::vector<uint8_t> referenced(A, 0);
@@ -284,7 +298,6 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
     }
   }
 
-  const int32_t max_cols = kTileCols * kMaxBlocks;
   auto is_decode_class = [&](int32_t r) {
     int32_t n = p->req[r].n;
     return n >= 1 && n * G <= kTileCols;
@@ -308,10 +321,10 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
     const int32_t nc = nchunks(P, pchunk);
     struct RowBlock { int32_t begin, tokens; };
     std::vector<RowBlock> blocks;
-    int32_t cols = max_cols;  // forces a new block at the first member
+    int32_t cols = kDecodeTileCols;  // forces a new block at the first member
     for (int32_t r : members) {
       int32_t n = p->req[r].n;
-      if (cols + n * G > max_cols) {
+      if (cols + n * G > kDecodeTileCols) {
         blocks.push_back(RowBlock{static_cast<int32_t>(p->row_tok.size()), 0});
         cols = 0;
       }
@@ -396,7 +409,7 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
     const int32_t a = b->agent[r];
     const int32_t P = a >= 0 ? pt->prefix_len[a] : 0;
     const int32_t L = b->suffix_len[r];
-    const int32_t per = max_cols / G;
+    const int32_t per = kExtendTileCols / G;
     for (int32_t i0 = 0; i0 < ri.n; i0 += per) {
       const int32_t i1 = std::min(ri.n, i0 + per);
       const int32_t rbeg = static_cast<int32_t>(p->row_tok.size());
@@ -426,16 +439,23 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
     return delete p, fail(PFX_ERANGE, "pfx_plan_create: too many partial rows");
   p->num_part_rows = part_rows;
 
-  // Phase A (four-wave workgroups): longest key ranges first so the tail
-  // stays short.  Phase B (one-wave workgroups) runs after phase A on the
-  // same stream, so every partial it merges is complete and visible.
-  auto cost = [](const Item& it) {
-    return int64_t(it.s0_kend - it.s0_kbeg + it.s1_kend - it.s1_kbeg) * (it.nblk + 1);
-  };
+  // Phase A runs as two launches -- 16 columns per wave (decode prefix
+  // pieces, early suffix chunks), then 32 columns per wave (extend blocks)
+  // -- and phase B after both on the same stream, so every partial it
+  // merges is complete and visible.  Longest key ranges go first inside
+  // each launch so the tail stays short.
+  auto cost = [](const Item& it) { return int64_t(it.s0_kend - it.s0_kbeg + it.s1_kend - it.s1_kbeg); };
   auto by_cost = [&](const Item& x, const Item& y) { return cost(x) > cost(y); };
-  std::stable_sort(items.begin(), items.end(), by_cost);
+  std::vector<Item> tile1, tile2;
+  for (const Item& it : items) (it.kind == kExtendItem ? tile2 : tile1).push_back(it);
+  std::stable_sort(tile1.begin(), tile1.end(), by_cost);
+  std::stable_sort(tile2.begin(), tile2.end(), by_cost);
   std::stable_sort(final_items.begin(), final_items.end(), by_cost);
-  p->n_items_a = static_cast<int32_t>(items.size());
+  p->n_tile1 = static_cast<int32_t>(tile1.size());
+  p->n_tile2 = static_cast<int32_t>(tile2.size());
+  items.clear();
+  items.insert(items.end(), tile1.begin(), tile1.end());
+  items.insert(items.end(), tile2.begin(), tile2.end());
   items.insert(items.end(), final_items.begin(), final_items.end());
   p->items = std::move(items);
 

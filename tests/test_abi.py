@@ -161,7 +161,7 @@ def enumerate_coverage(plan, batch):
     slots = {}
     for it in items:
         (h, rb, rc, nblk, s0p, s0b, s0e, s1p, s1b, s1e, cbase, slot, kind, req, _, _) = it
-        assert 1 <= nblk <= 4 and rc * G <= nblk * 16 and (rc * G > (nblk - 1) * 16)
+        assert 1 <= nblk <= 8 and rc * G <= nblk * 16 and (rc * G > (nblk - 1) * 16)
         for j in range(rc):
             tok = int(row_tok[rb + j])
             r = int(tok_req[tok])
@@ -257,7 +257,7 @@ def test_config_plans_build_and_group_prefixes():
             assert s.num_extend_items == 0
         if cfg == 3:
             assert s.num_prefix_items == 0 and s.num_suffix_items == 0
-            assert s.num_extend_items == sum((int(n) + 15) // 16 for n in b.n_rows) * 8
+            assert s.num_extend_items == sum((int(n) + 31) // 32 for n in b.n_rows) * 8
 
 
 def test_upload_rejects_small_workspace_without_gpu_work():
