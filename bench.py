@@ -110,8 +110,10 @@ def bench_extend(args, torch, B, RN, W):
     return dict(ms=ms, attn_ms=attn_ms, flops=b.attention_flops(), steps=steps)
 
 
-def cpu_baseline(res, W):
-    """The fp64 oracle on a bounded sample of the decode step, on this host."""
+def cpu_baseline(res, W, seconds=12.0):
+    """The fp64 oracle, as it stands, on a bounded sample of the decode step:
+    whole requests (all heads) in request order, repeated until ``seconds``
+    of CPU work; throughput in unique KV bytes per second."""
     import numpy as np
 
     import oracle
@@ -122,26 +124,63 @@ def cpu_baseline(res, W):
     pp = [np.array([index[int(p)] for p in pl]) for pl in b.prefix_pages]
     sp = [np.array([index[int(p)] for p in pl]) for pl in b.suffix_pages]
     kp, vp = oracle.append_kv(hv.k_pages, hv.v_pages, sp, b.suffix_len, b.n_rows, hv.k_new, hv.v_new)
+    tau = b.num_kv_heads * b.head_dim * 4
+    per_agent = {int(a): int(np.sum(b.agent == a)) for a in set(b.agent.tolist())}
     t0 = time.perf_counter()
     done = 0
-    nbytes = 0
-    tau = b.num_kv_heads * b.head_dim * 4
-    for r in range(len(b.agent)):
+    nbytes = 0.0
+    while time.perf_counter() - t0 < seconds:
+        r = done % len(b.agent)
         oracle.prefix_shared_attention(kp, vp, pp, b.prefix_len, b.agent, sp, b.suffix_len, b.n_rows, hv.q,
                                        b.num_q_heads, rows={r: [0]})
-        done += 1
-        # bytes the request reads: its agent's prefix (shared, counted once per
-        # request here as the oracle re-reads it) is not unique work, so count
-        # the unique share: suffix + prefix / requests-per-agent
+        # the request's unique share: its own suffix plus its agent's prefix
+        # divided among the agent's requests (summing to U over the batch)
         a = int(b.agent[r])
-        share = int(b.prefix_len[a]) / int(np.sum(b.agent == a))
-        nbytes += (int(b.suffix_len[r]) + share) * tau
-        if time.perf_counter() - t0 > 20.0:
-            break
+        nbytes += (int(b.suffix_len[r]) + int(b.prefix_len[a]) / per_agent[a]) * tau
+        done += 1
     dt = time.perf_counter() - t0
+    threads = os.environ.get("OMP_NUM_THREADS", "unset")
     return {"value": round(nbytes / dt / 1e9, 4), "unit": "GB/s", "cores": cores, "kind": "oracle",
-            "sample": f"{done} of {len(b.agent)} decode requests of the decode-8B step (all 32 heads each), "
-                      f"fp64 numpy oracle, {dt:.1f} s; unique-KV-byte share per request"}
+            "sample": f"{done} decode requests (all 32 heads each; the 64-request decode-8B step cycled) in "
+                      f"{dt:.1f} s, fp64 numpy oracle, BLAS threads {threads}"}
+
+
+def copy_calibration(torch, B):
+    """A plain device-to-device copy of known size through pfx_page_copy
+    (used to scale the HBM byte counters read by rocprofv3)."""
+    import numpy as np
+
+    pages = 16384                      # 16384 pages x 32 KiB x (K + V) = 1 GiB read, 1 GiB written
+    shape = (pages, 8, 16, 128)
+    src_k = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
+    src_v = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
+    dst_k = torch.empty_like(src_k)
+    dst_v = torch.empty_like(src_v)
+    ids = np.arange(pages, dtype=np.int32)
+    ws = torch.empty(B.pfx_page_copy_workspace_bytes(pages) + 256, dtype=torch.uint8, device="cuda")
+    src = B.make_pool(pages, 8, 128, src_k, src_v)
+    dst = B.make_pool(pages, 8, 128, dst_k, dst_v)
+    for _ in range(3):
+        B.pfx_page_copy(dst, src, ids, ids, ws)
+    torch.cuda.synchronize()
+    return 2 * pages * 8 * 16 * 128 * 2
+
+
+def traffic_from_profile(kind):
+    """HBM bytes per launch from the committed counter summary, if it was
+    taken with the kernel source as it is now; else None."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    src = os.path.join(ROOT, "paper_2608_25523_amd", "csrc", "pfx_kernels.hip")
+    try:
+        rec = json.load(open(path))
+        digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_sha256") != digest:
+        return None
+    return rec.get(kind, {}).get("bytes_per_step")
 
 
 def main():
@@ -152,6 +191,8 @@ def main():
     ap.add_argument("--replicas", type=int, default=10)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-extend", action="store_true")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="also run a 1 GiB device copy (counter calibration for rocprofv3 --pmc runs)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}), flush=True)
@@ -164,6 +205,8 @@ def main():
     from paper_2608_25523_amd import workloads as W
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.calib_copy:
+        log(f"calibration copy: {copy_calibration(torch, B)} bytes moved per launch")
     log("decode-8B: building inputs")
     dec = bench_decode(args, torch, B, RN, W)
     log(f"decode-8B: {dec['ms'] * 1e3:.1f} us/step, attention {dec['attn_ms'] * 1e3:.1f} us")
@@ -200,7 +243,7 @@ def main():
                    "prefix_items": st.num_prefix_items, "suffix_items": st.num_suffix_items},
         "roofline": {"bound": "hbm", "kernel": "attn_kernel (pfx_attention)",
                      "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic_from_profile("decode"),
                      "attn_us": round(dec["attn_ms"] * 1e3, 3)},
         "cpu_baseline": cpu,
     }
@@ -212,7 +255,7 @@ def main():
             "ms_per_step": round(ext["ms"], 4), "steps": ext["steps"],
             "roofline": {"bound": "mfma", "kernel": "attn_kernel (pfx_attention)", "achieved": round(tf, 2),
                          "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(tf / BF16_PEAK_TFLOPS, 4),
-                         "traffic": None, "flops": ext["flops"]},
+                         "traffic": traffic_from_profile("extend"), "flops": ext["flops"]},
         }
     print(json.dumps(out), flush=True)
 

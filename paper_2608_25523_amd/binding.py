@@ -72,17 +72,17 @@ class pfx_plan_stats(C.Structure):
                 ("pages_needed", C.c_int32), ("workspace_bytes", C.c_int64)]
 
 
-def _load():
+def _load(path: str = LIB_PATH):
     # torch bundles its own HIP runtime with the same soname as the system
     # one.  Loading torch first makes this library bind to that same runtime,
     # so one process never holds two HIP runtimes (the second would find no
     # device).
     import torch  # noqa: F401
 
-    if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2608_25523_amd.build` "
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it with `python -m paper_2608_25523_amd.build` "
                           "(there is no CPU fallback)")
-    lib = C.CDLL(LIB_PATH)
+    lib = C.CDLL(path)
     P = C.c_void_p
     i32, i64, sz = C.c_int32, C.c_int64, C.c_size_t
     sig = {
@@ -177,7 +177,7 @@ class Allocator:
         return n.value
 
     def __del__(self):
-        if getattr(self, "h", None):
+        if getattr(self, "h", None) and LIB is not None:
             LIB.pfx_alloc_destroy(self.h)
             self.h = None
 
@@ -222,7 +222,7 @@ class Plan:
         return self
 
     def __del__(self):
-        if getattr(self, "h", None):
+        if getattr(self, "h", None) and LIB is not None:
             LIB.pfx_plan_destroy(self.h)
             self.h = None
 

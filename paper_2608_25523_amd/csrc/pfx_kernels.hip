@@ -295,6 +295,7 @@ __device__ __forceinline__ void merge_row8(const float* o_row, size_t o_stride, 
 // t * chunks + (c ^ t): the MFMA operand reads (16 tokens at one chunk, or
 // one token's 16 chunks) then fall in 16 different bank groups.
 // ---------------------------------------------------------------------------
+// Stages of the LDS ring (NS - 1 steps in flight per workgroup).
 constexpr int kStages = 4;
 
 template <int D>
@@ -320,7 +321,31 @@ __device__ __forceinline__ void wait_vmcnt(int n) {
     case 5: PFX_VMCNT(5); break;
     case 6: PFX_VMCNT(6); break;
     case 7: PFX_VMCNT(7); break;
-    default: PFX_VMCNT(8); break;
+    case 8: PFX_VMCNT(8); break;
+    case 9: PFX_VMCNT(9); break;
+    case 10: PFX_VMCNT(10); break;
+    case 11: PFX_VMCNT(11); break;
+    case 12: PFX_VMCNT(12); break;
+    case 13: PFX_VMCNT(13); break;
+    case 14: PFX_VMCNT(14); break;
+    case 15: PFX_VMCNT(15); break;
+    case 16: PFX_VMCNT(16); break;
+    case 17: PFX_VMCNT(17); break;
+    case 18: PFX_VMCNT(18); break;
+    case 19: PFX_VMCNT(19); break;
+    case 20: PFX_VMCNT(20); break;
+    case 21: PFX_VMCNT(21); break;
+    case 22: PFX_VMCNT(22); break;
+    case 23: PFX_VMCNT(23); break;
+    case 24: PFX_VMCNT(24); break;
+    case 25: PFX_VMCNT(25); break;
+    case 26: PFX_VMCNT(26); break;
+    case 27: PFX_VMCNT(27); break;
+    case 28: PFX_VMCNT(28); break;
+    case 29: PFX_VMCNT(29); break;
+    case 30: PFX_VMCNT(30); break;
+    case 31: PFX_VMCNT(31); break;
+    default: PFX_VMCNT(32); break;
   }
 #undef PFX_VMCNT
 }
@@ -443,16 +468,16 @@ __device__ __forceinline__ void write_block(const AttnArgs& a, const Item& it, c
 // One step of a phase-A item: wait for this wave's copies of step st, meet
 // the other waves (stage st complete everywhere, stage st-1 consumed), refill
 // that freed stage with step st + kStages - 1, then multiply stage st.
-template <int D, int QBW>
+template <int D, int QBW, int NS>
 __device__ __forceinline__ void tile_step(WaveState<D, QBW>& ws, const bf16x8 (&qf)[QBW][D / 32], const int (&lim)[QBW],
                                           const unsigned char* cur, unsigned char* refill, const AttnArgs& a,
                                           const Item& it, const int* ptab, int p0n, int st, int s0_steps, int nsteps,
                                           int nb, int h, int wave, int lane) {
   using TG = TileGeom<D>;
-  const int ahead = nsteps - 1 - st < kStages - 2 ? nsteps - 1 - st : kStages - 2;
+  const int ahead = nsteps - 1 - st < NS - 2 ? nsteps - 1 - st : NS - 2;
   wait_vmcnt(ahead * TG::loads_per_wave);
   __syncthreads();
-  if (st + kStages - 1 < nsteps) issue_tile<D>(refill, a, it, ptab, p0n, st + kStages - 1, s0_steps, h, wave, lane);
+  if (st + NS - 1 < nsteps) issue_tile<D>(refill, a, it, ptab, p0n, st + NS - 1, s0_steps, h, wave, lane);
   if (nb > 0) {
     KVRegs<D> r;
     read_tile<D>(r, cur, lane & 15, lane >> 4);
@@ -460,18 +485,13 @@ __device__ __forceinline__ void tile_step(WaveState<D, QBW>& ws, const bf16x8 (&
   }
 }
 
-template <int D, int QBW>
+template <int D, int QBW, int NS>
 __global__ __launch_bounds__(256, 2) void tile_kernel(AttnArgs a) {
   using TG = TileGeom<D>;
   constexpr int KS = D / 32;
   constexpr int CH = D / 16;
-  __shared__ __attribute__((aligned(1024))) unsigned char ring0[TG::stage_bytes];
-  __shared__ __attribute__((aligned(1024))) unsigned char ring1[TG::stage_bytes];
-  __shared__ __attribute__((aligned(1024))) unsigned char ring2[TG::stage_bytes];
-  __shared__ __attribute__((aligned(1024))) unsigned char ring3[TG::stage_bytes];
+  __shared__ __attribute__((aligned(1024))) unsigned char ring[NS][TG::stage_bytes];
   __shared__ int ptab[kMaxTilePages];
-  static_assert(kStages == 4, "the step loop below is unrolled for four stages");
-
   const Item it = a.plan.items[a.item_base + blockIdx.x];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
@@ -525,19 +545,11 @@ __global__ __launch_bounds__(256, 2) void tile_kernel(AttnArgs a) {
   const int nsteps = s0_steps + s1_steps;
   __syncthreads();  // page table ready
 
-  if (0 < nsteps) issue_tile<D>(ring0, a, it, ptab, p0n, 0, s0_steps, h, wave, lane);
-  if (1 < nsteps) issue_tile<D>(ring1, a, it, ptab, p0n, 1, s0_steps, h, wave, lane);
-  if (2 < nsteps) issue_tile<D>(ring2, a, it, ptab, p0n, 2, s0_steps, h, wave, lane);
-
-  for (int st = 0; st < nsteps; st += kStages) {
-    tile_step<D, QBW>(ws, qf, lim, ring0, ring3, a, it, ptab, p0n, st, s0_steps, nsteps, nb, h, wave, lane);
-    if (st + 1 >= nsteps) break;
-    tile_step<D, QBW>(ws, qf, lim, ring1, ring0, a, it, ptab, p0n, st + 1, s0_steps, nsteps, nb, h, wave, lane);
-    if (st + 2 >= nsteps) break;
-    tile_step<D, QBW>(ws, qf, lim, ring2, ring1, a, it, ptab, p0n, st + 2, s0_steps, nsteps, nb, h, wave, lane);
-    if (st + 3 >= nsteps) break;
-    tile_step<D, QBW>(ws, qf, lim, ring3, ring2, a, it, ptab, p0n, st + 3, s0_steps, nsteps, nb, h, wave, lane);
-  }
+  for (int st = 0; st < NS - 1 && st < nsteps; ++st)
+    issue_tile<D>(ring[st], a, it, ptab, p0n, st, s0_steps, h, wave, lane);
+  for (int st = 0; st < nsteps; ++st)
+    tile_step<D, QBW, NS>(ws, qf, lim, ring[st % NS], ring[(st + NS - 1) % NS], a, it, ptab, p0n, st, s0_steps,
+                          nsteps, nb, h, wave, lane);
 
 #pragma unroll
   for (int b = 0; b < QBW; ++b) {
@@ -716,11 +728,11 @@ template <int D>
 static void launch_phases(AttnArgs a, const pfx_plan* p, hipStream_t s) {
   if (p->n_tile1) {
     a.item_base = 0;
-    hipLaunchKernelGGL((tile_kernel<D, 1>), dim3(p->n_tile1), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((tile_kernel<D, 1, kStages>), dim3(p->n_tile1), dim3(256), 0, s, a);
   }
   if (p->n_tile2) {
     a.item_base = p->n_tile1;
-    hipLaunchKernelGGL((tile_kernel<D, 2>), dim3(p->n_tile2), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((tile_kernel<D, 2, kStages>), dim3(p->n_tile2), dim3(256), 0, s, a);
   }
   const int n_b = static_cast<int>(p->items.size()) - p->n_tile1 - p->n_tile2;
   if (n_b) {
