@@ -19,9 +19,10 @@
 // its own query columns (16 or 32 of them); the item writes either final
 // rows (extend) or a partial result over its key range (a prefix chunk
 // shared by an agent's decode rows, or an early suffix chunk).
-// Phase B: one wave per (decode request, KV head) streams the last suffix
-// chunk and merges the request's phase-A partials in registers
-// (log-sum-exp merge) before writing the final rows.  The launch boundary
+// Phase B: one workgroup per (decode request, KV head) streams the last
+// suffix chunk, its four waves splitting the steps, and merges their states
+// with the request's phase-A partials (log-sum-exp merge) through LDS
+// before writing the final rows.  The launch boundary
 // orders the two phases, so no atomics or device-wide fences are needed.
 #include <hip/hip_runtime.h>
 
@@ -179,51 +180,78 @@ struct WaveState {
   float l[QB];        // this lane's share of the running sum
 };
 
-template <int D, int QB>
-__device__ __forceinline__ void compute_step(WaveState<D, QB>& ws, KVRegs<D>& r, const bf16x8 (&qf)[QB][D / 32],
-                                             const int (&lim)[QB], const StepPos& p, int nblk, int grp,
-                                             float scale_log2) {
+// NSUB consecutive 32-key steps against the wave's query blocks, with one
+// online-softmax update for all of them: the NSUB score chains are
+// independent (instruction-level parallelism for a lone wave), and the
+// cross-lane max and the rescale check are paid once per NSUB * 32 keys.
+// Steps u >= nvalid are skipped.
+template <int D, int QB, int NSUB>
+__device__ __forceinline__ void compute_steps(WaveState<D, QB>& ws, KVRegs<D>* const (&rp)[NSUB],
+                                              const bf16x8 (&qf)[QB][D / 32], const int (&lim)[QB],
+                                              const StepPos (&p)[NSUB], int nvalid, int nblk, int grp,
+                                              float scale_log2) {
   constexpr int KS = D / 32;
   constexpr int CH = D / 16;
-  const bool tail = p.k0 + kStepKeys > p.kend;
-  if (tail) {
-    // Keys past the end of the segment: zero their V (the slots may hold
-    // anything) -- their probabilities are forced to 0 below.
+  bool any_mask = false;
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (p.k0 + 16 * t + 4 * grp + i >= p.kend) r.v[t][i] = typename VecCH<D>::T{};
-  }
-  const bool need_mask = tail || p.seg == 1;
-#pragma unroll
-  for (int b = 0; b < QB; ++b) {
-    if (b >= nblk) break;
-    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, r.k[0][s]), qf[b][s], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, r.k[1][s]), qf[b][s], s1, 0, 0, 0);
-    }
-    float x[8];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      x[i] = s0[i] * scale_log2;
-      x[4 + i] = s1[i] * scale_log2;
-    }
-    if (need_mask) {
-      const int lim_b = p.seg == 1 ? lim[b] : 0x7fffffff;
+  for (int u = 0; u < NSUB; ++u) {
+    if (u >= nvalid) break;
+    const bool tail = p[u].k0 + kStepKeys > p[u].kend;
+    any_mask |= tail || p[u].seg == 1;
+    if (tail) {
+      // Keys past the end of the segment: zero their V (the slots may hold
+      // anything) -- their probabilities are forced to 0 below.
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int key = p.k0 + 16 * t + 4 * grp + i;
-          if (key >= p.kend || key > lim_b) x[4 * t + i] = -INFINITY;
-        }
+        for (int i = 0; i < 4; ++i)
+          if (p[u].k0 + 16 * t + 4 * grp + i >= p[u].kend) rp[u]->v[t][i] = typename VecCH<D>::T{};
     }
-    float mx = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+  }
+#pragma unroll
+  for (int b = 0; b < QB; ++b) {
+    if (b >= nblk) break;
+    // Raw scores s = q.k; lane holds keys 16t + 4*grp + i of each step.
+    float sc[NSUB][8];
+#pragma unroll
+    for (int u = 0; u < NSUB; ++u) {
+      if (u >= nvalid) break;
+      f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, rp[u]->k[0][s]), qf[b][s], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, rp[u]->k[1][s]), qf[b][s], s1, 0, 0, 0);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        sc[u][i] = s0[i];
+        sc[u][4 + i] = s1[i];
+      }
+    }
+    if (any_mask) {
+#pragma unroll
+      for (int u = 0; u < NSUB; ++u) {
+        if (u >= nvalid) break;
+        const int lim_b = p[u].seg == 1 ? lim[b] : 0x7fffffff;
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int key = p[u].k0 + 16 * t + 4 * grp + i;
+            if (key >= p[u].kend || key > lim_b) sc[u][4 * t + i] = -INFINITY;
+          }
+      }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < NSUB; ++u) {
+      if (u >= nvalid) break;
+      mx = fmaxf(mx, fmaxf(fmaxf(fmaxf(sc[u][0], sc[u][1]), fmaxf(sc[u][2], sc[u][3])),
+                           fmaxf(fmaxf(sc[u][4], sc[u][5]), fmaxf(sc[u][6], sc[u][7]))));
+    }
     mx = fmaxf(mx, __shfl_xor(mx, 16));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
+    mx *= scale_log2;  // scale > 0: max of the scaled scores
     const bool raise = mx > ws.m[b] + kRescaleSlack;
     if (__any(raise)) {
       const float mnew = raise ? mx : ws.m[b];
@@ -233,24 +261,36 @@ __device__ __forceinline__ void compute_step(WaveState<D, QB>& ws, KVRegs<D>& r,
       for (int jj = 0; jj < CH; ++jj) ws.acc[b][jj] *= alpha;
       ws.m[b] = mnew;
     }
-    float pr[8];
-    float psum = 0.f;
+    const float neg_m = -ws.m[b];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      pr[j] = fast_exp2(x[j] - ws.m[b]);
-      psum += pr[j];
+    for (int u = 0; u < NSUB; ++u) {
+      if (u >= nvalid) break;
+      float pr[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        pr[j] = fast_exp2(fmaf(sc[u][j], scale_log2, neg_m));
+        ws.l[b] += pr[j];
+      }
+      u32x4 pw;
+      pw[0] = pack_bf16(pr[0], pr[1]);
+      pw[1] = pack_bf16(pr[2], pr[3]);
+      pw[2] = pack_bf16(pr[4], pr[5]);
+      pw[3] = pack_bf16(pr[6], pr[7]);
+      const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
+#pragma unroll
+      for (int jj = 0; jj < CH; ++jj)
+        ws.acc[b][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v_operand<D>(*rp[u], jj), pb, ws.acc[b][jj], 0, 0, 0);
     }
-    ws.l[b] += psum;
-    u32x4 pw;
-    pw[0] = pack_bf16(pr[0], pr[1]);
-    pw[1] = pack_bf16(pr[2], pr[3]);
-    pw[2] = pack_bf16(pr[4], pr[5]);
-    pw[3] = pack_bf16(pr[6], pr[7]);
-    const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
-#pragma unroll
-    for (int jj = 0; jj < CH; ++jj)
-      ws.acc[b][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v_operand<D>(r, jj), pb, ws.acc[b][jj], 0, 0, 0);
   }
+}
+
+template <int D, int QB>
+__device__ __forceinline__ void compute_step(WaveState<D, QB>& ws, KVRegs<D>& r, const bf16x8 (&qf)[QB][D / 32],
+                                             const int (&lim)[QB], const StepPos& p, int nblk, int grp,
+                                             float scale_log2) {
+  KVRegs<D>* const one[1] = {&r};
+  const StepPos pos[1] = {p};
+  compute_steps<D, QB, 1>(ws, one, qf, lim, pos, 1, nblk, grp, scale_log2);
 }
 
 // Merge `nparts` partial results for 8 consecutive dims of one row:
@@ -295,8 +335,11 @@ __device__ __forceinline__ void merge_row8(const float* o_row, size_t o_stride, 
 // t * chunks + (c ^ t): the MFMA operand reads (16 tokens at one chunk, or
 // one token's 16 chunks) then fall in 16 different bank groups.
 // ---------------------------------------------------------------------------
-// Stages of the LDS ring (NS - 1 steps in flight per workgroup).
+// Stages of the LDS ring: extend workgroups (one wave group) keep 3 steps in
+// flight; decode prefix workgroups (two groups taking alternate steps) keep
+// two rounds of two steps in flight.
 constexpr int kStages = 4;
+constexpr int kDecodeStages = 6;
 
 template <int D>
 struct TileGeom {
@@ -468,32 +511,47 @@ __device__ __forceinline__ void write_block(const AttnArgs& a, const Item& it, c
 // One step of a phase-A item: wait for this wave's copies of step st, meet
 // the other waves (stage st complete everywhere, stage st-1 consumed), refill
 // that freed stage with step st + kStages - 1, then multiply stage st.
-template <int D, int QBW, int NS>
-__device__ __forceinline__ void tile_step(WaveState<D, QBW>& ws, const bf16x8 (&qf)[QBW][D / 32], const int (&lim)[QBW],
-                                          const unsigned char* cur, unsigned char* refill, const AttnArgs& a,
-                                          const Item& it, const int* ptab, int p0n, int st, int s0_steps, int nsteps,
-                                          int nb, int h, int wave, int lane) {
+// One round of a phase-A item: every wave waits for its own copies of the
+// round, all waves meet (the round's stages complete everywhere, the previous
+// round's stages consumed), the freed stages are refilled with the round
+// R - 1 ahead, and each wave group multiplies its own step of the round.
+template <int D, int QBW, int NS, int NG>
+__device__ __forceinline__ void tile_round(WaveState<D, QBW>& ws, const bf16x8 (&qf)[QBW][D / 32],
+                                           const int (&lim)[QBW], unsigned char (*ring)[TileGeom<D>::stage_bytes],
+                                           const AttnArgs& a, const Item& it, const int* ptab, int p0n, int r,
+                                           int s0_steps, int nsteps, int nb, int h, int g, int wq, int lane) {
   using TG = TileGeom<D>;
-  const int ahead = nsteps - 1 - st < NS - 2 ? nsteps - 1 - st : NS - 2;
-  wait_vmcnt(ahead * TG::loads_per_wave);
+  constexpr int R = NS / NG;  // rounds held by the ring
+  const int st = NG * r + g;  // this group's step in round r
+  const int last = (nsteps - 1 - g) / NG;  // this group's last round (negative: none)
+  const int ahead = last - r < R - 2 ? last - r : R - 2;
+  wait_vmcnt(ahead > 0 ? ahead * TG::loads_per_wave : 0);
   __syncthreads();
-  if (st + NS - 1 < nsteps) issue_tile<D>(refill, a, it, ptab, p0n, st + NS - 1, s0_steps, h, wave, lane);
-  if (nb > 0) {
-    KVRegs<D> r;
-    read_tile<D>(r, cur, lane & 15, lane >> 4);
-    compute_step<D, QBW>(ws, r, qf, lim, step_pos(it, st, s0_steps), nb, lane >> 4, a.scale_log2);
+  const int nxt = st + NG * (R - 1);
+  if (nxt < nsteps) issue_tile<D>(ring[nxt % NS], a, it, ptab, p0n, nxt, s0_steps, h, wq, lane);
+  if (nb > 0 && st < nsteps) {
+    KVRegs<D> kv;
+    read_tile<D>(kv, ring[st % NS], lane & 15, lane >> 4);
+    compute_step<D, QBW>(ws, kv, qf, lim, step_pos(it, st, s0_steps), nb, lane >> 4, a.scale_log2);
   }
 }
 
-template <int D, int QBW, int NS>
-__global__ __launch_bounds__(256, 2) void tile_kernel(AttnArgs a) {
+// Phase A kernel.  NG groups of four waves: the four waves of a group own
+// different query columns; the groups take alternate 32-key steps of the item
+// (more waves per SIMD without more partial results) and merge their
+// softmax states through LDS before the rows are written.
+template <int D, int QBW, int NS, int NG>
+__global__ __launch_bounds__(256 * NG, 2) void tile_kernel(AttnArgs a) {
   using TG = TileGeom<D>;
   constexpr int KS = D / 32;
   constexpr int CH = D / 16;
+  static_assert(NS % NG == 0 && NS / NG >= 2, "the ring holds whole rounds");
   __shared__ __attribute__((aligned(1024))) unsigned char ring[NS][TG::stage_bytes];
   __shared__ int ptab[kMaxTilePages];
   const Item it = a.plan.items[a.item_base + blockIdx.x];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = wave / kTileWaves;   // wave group: which steps
+  const int wq = wave % kTileWaves;  // role inside the group: which columns, which quarter of a stage
   const int lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
   const int h = it.kv_head;
@@ -504,27 +562,27 @@ __global__ __launch_bounds__(256, 2) void tile_kernel(AttnArgs a) {
   const int p0n = it.s0_kend > it.s0_kbeg ? ((it.s0_kend + 15) >> 4) - p0b : 0;
   const int p1b = it.s1_kbeg >> 4;
   const int p1n = it.s1_kend > it.s1_kbeg ? ((it.s1_kend + 15) >> 4) - p1b : 0;
-  for (int i = threadIdx.x; i < p0n + p1n; i += 256)
+  for (int i = threadIdx.x; i < p0n + p1n; i += 256 * NG)
     ptab[i] = i < p0n ? a.plan.page_list[it.s0_page_off + p0b + i] : a.plan.page_list[it.s1_page_off + p1b + i - p0n];
 
-  // This wave's query columns: blocks wave*QBW .. wave*QBW + QBW - 1.
+  // This wave's query columns: blocks wq*QBW .. wq*QBW + QBW - 1.
   const int ncols = it.row_count * G;
-  int nb = (ncols - wave * QBW * kTileCols + kTileCols - 1) / kTileCols;
+  int nb = (ncols - wq * QBW * kTileCols + kTileCols - 1) / kTileCols;
   nb = nb < 0 ? 0 : (nb > QBW ? QBW : nb);
   bf16x8 qf[QBW][KS];
   int lim[QBW];
   int tok_of[QBW];
 #pragma unroll
   for (int b = 0; b < QBW; ++b) {
-    const int c = (wave * QBW + b) * kTileCols + col;
+    const int c = (wq * QBW + b) * kTileCols + col;
     int j = c >> a.group_shift;
-    const int g = c & (G - 1);
+    const int gg = c & (G - 1);
     if (j >= it.row_count) j = 0;
     const int tok = a.plan.row_tok[it.row_begin + j];
     tok_of[b] = tok;
     lim[b] = tok + it.causal_base;
     if (b < nb) {
-      const uint16_t* qp = a.q + (size_t(tok) * a.hq + h * G + g) * D + 8 * grp;
+      const uint16_t* qp = a.q + (size_t(tok) * a.hq + h * G + gg) * D + 8 * grp;
 #pragma unroll
       for (int s = 0; s < KS; ++s) qf[b][s] = *reinterpret_cast<const bf16x8*>(qp + 32 * s);
     } else {
@@ -543,119 +601,215 @@ __global__ __launch_bounds__(256, 2) void tile_kernel(AttnArgs a) {
   const int s0_steps = (it.s0_kend - it.s0_kbeg + kStepKeys - 1) / kStepKeys;
   const int s1_steps = (it.s1_kend - it.s1_kbeg + kStepKeys - 1) / kStepKeys;
   const int nsteps = s0_steps + s1_steps;
+  const int rounds = (nsteps + NG - 1) / NG;
   __syncthreads();  // page table ready
 
-  for (int st = 0; st < NS - 1 && st < nsteps; ++st)
-    issue_tile<D>(ring[st], a, it, ptab, p0n, st, s0_steps, h, wave, lane);
-  for (int st = 0; st < nsteps; ++st)
-    tile_step<D, QBW, NS>(ws, qf, lim, ring[st % NS], ring[(st + NS - 1) % NS], a, it, ptab, p0n, st, s0_steps,
-                          nsteps, nb, h, wave, lane);
+  constexpr int R = NS / NG;
+  for (int r = 0; r < R - 1; ++r) {
+    const int st = NG * r + g;
+    if (st < nsteps) issue_tile<D>(ring[st % NS], a, it, ptab, p0n, st, s0_steps, h, wq, lane);
+  }
+  for (int r = 0; r < rounds; ++r)
+    tile_round<D, QBW, NS, NG>(ws, qf, lim, ring, a, it, ptab, p0n, r, s0_steps, nsteps, nb, h, g, wq, lane);
+
+  if constexpr (NG == 2) {
+    // Group 1 hands its state to group 0, lane for lane (same register layout).
+    constexpr int NV = QBW * (4 * CH + 2);
+    float* xch = reinterpret_cast<float*>(&ring[0][0]);  // kTileWaves * NV * 64 floats
+    static_assert(kTileWaves * NV * 64 * 4 <= NS * TG::stage_bytes, "exchange fits in the ring");
+    __syncthreads();  // ring no longer read
+    if (g == 1) {
+#pragma unroll
+      for (int b = 0; b < QBW; ++b) {
+        float* x = xch + ((wq * QBW + b) * (4 * CH + 2)) * 64 + lane;
+#pragma unroll
+        for (int jj = 0; jj < CH; ++jj)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) x[(4 * jj + i) * 64] = ws.acc[b][jj][i];
+        x[(4 * CH) * 64] = ws.m[b];
+        x[(4 * CH + 1) * 64] = ws.l[b];
+      }
+    }
+    __syncthreads();
+    if (g == 1) return;
+#pragma unroll
+    for (int b = 0; b < QBW; ++b) {
+      const float* x = xch + ((wq * QBW + b) * (4 * CH + 2)) * 64 + lane;
+      const float m1 = x[(4 * CH) * 64];
+      const float mn = fmaxf(ws.m[b], m1);
+      const float f0 = fast_exp2(ws.m[b] - mn), f1 = fast_exp2(m1 - mn);
+      ws.l[b] = ws.l[b] * f0 + x[(4 * CH + 1) * 64] * f1;
+#pragma unroll
+      for (int jj = 0; jj < CH; ++jj)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) ws.acc[b][jj][i] = ws.acc[b][jj][i] * f0 + x[(4 * jj + i) * 64] * f1;
+      ws.m[b] = mn;
+    }
+  }
 
 #pragma unroll
   for (int b = 0; b < QBW; ++b) {
     if (b >= nb) break;
-    write_block<D>(a, it, ws.acc[b], ws.m[b], ws.l[b], (wave * QBW + b) * kTileCols + col, tok_of[b], grp);
+    write_block<D>(a, it, ws.acc[b], ws.m[b], ws.l[b], (wq * QBW + b) * kTileCols + col, tok_of[b], grp);
   }
 }
 
-// Phase B: one wave per (decode request, KV head): the request's last suffix
-// chunk, merged with the partials phase A wrote for the same rows.
+// Phase B: one workgroup per (decode request, KV head).  Its four waves take
+// the request's last suffix chunk's 32-key steps round-robin (each with the
+// request's <= 16 query columns and its own softmax state), then combine
+// their states and the partials phase A wrote for the same rows through LDS
+// (log-sum-exp merge), and write the final rows.
 template <int D>
-__global__ __launch_bounds__(64, 2) void attn_final_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256, 2) void attn_final_kernel(AttnArgs a) {
   constexpr int KS = D / 32;
   constexpr int CH = D / 16;
+  constexpr int DS = D / 16;          // dims per thread in the combine
+  constexpr int kPrefetchParts = 2;   // phase-A partials fetched at the start
+  __shared__ float red_o[kTileWaves][kTileCols][D + 4];
+  __shared__ float red_m[kTileWaves][kTileCols];
+  __shared__ float red_l[kTileWaves][kTileCols];
   const Item it = a.plan.items[a.item_base + blockIdx.x];
-  const int lane = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
   const int h = it.kv_head;
   const int G = a.group;
-  int j = col >> a.group_shift;
-  const int g = col & (G - 1);
-  const bool valid = j < it.row_count;
-  if (!valid) j = 0;
-  const int tok = a.plan.row_tok[it.row_begin + j];
-  const int qh = h * G + g;
-  bf16x8 qf[1][KS];
-  int lim[1] = {tok + it.causal_base};
-  {
-    const uint16_t* qp = a.q + (size_t(tok) * a.hq + qh) * D + 8 * grp;
-#pragma unroll
-    for (int s = 0; s < KS; ++s) qf[0][s] = *reinterpret_cast<const bf16x8*>(qp + 32 * s);
-  }
-  WaveState<D, 1> ws;
-  ws.m[0] = kNegBig;
-  ws.l[0] = 0.f;
-#pragma unroll
-  for (int jj = 0; jj < CH; ++jj) ws.acc[0][jj] = f32x4{0.f, 0.f, 0.f, 0.f};
-
   const int s0_steps = (it.s0_kend - it.s0_kbeg + kStepKeys - 1) / kStepKeys;
   const int s1_steps = (it.s1_kend - it.s1_kbeg + kStepKeys - 1) / kStepKeys;
   const int nsteps = s0_steps + s1_steps;
+
+  // The wave's first step: its pages are looked up and its K/V requested
+  // before anything else, since that is the longest dependent chain.
   KVRegs<D> bufA, bufB;
   PageWindow win{0, -1, 0};
-  int st = 0;
+  int st = wave;
   if (st < nsteps) load_kv<D>(bufA, a, win, step_pos(it, st, s0_steps), h, lane);
-  while (st < nsteps) {
-    if (st + 1 < nsteps) load_kv<D>(bufB, a, win, step_pos(it, st + 1, s0_steps), h, lane);
-    compute_step<D, 1>(ws, bufA, qf, lim, step_pos(it, st, s0_steps), 1, grp, a.scale_log2);
-    if (++st >= nsteps) break;
-    if (st + 1 < nsteps) load_kv<D>(bufA, a, win, step_pos(it, st + 1, s0_steps), h, lane);
-    compute_step<D, 1>(ws, bufB, qf, lim, step_pos(it, st, s0_steps), 1, grp, a.scale_log2);
-    ++st;
+
+  // Combine-phase ownership: thread t owns column t / 16 and dims
+  // (t % 16) * D/16 .. +D/16.  That row's phase-A partials are fetched now
+  // so their latency hides behind the streaming below.
+  const int cc = threadIdx.x >> 4;
+  const int d0 = (threadIdx.x & 15) * DS;
+  const int cj = cc >> a.group_shift;
+  const bool c_valid = cj < it.row_count;
+  const int c_tok = a.plan.row_tok[it.row_begin + (c_valid ? cj : 0)];
+  const int c_qh = h * G + (cc & (G - 1));
+  const ReqInfo ri = a.plan.req[a.plan.tok_req[c_tok]];
+  const size_t i_row = size_t(c_tok - ri.q_start);
+  float pl[kPrefetchParts];
+  f32x4 po[kPrefetchParts][DS / 4];
+#pragma unroll
+  for (int s = 0; s < kPrefetchParts; ++s) {
+    pl[s] = -INFINITY;
+    if (s < ri.nparts) {
+      const size_t prow = size_t(ri.part_base) + size_t(s) * ri.n + i_row;
+      pl[s] = a.plan.l_part[prow * a.hq + c_qh];
+      const float* op = a.plan.o_part + (prow * a.hq + c_qh) * D + d0;
+#pragma unroll
+      for (int e = 0; e < DS / 4; ++e) po[s][e] = *reinterpret_cast<const f32x4*>(op + 4 * e);
+    } else {
+#pragma unroll
+      for (int e = 0; e < DS / 4; ++e) po[s][e] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
   }
 
-  float l = ws.l[0];
-  l += __shfl_xor(l, 16);
-  l += __shfl_xor(l, 32);
-  // This wave's own result in log2 units, then the phase-A partials.
-  const float own = l > 0.f ? ws.m[0] + log2f(l) : -INFINITY;
-  const float inv_l = l > 0.f ? 1.0f / l : 0.f;
-  float o[4 * CH];
+  {
+    int j = col >> a.group_shift;
+    if (j >= it.row_count) j = 0;  // padding column: a copy of the first token, never stored
+    const int tok = a.plan.row_tok[it.row_begin + j];
+    const int qh = h * G + (col & (G - 1));
+    bf16x8 qf[1][KS];
+    int lim[1] = {tok + it.causal_base};
+    const uint16_t* qp = a.q + (size_t(tok) * a.hq + qh) * D + 8 * grp;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+    for (int s = 0; s < KS; ++s) qf[0][s] = *reinterpret_cast<const bf16x8*>(qp + 32 * s);
+    WaveState<D, 1> ws;
+    ws.m[0] = kNegBig;
+    ws.l[0] = 0.f;
 #pragma unroll
-    for (int jj = 0; jj < CH; ++jj) o[CH * i + jj] = ws.acc[0][jj][i] * inv_l;
-  const int r = a.plan.tok_req[tok];
-  const ReqInfo ri = a.plan.req[r];
-  float lse2 = own;
-  if (ri.nparts > 0) {
-    const size_t i_row = size_t(tok - ri.q_start);
-    float mx = own;
-    for (int s = 0; s < ri.nparts; ++s) {
-      const size_t prow = size_t(ri.part_base) + size_t(s) * ri.n + i_row;
-      mx = fmaxf(mx, a.plan.l_part[prow * a.hq + qh] * kLog2e);
+    for (int jj = 0; jj < CH; ++jj) ws.acc[0][jj] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // Two register buffers: the wave's next step is in flight while one is multiplied.
+    while (st < nsteps) {
+      int nst = st + kTileWaves;
+      if (nst < nsteps) load_kv<D>(bufB, a, win, step_pos(it, nst, s0_steps), h, lane);
+      compute_step<D, 1>(ws, bufA, qf, lim, step_pos(it, st, s0_steps), 1, grp, a.scale_log2);
+      st = nst;
+      if (st >= nsteps) break;
+      nst = st + kTileWaves;
+      if (nst < nsteps) load_kv<D>(bufA, a, win, step_pos(it, nst, s0_steps), h, lane);
+      compute_step<D, 1>(ws, bufB, qf, lim, step_pos(it, st, s0_steps), 1, grp, a.scale_log2);
+      st = nst;
     }
-    float z = fast_exp2(own - mx);
+    float l = ws.l[0];
+    l += __shfl_xor(l, 16);
+    l += __shfl_xor(l, 32);
 #pragma unroll
-    for (int e = 0; e < 4 * CH; ++e) o[e] *= z;
-    for (int s = 0; s < ri.nparts; ++s) {
-      const size_t prow = size_t(ri.part_base) + size_t(s) * ri.n + i_row;
-      const float w = fast_exp2(a.plan.l_part[prow * a.hq + qh] * kLog2e - mx);
-      z += w;
-      const float* op = a.plan.o_part + (prow * a.hq + qh) * D + 4 * CH * grp;
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int e = 0; e < 4 * CH; e += 4) {
-        const f32x4 v = *reinterpret_cast<const f32x4*>(op + e);
-        o[e] += w * v[0];
-        o[e + 1] += w * v[1];
-        o[e + 2] += w * v[2];
-        o[e + 3] += w * v[3];
-      }
+      for (int jj = 0; jj < CH; ++jj) red_o[wave][col][CH * (4 * grp + i) + jj] = ws.acc[0][jj][i];
+    if (grp == 0) {
+      red_m[wave][col] = ws.m[0];
+      red_l[wave][col] = l;
     }
-    const float inv = 1.0f / z;
-#pragma unroll
-    for (int e = 0; e < 4 * CH; ++e) o[e] *= inv;
-    lse2 = mx + log2f(z);
   }
-  if (!valid) return;
-  uint16_t* out = a.o + (size_t(tok) * a.hq + qh) * D + 4 * CH * grp;
+  __syncthreads();
+
+  // Combine the four waves and the phase-A partials of row (c_tok, c_qh).
+  if (!c_valid) return;
+  const int c = cc;
+  float mx = kNegBig;
 #pragma unroll
-  for (int e = 0; e < 4 * CH; e += 8) {
-    u32x4 w = {pack_bf16(o[e], o[e + 1]), pack_bf16(o[e + 2], o[e + 3]), pack_bf16(o[e + 4], o[e + 5]),
-               pack_bf16(o[e + 6], o[e + 7])};
-    *reinterpret_cast<u32x4*>(out + e) = w;
+  for (int w = 0; w < kTileWaves; ++w) mx = fmaxf(mx, red_m[w][c]);
+#pragma unroll
+  for (int s = 0; s < kPrefetchParts; ++s) mx = fmaxf(mx, pl[s] * kLog2e);
+  for (int s = kPrefetchParts; s < ri.nparts; ++s) {
+    const size_t prow = size_t(ri.part_base) + size_t(s) * ri.n + i_row;
+    mx = fmaxf(mx, a.plan.l_part[prow * a.hq + c_qh] * kLog2e);
   }
-  if (a.lse && grp == 0) a.lse[size_t(tok) * a.hq + qh] = lse2 * kLn2;
+  float z = 0.f;
+  float o[DS];
+#pragma unroll
+  for (int e = 0; e < DS; ++e) o[e] = 0.f;
+#pragma unroll
+  for (int w = 0; w < kTileWaves; ++w) {
+    const float f = fast_exp2(red_m[w][c] - mx);
+    z += f * red_l[w][c];
+#pragma unroll
+    for (int e = 0; e < DS; ++e) o[e] += f * red_o[w][c][d0 + e];
+  }
+#pragma unroll
+  for (int s = 0; s < kPrefetchParts; ++s) {
+    const float f = fast_exp2(pl[s] * kLog2e - mx);  // 0 for slots past nparts
+    z += f;
+#pragma unroll
+    for (int e = 0; e < DS; ++e) o[e] += f * po[s][e / 4][e % 4];
+  }
+  for (int s = kPrefetchParts; s < ri.nparts; ++s) {
+    const size_t prow = size_t(ri.part_base) + size_t(s) * ri.n + i_row;
+    const float f = fast_exp2(a.plan.l_part[prow * a.hq + c_qh] * kLog2e - mx);
+    z += f;
+    const float* op = a.plan.o_part + (prow * a.hq + c_qh) * D + d0;
+#pragma unroll
+    for (int e = 0; e < DS; e += 4) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(op + e);
+      o[e] += f * v[0];
+      o[e + 1] += f * v[1];
+      o[e + 2] += f * v[2];
+      o[e + 3] += f * v[3];
+    }
+  }
+  const float inv = 1.0f / z;
+  uint16_t* out = a.o + (size_t(c_tok) * a.hq + c_qh) * D + d0;
+  if constexpr (DS == 8) {
+    u32x4 w = {pack_bf16(o[0] * inv, o[1] * inv), pack_bf16(o[2] * inv, o[3] * inv), pack_bf16(o[4] * inv, o[5] * inv),
+               pack_bf16(o[6] * inv, o[7] * inv)};
+    *reinterpret_cast<u32x4*>(out) = w;
+  } else {
+    u32x2 w = {pack_bf16(o[0] * inv, o[1] * inv), pack_bf16(o[2] * inv, o[3] * inv)};
+    *reinterpret_cast<u32x2*>(out) = w;
+  }
+  if (a.lse && d0 == 0) a.lse[size_t(c_tok) * a.hq + c_qh] = (mx + log2f(z)) * kLn2;
 }
 
 template <int D>
@@ -728,16 +882,16 @@ template <int D>
 static void launch_phases(AttnArgs a, const pfx_plan* p, hipStream_t s) {
   if (p->n_tile1) {
     a.item_base = 0;
-    hipLaunchKernelGGL((tile_kernel<D, 1, kStages>), dim3(p->n_tile1), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((tile_kernel<D, 1, kDecodeStages, 2>), dim3(p->n_tile1), dim3(512), 0, s, a);
   }
   if (p->n_tile2) {
     a.item_base = p->n_tile1;
-    hipLaunchKernelGGL((tile_kernel<D, 2, kStages>), dim3(p->n_tile2), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((tile_kernel<D, 2, kStages, 1>), dim3(p->n_tile2), dim3(256), 0, s, a);
   }
   const int n_b = static_cast<int>(p->items.size()) - p->n_tile1 - p->n_tile2;
   if (n_b) {
     a.item_base = p->n_tile1 + p->n_tile2;
-    hipLaunchKernelGGL((attn_final_kernel<D>), dim3(n_b), dim3(64), 0, s, a);
+    hipLaunchKernelGGL((attn_final_kernel<D>), dim3(n_b), dim3(256), 0, s, a);
   }
 }
 
