@@ -187,7 +187,7 @@ int pfx_plan_workspace_bytes(const pfx_plan* plan, size_t* bytes);
 int pfx_plan_get_stats(const pfx_plan* plan, pfx_plan_stats* out);
 
 /* Copy one of the plan's host arrays out, for inspection and tests:
- * which = 0: work items, 16 int32 each; 1: row-token list; 2: page list.
+ * which = 0: work items, 32 int32 each; 1: row-token list; 2: page list.
  * Writes min(cap, size) values and sets *count to the full size. */
 int pfx_plan_export(const pfx_plan* plan, int32_t which, int32_t* out, int64_t cap, int64_t* count);
 

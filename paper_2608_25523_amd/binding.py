@@ -206,7 +206,7 @@ class Plan:
         _check(LIB.pfx_plan_export(self.h, which, None, 0, C.byref(cnt)))
         out = np.zeros(cnt.value, np.int32)
         _check(LIB.pfx_plan_export(self.h, which, out.ctypes.data_as(C.c_void_p), cnt.value, C.byref(cnt)))
-        return out.reshape(-1, 16) if which == 0 else out
+        return out.reshape(-1, 32) if which == 0 else out
 
     def upload(self, workspace=None, stream=None, device="cuda"):
         """Copy the plan into a device workspace (a uint8 tensor; allocated by

@@ -33,10 +33,14 @@ enum ItemKind : int32_t { kPrefixItem = 0, kSuffixItem = 1, kExtendItem = 2 };
 //   segment 0 (no mask):  keys [s0_kbeg, s0_kend) of the list at s0_page_off;
 //   segment 1 (causal):   keys [s1_kbeg, s1_kend) of the list at s1_page_off,
 //                         key k visible to token t iff k <= t + causal_base.
-// out_slot >= 0: partial slot out_slot of every request the item covers
-// (phase A).  out_slot < 0: final rows -- directly (extend items), or, for a
-// request's last suffix chunk (phase B), after merging the request's
-// phase-A partials.
+// out_slot >= 0: partial slot out_slot of every request the item covers;
+// out_slot < 0: final rows (extend items, and decode rows whose keys one
+// item covers entirely).
+// tok0 >= 0: the item's tokens are tok0, tok0 + 1, ... (one request), so
+// row_tok need not be read.  first_pages: the first kItemPages page ids of
+// the item's keys in order (segment 0's pages, then segment 1's), so the
+// first steps can be requested before the rest of the page list arrives.
+constexpr int kItemPages = 16;
 struct alignas(16) Item {
   int32_t kv_head;
   int32_t row_begin;
@@ -48,15 +52,17 @@ struct alignas(16) Item {
   int32_t out_slot;
   int32_t kind;
   int32_t req;  // request of a suffix/extend item, -1 for prefix items
-  int32_t pad0, pad1;
+  int32_t tok0;
+  int32_t pad0;
+  int32_t first_pages[kItemPages];
 };
-static_assert(sizeof(Item) == 64, "Item is 16 int32");
+static_assert(sizeof(Item) == 128, "Item is 32 int32");
 
 // Per-request bookkeeping on the device.
 struct ReqInfo {
   int32_t q_start;    // first query row
   int32_t n;          // query rows
-  int32_t nparts;     // partial results written in phase A (0: none)
+  int32_t nparts;     // partial results of each row, merged last (0: rows written directly)
   int32_t part_base;  // partial row of (slot, row i): part_base + slot * n + i
 };
 
@@ -68,6 +74,7 @@ struct DevPlan {
   const int32_t* tok_req;
   const ReqInfo* req;
   const int32_t* tok_slot;  // page * 16 + slot of every new token (append)
+  const int32_t* merge_tok; // tokens whose rows merge several partial results
   float* o_part;            // [num_part_rows][hq][d]
   float* l_part;            // [num_part_rows][hq]
 };
@@ -77,9 +84,10 @@ struct DevPlan {
 struct pfx_plan {
   int32_t num_pages = 0, hkv = 0, d = 0, hq = 0, group = 0, mode = 0;
   int32_t num_reqs = 0, num_tokens = 0;
-  // items[0, n_tile1): phase A, 16 columns per wave; then n_tile2 phase-A
-  // items with 32 columns per wave (extend); the rest: phase B.
-  int32_t n_tile1 = 0, n_tile2 = 0;
+  // items[0, n_decode): decode pieces (prefix chunks and suffix chunks,
+  // writing partials or single-piece rows); then n_extend extend blocks.
+  int32_t n_decode = 0, n_extend = 0;
+  std::vector<int32_t> merge_tok;  // tokens whose rows merge several pieces
   std::vector<pfx::Item> items;
   std::vector<int32_t> row_tok, page_list, tok_req, tok_slot;
   std::vector<pfx::ReqInfo> req;
@@ -88,7 +96,7 @@ struct pfx_plan {
   int32_t pages_needed = 0;
   // byte offsets inside the workspace
   size_t off_items = 0, off_row_tok = 0, off_page_list = 0, off_tok_req = 0, off_req = 0,
-         off_tok_slot = 0, off_opart = 0, off_lpart = 0, total_bytes = 0, blob_bytes = 0;
+         off_tok_slot = 0, off_merge_tok = 0, off_opart = 0, off_lpart = 0, total_bytes = 0, blob_bytes = 0;
   std::vector<unsigned char> blob;  // host image of [0, blob_bytes)
   void* dev_ws = nullptr;
   size_t dev_ws_bytes = 0;

@@ -106,17 +106,19 @@ __device__ __forceinline__ StepPos step_pos(const Item& it, int st, int s0_steps
 // 64 consecutive page ids of a segment, one per lane, so a step finds its
 // pages with v_readlane instead of a dependent scalar load.
 struct PageWindow {
-  int32_t vpage;  // lane i: page id at list position base + i
+  int32_t vpage;  // lane i: page id at list position base + i (i < count)
   int32_t seg;    // segment held (-1: none)
   int32_t base;
+  int32_t count;
 };
 
 __device__ __forceinline__ void window_for(PageWindow& w, const int32_t* page_list, const StepPos& p, int lane) {
   const int pos = p.k0 >> 4;  // even: steps start on 32-key boundaries
-  if (p.seg != w.seg || pos < w.base || pos + 1 >= w.base + 64) {
+  if (p.seg != w.seg || pos < w.base || pos + 1 >= w.base + w.count) {
     const int npages = (p.kend + 15) >> 4;
     w.seg = p.seg;
     w.base = pos;
+    w.count = 64;
     w.vpage = (pos + lane < npages) ? page_list[p.list_off + pos + lane] : 0;
   }
 }
@@ -416,7 +418,7 @@ __device__ __forceinline__ uint32_t lds_address(const unsigned char* p) {
 // Issue this wave's share of step st into a stage buffer.
 template <int D>
 __device__ __forceinline__ void issue_tile(unsigned char* stage, const AttnArgs& a, const Item& it, const int* ptab,
-                                           int p0n, int st, int s0_steps, int h, int wave, int lane) {
+                                           int lead, int p0n, int st, int s0_steps, int h, int wave, int lane) {
   using TG = TileGeom<D>;
   const StepPos p = step_pos(it, st, s0_steps);
   const int t = wave & 1;
@@ -424,7 +426,8 @@ __device__ __forceinline__ void issue_tile(unsigned char* stage, const AttnArgs&
   const int seg_base = p.seg == 0 ? it.s0_kbeg : it.s1_kbeg;
   int idx = (p.seg == 0 ? 0 : p0n) + ((p.k0 - seg_base) >> 4);
   if (t == 1 && p.k0 + 16 < p.kend) idx += 1;  // a missing second page re-reads the first (masked later)
-  const int page = ptab[idx];
+  // The item's leading page ids sit one per lane in `lead`; later ones in the LDS table.
+  const int page = idx < kItemPages ? __builtin_amdgcn_readlane(lead, idx) : ptab[idx];
   const uint16_t* base = (is_v ? a.vpool : a.kpool) + (size_t(page) * a.hkv + h) * (16 * D);
   const uint32_t dst = lds_address(stage) + wave * TG::page_bytes;
 #pragma unroll
@@ -518,7 +521,7 @@ __device__ __forceinline__ void write_block(const AttnArgs& a, const Item& it, c
 template <int D, int QBW, int NS, int NG>
 __device__ __forceinline__ void tile_round(WaveState<D, QBW>& ws, const bf16x8 (&qf)[QBW][D / 32],
                                            const int (&lim)[QBW], unsigned char (*ring)[TileGeom<D>::stage_bytes],
-                                           const AttnArgs& a, const Item& it, const int* ptab, int p0n, int r,
+                                           const AttnArgs& a, const Item& it, const int* ptab, int lead, int p0n, int r,
                                            int s0_steps, int nsteps, int nb, int h, int g, int wq, int lane) {
   using TG = TileGeom<D>;
   constexpr int R = NS / NG;  // rounds held by the ring
@@ -528,7 +531,7 @@ __device__ __forceinline__ void tile_round(WaveState<D, QBW>& ws, const bf16x8 (
   wait_vmcnt(ahead > 0 ? ahead * TG::loads_per_wave : 0);
   __syncthreads();
   const int nxt = st + NG * (R - 1);
-  if (nxt < nsteps) issue_tile<D>(ring[nxt % NS], a, it, ptab, p0n, nxt, s0_steps, h, wq, lane);
+  if (nxt < nsteps) issue_tile<D>(ring[nxt % NS], a, it, ptab, lead, p0n, nxt, s0_steps, h, wq, lane);
   if (nb > 0 && st < nsteps) {
     KVRegs<D> kv;
     read_tile<D>(kv, ring[st % NS], lane & 15, lane >> 4);
@@ -536,19 +539,24 @@ __device__ __forceinline__ void tile_round(WaveState<D, QBW>& ws, const bf16x8 (
   }
 }
 
-// Phase A kernel.  NG groups of four waves: the four waves of a group own
-// different query columns; the groups take alternate 32-key steps of the item
-// (more waves per SIMD without more partial results) and merge their
-// softmax states through LDS before the rows are written.
+// LDS bytes of a tile item: the ring, then the page table.
+template <int D, int NS>
+constexpr int tile_smem_bytes() { return NS * TileGeom<D>::stage_bytes + kMaxTilePages * 4; }
+
+// An item whose K/V streams through an LDS ring shared by the workgroup.
+// NG groups of four waves: the four waves of a group own different query
+// columns; the groups take alternate 32-key steps of the item and merge
+// their softmax states through LDS before the rows are written.
 template <int D, int QBW, int NS, int NG>
-__global__ __launch_bounds__(256 * NG, 2) void tile_kernel(AttnArgs a) {
+__device__ __forceinline__ void tile_item(const AttnArgs& a, const Item* itp, unsigned char* smem) {
   using TG = TileGeom<D>;
   constexpr int KS = D / 32;
   constexpr int CH = D / 16;
   static_assert(NS % NG == 0 && NS / NG >= 2, "the ring holds whole rounds");
-  __shared__ __attribute__((aligned(1024))) unsigned char ring[NS][TG::stage_bytes];
-  __shared__ int ptab[kMaxTilePages];
-  const Item it = a.plan.items[a.item_base + blockIdx.x];
+  auto ring = reinterpret_cast<unsigned char (*)[TG::stage_bytes]>(smem);
+  int* ptab = reinterpret_cast<int*>(smem + NS * TG::stage_bytes);
+  const int lead = itp->first_pages[threadIdx.x & (kItemPages - 1)];  // issued before the item's scalar load
+  const Item it = *itp;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = wave / kTileWaves;   // wave group: which steps
   const int wq = wave % kTileWaves;  // role inside the group: which columns, which quarter of a stage
@@ -578,7 +586,7 @@ __global__ __launch_bounds__(256 * NG, 2) void tile_kernel(AttnArgs a) {
     int j = c >> a.group_shift;
     const int gg = c & (G - 1);
     if (j >= it.row_count) j = 0;
-    const int tok = a.plan.row_tok[it.row_begin + j];
+    const int tok = it.tok0 >= 0 ? it.tok0 + j : a.plan.row_tok[it.row_begin + j];
     tok_of[b] = tok;
     lim[b] = tok + it.causal_base;
     if (b < nb) {
@@ -602,15 +610,16 @@ __global__ __launch_bounds__(256 * NG, 2) void tile_kernel(AttnArgs a) {
   const int s1_steps = (it.s1_kend - it.s1_kbeg + kStepKeys - 1) / kStepKeys;
   const int nsteps = s0_steps + s1_steps;
   const int rounds = (nsteps + NG - 1) / NG;
-  __syncthreads();  // page table ready
-
+  // The first rounds' pages are among the leading ids: request them before
+  // waiting for the page table.
   constexpr int R = NS / NG;
   for (int r = 0; r < R - 1; ++r) {
     const int st = NG * r + g;
-    if (st < nsteps) issue_tile<D>(ring[st % NS], a, it, ptab, p0n, st, s0_steps, h, wq, lane);
+    if (st < nsteps) issue_tile<D>(ring[st % NS], a, it, ptab, lead, p0n, st, s0_steps, h, wq, lane);
   }
+  __syncthreads();  // page table ready
   for (int r = 0; r < rounds; ++r)
-    tile_round<D, QBW, NS, NG>(ws, qf, lim, ring, a, it, ptab, p0n, r, s0_steps, nsteps, nb, h, g, wq, lane);
+    tile_round<D, QBW, NS, NG>(ws, qf, lim, ring, a, it, ptab, lead, p0n, r, s0_steps, nsteps, nb, h, g, wq, lane);
 
   if constexpr (NG == 2) {
     // Group 1 hands its state to group 0, lane for lane (same register layout).
@@ -654,69 +663,41 @@ __global__ __launch_bounds__(256 * NG, 2) void tile_kernel(AttnArgs a) {
   }
 }
 
-// Phase B: one workgroup per (decode request, KV head).  Its four waves take
-// the request's last suffix chunk's 32-key steps round-robin (each with the
-// request's <= 16 query columns and its own softmax state), then combine
-// their states and the partials phase A wrote for the same rows through LDS
-// (log-sum-exp merge), and write the final rows.
+// LDS bytes of a suffix unit: the four waves' states.
 template <int D>
-__global__ __launch_bounds__(256, 2) void attn_final_kernel(AttnArgs a) {
+constexpr int unit_smem_bytes() { return kTileWaves * kTileCols * (D + 4) * 4 + 2 * kTileWaves * kTileCols * 4; }
+
+// A decode request's suffix chunk for one KV head: the four waves take its
+// 32-key steps round-robin (each with the request's <= 16 query columns, two
+// register buffers and its own softmax state), then combine through LDS and
+// write the chunk's partial result, or the final rows when the chunk is all
+// the row sees.
+template <int D>
+__device__ __forceinline__ void suffix_unit(const AttnArgs& a, const Item* itp, unsigned char* smem) {
   constexpr int KS = D / 32;
   constexpr int CH = D / 16;
-  constexpr int DS = D / 16;          // dims per thread in the combine
-  constexpr int kPrefetchParts = 2;   // phase-A partials fetched at the start
-  __shared__ float red_o[kTileWaves][kTileCols][D + 4];
-  __shared__ float red_m[kTileWaves][kTileCols];
-  __shared__ float red_l[kTileWaves][kTileCols];
-  const Item it = a.plan.items[a.item_base + blockIdx.x];
+  constexpr int DS = D / 16;  // dims per thread in the combine
+  auto red_o = reinterpret_cast<float (*)[kTileCols][D + 4]>(smem);
+  auto red_m = reinterpret_cast<float (*)[kTileCols]>(smem + kTileWaves * kTileCols * (D + 4) * 4);
+  auto red_l = red_m + kTileWaves;
+  // The item's leading page ids are requested before its scalar fields: the
+  // window they form covers the first steps of all four waves.
+  PageWindow win{itp->first_pages[threadIdx.x & (kItemPages - 1)], 1, 0, kItemPages};
+  const Item it = *itp;
+  win.base = it.s1_kbeg >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
   const int h = it.kv_head;
   const int G = a.group;
-  const int s0_steps = (it.s0_kend - it.s0_kbeg + kStepKeys - 1) / kStepKeys;
-  const int s1_steps = (it.s1_kend - it.s1_kbeg + kStepKeys - 1) / kStepKeys;
-  const int nsteps = s0_steps + s1_steps;
-
-  // The wave's first step: its pages are looked up and its K/V requested
-  // before anything else, since that is the longest dependent chain.
-  KVRegs<D> bufA, bufB;
-  PageWindow win{0, -1, 0};
-  int st = wave;
-  if (st < nsteps) load_kv<D>(bufA, a, win, step_pos(it, st, s0_steps), h, lane);
-
-  // Combine-phase ownership: thread t owns column t / 16 and dims
-  // (t % 16) * D/16 .. +D/16.  That row's phase-A partials are fetched now
-  // so their latency hides behind the streaming below.
-  const int cc = threadIdx.x >> 4;
-  const int d0 = (threadIdx.x & 15) * DS;
-  const int cj = cc >> a.group_shift;
-  const bool c_valid = cj < it.row_count;
-  const int c_tok = a.plan.row_tok[it.row_begin + (c_valid ? cj : 0)];
-  const int c_qh = h * G + (cc & (G - 1));
-  const ReqInfo ri = a.plan.req[a.plan.tok_req[c_tok]];
-  const size_t i_row = size_t(c_tok - ri.q_start);
-  float pl[kPrefetchParts];
-  f32x4 po[kPrefetchParts][DS / 4];
-#pragma unroll
-  for (int s = 0; s < kPrefetchParts; ++s) {
-    pl[s] = -INFINITY;
-    if (s < ri.nparts) {
-      const size_t prow = size_t(ri.part_base) + size_t(s) * ri.n + i_row;
-      pl[s] = a.plan.l_part[prow * a.hq + c_qh];
-      const float* op = a.plan.o_part + (prow * a.hq + c_qh) * D + d0;
-#pragma unroll
-      for (int e = 0; e < DS / 4; ++e) po[s][e] = *reinterpret_cast<const f32x4*>(op + 4 * e);
-    } else {
-#pragma unroll
-      for (int e = 0; e < DS / 4; ++e) po[s][e] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-  }
-
+  const int nsteps = (it.s1_kend - it.s1_kbeg + kStepKeys - 1) / kStepKeys;
   {
+    KVRegs<D> bufA, bufB;
+    int st = wave;
+    if (st < nsteps) load_kv<D>(bufA, a, win, step_pos(it, st, 0), h, lane);
     int j = col >> a.group_shift;
     if (j >= it.row_count) j = 0;  // padding column: a copy of the first token, never stored
-    const int tok = a.plan.row_tok[it.row_begin + j];
+    const int tok = it.tok0 + j;  // a suffix unit's tokens are consecutive
     const int qh = h * G + (col & (G - 1));
     bf16x8 qf[1][KS];
     int lim[1] = {tok + it.causal_base};
@@ -728,17 +709,15 @@ __global__ __launch_bounds__(256, 2) void attn_final_kernel(AttnArgs a) {
     ws.l[0] = 0.f;
 #pragma unroll
     for (int jj = 0; jj < CH; ++jj) ws.acc[0][jj] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    // Two register buffers: the wave's next step is in flight while one is multiplied.
     while (st < nsteps) {
       int nst = st + kTileWaves;
-      if (nst < nsteps) load_kv<D>(bufB, a, win, step_pos(it, nst, s0_steps), h, lane);
-      compute_step<D, 1>(ws, bufA, qf, lim, step_pos(it, st, s0_steps), 1, grp, a.scale_log2);
+      if (nst < nsteps) load_kv<D>(bufB, a, win, step_pos(it, nst, 0), h, lane);
+      compute_step<D, 1>(ws, bufA, qf, lim, step_pos(it, st, 0), 1, grp, a.scale_log2);
       st = nst;
       if (st >= nsteps) break;
       nst = st + kTileWaves;
-      if (nst < nsteps) load_kv<D>(bufA, a, win, step_pos(it, nst, s0_steps), h, lane);
-      compute_step<D, 1>(ws, bufB, qf, lim, step_pos(it, st, s0_steps), 1, grp, a.scale_log2);
+      if (nst < nsteps) load_kv<D>(bufA, a, win, step_pos(it, nst, 0), h, lane);
+      compute_step<D, 1>(ws, bufB, qf, lim, step_pos(it, st, 0), 1, grp, a.scale_log2);
       st = nst;
     }
     float l = ws.l[0];
@@ -755,18 +734,16 @@ __global__ __launch_bounds__(256, 2) void attn_final_kernel(AttnArgs a) {
   }
   __syncthreads();
 
-  // Combine the four waves and the phase-A partials of row (c_tok, c_qh).
-  if (!c_valid) return;
-  const int c = cc;
+  // Combine: thread t owns column t / 16 and dims (t % 16) * D/16 .. +D/16.
+  const int c = threadIdx.x >> 4;
+  const int d0 = (threadIdx.x & 15) * DS;
+  const int j = c >> a.group_shift;
+  if (j >= it.row_count) return;
+  const int tok = it.tok0 + j;
+  const int qh = h * G + (c & (G - 1));
   float mx = kNegBig;
 #pragma unroll
   for (int w = 0; w < kTileWaves; ++w) mx = fmaxf(mx, red_m[w][c]);
-#pragma unroll
-  for (int s = 0; s < kPrefetchParts; ++s) mx = fmaxf(mx, pl[s] * kLog2e);
-  for (int s = kPrefetchParts; s < ri.nparts; ++s) {
-    const size_t prow = size_t(ri.part_base) + size_t(s) * ri.n + i_row;
-    mx = fmaxf(mx, a.plan.l_part[prow * a.hq + c_qh] * kLog2e);
-  }
   float z = 0.f;
   float o[DS];
 #pragma unroll
@@ -778,38 +755,121 @@ __global__ __launch_bounds__(256, 2) void attn_final_kernel(AttnArgs a) {
 #pragma unroll
     for (int e = 0; e < DS; ++e) o[e] += f * red_o[w][c][d0 + e];
   }
-#pragma unroll
-  for (int s = 0; s < kPrefetchParts; ++s) {
-    const float f = fast_exp2(pl[s] * kLog2e - mx);  // 0 for slots past nparts
-    z += f;
-#pragma unroll
-    for (int e = 0; e < DS; ++e) o[e] += f * po[s][e / 4][e % 4];
-  }
-  for (int s = kPrefetchParts; s < ri.nparts; ++s) {
-    const size_t prow = size_t(ri.part_base) + size_t(s) * ri.n + i_row;
-    const float f = fast_exp2(a.plan.l_part[prow * a.hq + c_qh] * kLog2e - mx);
-    z += f;
-    const float* op = a.plan.o_part + (prow * a.hq + c_qh) * D + d0;
+  // A row can see none of a chunk's keys (a multi-row decode request whose
+  // later suffix chunk starts after its first row): O = 0, LSE = -inf.
+  const float inv = z > 0.f ? 1.0f / z : 0.f;
+  const float lse_nat = z > 0.f ? (mx + log2f(z)) * kLn2 : -INFINITY;
+  if (it.out_slot < 0) {
+    uint16_t* out = a.o + (size_t(tok) * a.hq + qh) * D + d0;
+    if constexpr (DS == 8) {
+      u32x4 w = {pack_bf16(o[0] * inv, o[1] * inv), pack_bf16(o[2] * inv, o[3] * inv),
+                 pack_bf16(o[4] * inv, o[5] * inv), pack_bf16(o[6] * inv, o[7] * inv)};
+      *reinterpret_cast<u32x4*>(out) = w;
+    } else {
+      u32x2 w = {pack_bf16(o[0] * inv, o[1] * inv), pack_bf16(o[2] * inv, o[3] * inv)};
+      *reinterpret_cast<u32x2*>(out) = w;
+    }
+    if (a.lse && d0 == 0) a.lse[size_t(tok) * a.hq + qh] = lse_nat;
+  } else {
+    const ReqInfo ri = a.plan.req[it.req];
+    const size_t prow = size_t(ri.part_base) + size_t(it.out_slot) * ri.n + (tok - ri.q_start);
+    float* out = a.plan.o_part + (prow * a.hq + qh) * D + d0;
 #pragma unroll
     for (int e = 0; e < DS; e += 4) {
-      const f32x4 v = *reinterpret_cast<const f32x4*>(op + e);
-      o[e] += f * v[0];
-      o[e + 1] += f * v[1];
-      o[e + 2] += f * v[2];
-      o[e + 3] += f * v[3];
+      f32x4 v = {o[e] * inv, o[e + 1] * inv, o[e + 2] * inv, o[e + 3] * inv};
+      *reinterpret_cast<f32x4*>(out + e) = v;
+    }
+    if (d0 == 0) a.plan.l_part[prow * a.hq + qh] = lse_nat;
+  }
+}
+
+// Extend blocks: final rows, 32 query columns per wave, one wave group.
+template <int D>
+__global__ __launch_bounds__(256, 2) void extend_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[tile_smem_bytes<D, kStages>()];
+  tile_item<D, 2, kStages, 1>(a, a.plan.items + a.item_base + blockIdx.x, smem);
+}
+
+// Decode pieces in one launch: prefix chunks shared by an agent's decode
+// rows (LDS tiles, 16 columns per wave) and suffix chunks (four-wave units);
+// none depends on another.
+template <int D>
+__global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
+  constexpr int kSmem = tile_smem_bytes<D, kStages>() > unit_smem_bytes<D>() ? tile_smem_bytes<D, kStages>()
+                                                                             : unit_smem_bytes<D>();
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[kSmem];
+  const Item* itp = a.plan.items + a.item_base + blockIdx.x;
+  if (itp->kind == kPrefixItem)
+    tile_item<D, 1, kStages, 1>(a, itp, smem);
+  else
+    suffix_unit<D>(a, itp, smem);
+}
+
+// The rows of decode requests seen by several pieces: log-sum-exp merge of
+// their partial results.  One thread per (token, query head, 8 dims); the
+// first kMergeBatch partials of the row are all requested before any is
+// used, so a row pays one memory latency rather than one per partial.
+constexpr int kMergeBatch = 8;
+
+template <int D>
+__global__ __launch_bounds__(256) void merge_rows_kernel(AttnArgs a, int n_tok) {
+  constexpr int SL = D / 8;
+  const size_t t = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (t >= size_t(n_tok) * a.hq * SL) return;
+  const int sl = int(t % SL);
+  const int qh = int((t / SL) % a.hq);
+  const int tok = a.plan.merge_tok[t / (size_t(SL) * a.hq)];
+  const ReqInfo ri = a.plan.req[a.plan.tok_req[tok]];
+  const size_t row0 = size_t(ri.part_base) + (tok - ri.q_start);
+  const size_t lstride = size_t(ri.n) * a.hq;
+  const float* lp = a.plan.l_part + row0 * a.hq + qh;
+  const float* op = a.plan.o_part + (row0 * a.hq + qh) * D + sl * 8;
+  const size_t ostride = lstride * D;
+  float lv[kMergeBatch];
+  f32x4 ov[kMergeBatch][2];
+#pragma unroll
+  for (int k = 0; k < kMergeBatch; ++k) {
+    if (k < ri.nparts) {
+      lv[k] = lp[k * lstride];
+      ov[k][0] = *reinterpret_cast<const f32x4*>(op + k * ostride);
+      ov[k][1] = *reinterpret_cast<const f32x4*>(op + k * ostride + 4);
+    } else {
+      lv[k] = -INFINITY;
+      ov[k][0] = ov[k][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int k = 0; k < kMergeBatch; ++k) mx = fmaxf(mx, lv[k]);
+  for (int k = kMergeBatch; k < ri.nparts; ++k) mx = fmaxf(mx, lp[k * lstride]);
+  float z = 0.f;
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int k = 0; k < kMergeBatch; ++k) {
+    const float w = fast_exp2((lv[k] - mx) * kLog2e);  // 0 for unused slots
+    z += w;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      acc[e] += w * ov[k][0][e];
+      acc[4 + e] += w * ov[k][1][e];
+    }
+  }
+  for (int k = kMergeBatch; k < ri.nparts; ++k) {
+    const float w = fast_exp2((lp[k * lstride] - mx) * kLog2e);
+    z += w;
+    const f32x4 x = *reinterpret_cast<const f32x4*>(op + k * ostride);
+    const f32x4 y = *reinterpret_cast<const f32x4*>(op + k * ostride + 4);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      acc[e] += w * x[e];
+      acc[4 + e] += w * y[e];
     }
   }
   const float inv = 1.0f / z;
-  uint16_t* out = a.o + (size_t(c_tok) * a.hq + c_qh) * D + d0;
-  if constexpr (DS == 8) {
-    u32x4 w = {pack_bf16(o[0] * inv, o[1] * inv), pack_bf16(o[2] * inv, o[3] * inv), pack_bf16(o[4] * inv, o[5] * inv),
-               pack_bf16(o[6] * inv, o[7] * inv)};
-    *reinterpret_cast<u32x4*>(out) = w;
-  } else {
-    u32x2 w = {pack_bf16(o[0] * inv, o[1] * inv), pack_bf16(o[2] * inv, o[3] * inv)};
-    *reinterpret_cast<u32x2*>(out) = w;
-  }
-  if (a.lse && d0 == 0) a.lse[size_t(c_tok) * a.hq + c_qh] = (mx + log2f(z)) * kLn2;
+  u32x4 w = {pack_bf16(acc[0] * inv, acc[1] * inv), pack_bf16(acc[2] * inv, acc[3] * inv),
+             pack_bf16(acc[4] * inv, acc[5] * inv), pack_bf16(acc[6] * inv, acc[7] * inv)};
+  *reinterpret_cast<u32x4*>(a.o + (size_t(tok) * a.hq + qh) * D + sl * 8) = w;
+  if (a.lse && sl == 0) a.lse[size_t(tok) * a.hq + qh] = mx + logf(z);
 }
 
 template <int D>
@@ -879,19 +939,19 @@ static int check_pool_matches(const pfx_pool* pool, const pfx_plan* p, const cha
 }
 
 template <int D>
-static void launch_phases(AttnArgs a, const pfx_plan* p, hipStream_t s) {
-  if (p->n_tile1) {
+static void launch_all(AttnArgs a, const pfx_plan* p, hipStream_t s) {
+  if (p->n_extend) {
+    a.item_base = p->n_decode;
+    hipLaunchKernelGGL((extend_kernel<D>), dim3(p->n_extend), dim3(256), 0, s, a);
+  }
+  if (p->n_decode) {
     a.item_base = 0;
-    hipLaunchKernelGGL((tile_kernel<D, 1, kDecodeStages, 2>), dim3(p->n_tile1), dim3(512), 0, s, a);
+    hipLaunchKernelGGL((decode_kernel<D>), dim3(p->n_decode), dim3(256), 0, s, a);
   }
-  if (p->n_tile2) {
-    a.item_base = p->n_tile1;
-    hipLaunchKernelGGL((tile_kernel<D, 2, kStages, 1>), dim3(p->n_tile2), dim3(256), 0, s, a);
-  }
-  const int n_b = static_cast<int>(p->items.size()) - p->n_tile1 - p->n_tile2;
-  if (n_b) {
-    a.item_base = p->n_tile1 + p->n_tile2;
-    hipLaunchKernelGGL((attn_final_kernel<D>), dim3(n_b), dim3(256), 0, s, a);
+  const int n_tok = static_cast<int>(p->merge_tok.size());
+  if (n_tok) {
+    const size_t threads = size_t(n_tok) * p->hq * (D / 8);
+    hipLaunchKernelGGL((merge_rows_kernel<D>), dim3((threads + 255) / 256), dim3(256), 0, s, a, n_tok);
   }
 }
 
@@ -955,7 +1015,7 @@ extern "C" int pfx_attention(const pfx_pool* pool, const pfx_plan* p, const void
   a.group_shift = __builtin_ctz(static_cast<unsigned>(p->group));
   a.scale_log2 = sm_scale * kLog2e;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (p->d == 128) launch_phases<128>(a, p, s); else launch_phases<64>(a, p, s);
+  if (p->d == 128) launch_all<128>(a, p, s); else launch_all<64>(a, p, s);
   return check_launch("pfx_attention");
 }
 

@@ -38,6 +38,7 @@ DevPlan dev_plan(const pfx_plan* p) {
   d.tok_req = reinterpret_cast<const int32_t*>(base + p->off_tok_req);
   d.req = reinterpret_cast<const ReqInfo*>(base + p->off_req);
   d.tok_slot = reinterpret_cast<const int32_t*>(base + p->off_tok_slot);
+  d.merge_tok = reinterpret_cast<const int32_t*>(base + p->off_merge_tok);
   d.o_part = reinterpret_cast<float*>(base + p->off_opart);
   d.l_part = reinterpret_cast<float*>(base + p->off_lpart);
   return d;
@@ -355,22 +356,23 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
         }
   }
 
-  // Decode rows against each request's own suffix, in chunks.  Every chunk
-  // but the last is a phase-A item writing a partial; the last chunk is the
-  // request's phase-B item, which merges all of the row's partials (prefix
-  // chunks and earlier suffix chunks) with its own state and writes the row.
+  // Decode rows against each request's own suffix, in chunks of up to
+  // schunk keys, one four-wave unit per (chunk, KV head).  A row seen by
+  // more than one piece (prefix chunks, suffix chunks) gets one partial
+  // result per piece, merged by the last launch; a row seen by a single
+  // piece is written directly.
   int64_t part_rows = 0;
-  std::vector<Item> final_items;
   for (int32_t r = 0; r < R; ++r) {
     if (!is_decode_class(r)) continue;
     const ReqInfo ri = p->req[r];
     const int32_t L = b->suffix_len[r];
     const int32_t ns = nchunks(L, schunk);
-    const int32_t nparts = prefix_chunks[r] + ns - 1;  // written in phase A
-    p->req[r].nparts = nparts;
-    if (nparts > 0) {
+    const int32_t pieces = prefix_chunks[r] + ns;
+    p->req[r].nparts = pieces > 1 ? pieces : 0;
+    if (pieces > 1) {
       p->req[r].part_base = static_cast<int32_t>(part_rows);
-      part_rows += int64_t(nparts) * ri.n;
+      part_rows += int64_t(pieces) * ri.n;
+      for (int32_t i = 0; i < ri.n; ++i) p->merge_tok.push_back(ri.q_start + i);
     }
     const int32_t rb = static_cast<int32_t>(p->row_tok.size());
     for (int32_t i = 0; i < ri.n; ++i) p->row_tok.push_back(ri.q_start + i);
@@ -389,13 +391,8 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
         it.causal_base = L - ri.n - ri.q_start;
         it.kind = kSuffixItem;
         it.req = r;
-        if (j + 1 < ns) {
-          it.out_slot = prefix_chunks[r] + j;
-          items.push_back(it);
-        } else {
-          it.out_slot = -1;
-          final_items.push_back(it);
-        }
+        it.out_slot = pieces > 1 ? prefix_chunks[r] + j : -1;
+        items.push_back(it);
         ++p->n_suffix_items;
       }
   }
@@ -439,24 +436,36 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
     return delete p, fail(PFX_ERANGE, "pfx_plan_create: too many partial rows");
   p->num_part_rows = part_rows;
 
-  // Phase A runs as two launches -- 16 columns per wave (decode prefix
-  // pieces, early suffix chunks), then 32 columns per wave (extend blocks)
-  // -- and phase B after both on the same stream, so every partial it
-  // merges is complete and visible.  Longest key ranges go first inside
-  // each launch so the tail stays short.
-  auto cost = [](const Item& it) { return int64_t(it.s0_kend - it.s0_kbeg + it.s1_kend - it.s1_kbeg); };
+  // Two launches, then the merge: decode pieces (prefix chunks shared by an
+  // agent's rows, and suffix chunks) all write partial results and depend on
+  // nothing, so they share one launch; extend blocks (final rows) are the
+  // other; the merge of rows with several pieces runs last on the same
+  // stream.  Longest key ranges first inside a launch keeps the tail short.
+  auto cost = [](const Item& it) {
+    const int64_t keys = it.s0_kend - it.s0_kbeg + it.s1_kend - it.s1_kbeg;
+    return it.kind == kPrefixItem ? keys * 2 : keys;  // prefix pieces also carry 4x the columns
+  };
   auto by_cost = [&](const Item& x, const Item& y) { return cost(x) > cost(y); };
-  std::vector<Item> tile1, tile2;
-  for (const Item& it : items) (it.kind == kExtendItem ? tile2 : tile1).push_back(it);
-  std::stable_sort(tile1.begin(), tile1.end(), by_cost);
-  std::stable_sort(tile2.begin(), tile2.end(), by_cost);
-  std::stable_sort(final_items.begin(), final_items.end(), by_cost);
-  p->n_tile1 = static_cast<int32_t>(tile1.size());
-  p->n_tile2 = static_cast<int32_t>(tile2.size());
+  std::vector<Item> dec, ext;
+  for (const Item& it : items) (it.kind == kExtendItem ? ext : dec).push_back(it);
+  std::stable_sort(dec.begin(), dec.end(), by_cost);
+  std::stable_sort(ext.begin(), ext.end(), by_cost);
+  // Each item's leading page ids and, for single-request items, its first token.
+  auto fill_head = [&](Item& it) {
+    int32_t k = 0;
+    for (int32_t pg = it.s0_kbeg >> 4; it.s0_kend > it.s0_kbeg && pg < (it.s0_kend + 15) >> 4 && k < kItemPages; ++pg)
+      it.first_pages[k++] = p->page_list[it.s0_page_off + pg];
+    for (int32_t pg = it.s1_kbeg >> 4; it.s1_kend > it.s1_kbeg && pg < (it.s1_kend + 15) >> 4 && k < kItemPages; ++pg)
+      it.first_pages[k++] = p->page_list[it.s1_page_off + pg];
+    it.tok0 = it.req >= 0 ? p->row_tok[it.row_begin] : -1;
+  };
+  for (Item& it : dec) fill_head(it);
+  for (Item& it : ext) fill_head(it);
+  p->n_decode = static_cast<int32_t>(dec.size());
+  p->n_extend = static_cast<int32_t>(ext.size());
   items.clear();
-  items.insert(items.end(), tile1.begin(), tile1.end());
-  items.insert(items.end(), tile2.begin(), tile2.end());
-  items.insert(items.end(), final_items.begin(), final_items.end());
+  items.insert(items.end(), dec.begin(), dec.end());
+  items.insert(items.end(), ext.begin(), ext.end());
   p->items = std::move(items);
 
   // ---- workspace layout ----
@@ -467,6 +476,7 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   p->off_tok_req = off;    off = align256(off + p->tok_req.size() * 4);
   p->off_req = off;        off = align256(off + p->req.size() * sizeof(ReqInfo));
   p->off_tok_slot = off;   off = align256(off + p->tok_slot.size() * 4);
+  p->off_merge_tok = off;  off = align256(off + p->merge_tok.size() * 4);
   p->blob_bytes = off;
   p->off_opart = off;      off = align256(off + size_t(part_rows) * hq * p->d * 4);
   p->off_lpart = off;      off = align256(off + size_t(part_rows) * hq * 4);
@@ -482,6 +492,7 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   put(p->off_tok_req, p->tok_req.data(), p->tok_req.size() * 4);
   put(p->off_req, p->req.data(), p->req.size() * sizeof(ReqInfo));
   put(p->off_tok_slot, p->tok_slot.data(), p->tok_slot.size() * 4);
+  put(p->off_merge_tok, p->merge_tok.data(), p->merge_tok.size() * 4);
 
   *out = p;
   return PFX_OK;
@@ -512,7 +523,7 @@ extern "C" int pfx_plan_export(const pfx_plan* p, int32_t which, int32_t* out, i
   const int32_t* src = nullptr;
   int64_t n = 0;
   switch (which) {
-    case 0: src = reinterpret_cast<const int32_t*>(p->items.data()); n = int64_t(p->items.size()) * 16; break;
+    case 0: src = reinterpret_cast<const int32_t*>(p->items.data()); n = int64_t(p->items.size()) * 32; break;
     case 1: src = p->row_tok.data(); n = int64_t(p->row_tok.size()); break;
     case 2: src = p->page_list.data(); n = int64_t(p->page_list.size()); break;
     default: return fail(PFX_EINVAL, "pfx_plan_export: which = %d", which);

@@ -41,6 +41,8 @@ def test_no_packed_fp32(isa):
 
 
 def test_no_scratch_in_attention_kernels(isa):
-    for kernel in re.findall(r"^(_ZN3pfx\w*(?:tile|final)_kernel\w*):", isa, flags=re.M):
+    kernels = re.findall(r"^(_ZN3pfx\w*(?:decode|extend|merge_rows)_kernel\w*):", isa, flags=re.M)
+    assert len(kernels) == 6  # three kernels, head dims 64 and 128
+    for kernel in kernels:
         body = isa.split(kernel + ":", 1)[1].split("s_endpgm", 1)[0]
         assert "scratch_" not in body, kernel
