@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define PFX_VERSION 10000 /* 1.0.0 */
+#define PFX_VERSION 20000 /* 2.0.0 */
 
 #define PFX_OK 0
 #define PFX_EINVAL (-1)       /* malformed argument (null pointer, bad CSR, overlapping pages, ...) */
@@ -160,20 +160,26 @@ void pfx_alloc_destroy(pfx_alloc* alloc);
 typedef struct pfx_plan pfx_plan;
 
 typedef struct pfx_plan_opts {
-  int32_t prefix_chunk; /* keys per prefix chunk for grouped decode (0 = automatic; multiple of 32) */
-  int32_t suffix_chunk; /* keys per suffix chunk for decode (0 = automatic; multiple of 32) */
-  int32_t reserved[6];  /* must be zero */
+  /* Workgroups the decode steps are divided among (0 = automatic: 512, two
+   * per compute unit of a 256-CU device).  More workers cut decode items into
+   * more pieces; fewer leave compute units idle. */
+  int32_t decode_workers;
+  int32_t reserved[7]; /* must be zero */
 } pfx_plan_opts;
 
 typedef struct pfx_plan_stats {
   int32_t num_requests;
   int32_t num_tokens;        /* sum of n_r: query rows of the batch */
-  int32_t num_items;         /* work items (one workgroup each) */
-  int32_t num_prefix_items;  /* grouped-decode items over a prefix chunk */
-  int32_t num_suffix_items;  /* decode items over a request's own suffix */
-  int32_t num_extend_items;  /* extend items (prefix + causal suffix) */
-  int32_t num_partial_rows;  /* (token, slot) partial results kept in the workspace */
-  int32_t pages_needed;      /* left-hand side of the Eq. (2) check, in pages */
+  int32_t num_items;           /* prefix + suffix + extend items */
+  int32_t num_prefix_items;    /* grouped decode: (agent, block of <= 64 decode columns, KV head) over the prefix */
+  int32_t num_suffix_items;    /* decode: (request, KV head) over the request's own suffix */
+  int32_t num_extend_items;    /* extend blocks: (<= 128 columns of one request, KV head), one workgroup each */
+  int32_t num_partial_rows;    /* partial result rows (one query head each) kept in the workspace */
+  int32_t pages_needed;        /* left-hand side of the Eq. (2) check, in pages */
+  int32_t num_decode_steps;    /* 32-key steps of all decode items */
+  int32_t num_decode_workers;  /* decode workgroups */
+  int32_t num_decode_segments; /* pieces of decode items, one per (item, worker) */
+  int32_t reserved;
   int64_t workspace_bytes;
 } pfx_plan_stats;
 
@@ -187,7 +193,10 @@ int pfx_plan_workspace_bytes(const pfx_plan* plan, size_t* bytes);
 int pfx_plan_get_stats(const pfx_plan* plan, pfx_plan_stats* out);
 
 /* Copy one of the plan's host arrays out, for inspection and tests:
- * which = 0: work items, 32 int32 each; 1: row-token list; 2: page list.
+ * which = 0: extend blocks, 32 int32 each; 1: their row-token list;
+ * 2: page list; 3: decode segments, 144 int32 each; 4: decode step table,
+ * 2 int32 per step; 5: decode workers, 4 int32 each; 6: tokens whose rows
+ * are merged; 7: their (base, count) of partial slots per KV head.
  * Writes min(cap, size) values and sets *count to the full size. */
 int pfx_plan_export(const pfx_plan* plan, int32_t which, int32_t* out, int64_t cap, int64_t* count);
 

@@ -14,32 +14,29 @@ namespace pfx {
 
 // Columns of one MFMA tile: the query side of a 16x16x32 bf16 product.
 constexpr int kTileCols = 16;
-// Waves per phase-A workgroup; each owns 16 (decode) or 32 (extend) columns.
+// Waves per workgroup of the attention kernels.
 constexpr int kTileWaves = 4;
-// Query columns of a phase-A item: decode prefix pieces and early suffix
-// chunks, and extend blocks.
+// Query columns of a decode prefix item (16 per wave) and of an extend
+// block (32 per wave).
 constexpr int kDecodeTileCols = kTileWaves * 16;
 constexpr int kExtendTileCols = kTileWaves * 32;
-// Page ids one phase-A item may reference (its LDS page table).
+// Page ids one extend block may reference (its LDS page table).
 constexpr int kMaxTilePages = 1024;
 // Keys processed per inner step (two 16-token pages).
 constexpr int kStepKeys = 32;
 
 enum ItemKind : int32_t { kPrefixItem = 0, kSuffixItem = 1, kExtendItem = 2 };
 
-// One unit of device work, run by one workgroup.  Its query columns are
-// row_count tokens (row_tok[row_begin ...]) times the G query heads of KV
-// head kv_head.  Keys come from up to two segments of the plan's page list:
+// One extend block, run by one workgroup.  Its query columns are row_count
+// tokens (row_tok[row_begin ...]) times the G query heads of KV head
+// kv_head.  Keys come from two segments of the plan's page list:
 //   segment 0 (no mask):  keys [s0_kbeg, s0_kend) of the list at s0_page_off;
 //   segment 1 (causal):   keys [s1_kbeg, s1_kend) of the list at s1_page_off,
 //                         key k visible to token t iff k <= t + causal_base.
-// out_slot >= 0: partial slot out_slot of every request the item covers;
-// out_slot < 0: final rows (extend items, and decode rows whose keys one
-// item covers entirely).
-// tok0 >= 0: the item's tokens are tok0, tok0 + 1, ... (one request), so
-// row_tok need not be read.  first_pages: the first kItemPages page ids of
-// the item's keys in order (segment 0's pages, then segment 1's), so the
-// first steps can be requested before the rest of the page list arrives.
+// Rows are written final (out_slot = -1).  tok0 >= 0: the tokens are tok0,
+// tok0 + 1, ... (one request).  first_pages: the first kItemPages page ids
+// of the keys in order (segment 0's pages, then segment 1's), so the first
+// steps can be requested before the rest of the page list arrives.
 constexpr int kItemPages = 16;
 struct alignas(16) Item {
   int32_t kv_head;
@@ -51,32 +48,80 @@ struct alignas(16) Item {
   int32_t causal_base;
   int32_t out_slot;
   int32_t kind;
-  int32_t req;  // request of a suffix/extend item, -1 for prefix items
+  int32_t req;
   int32_t tok0;
   int32_t pad0;
   int32_t first_pages[kItemPages];
 };
 static_assert(sizeof(Item) == 128, "Item is 32 int32");
 
-// Per-request bookkeeping on the device.
-struct ReqInfo {
-  int32_t q_start;    // first query row
-  int32_t n;          // query rows
-  int32_t nparts;     // partial results of each row, merged last (0: rows written directly)
-  int32_t part_base;  // partial row of (slot, row i): part_base + slot * n + i
+// Decode work.  A decode item is one KV head's whole key range for a set of
+// query rows: an agent's prefix against a block of its decode rows (<= 64
+// columns), or one request's suffix against its own rows.  Items are cut
+// into 32-key steps; the concatenated step list is divided into contiguous,
+// equal runs, one per workgroup ("worker").  The part of an item inside one
+// worker is a segment; an item cut by worker boundaries has several
+// segments ("pieces"), each giving a partial result of its rows.
+constexpr int kSegRows = kDecodeTileCols;  // rows of a segment (columns / G)
+constexpr int kWorkerSegs = 16;            // segments of one worker (held in LDS)
+constexpr int kWorkerSteps = 256;          // steps of one worker (its LDS step table)
+constexpr int kDefaultWorkers = 512;       // two resident workgroups on each of 256 CUs
+
+struct alignas(16) SegHead {
+  int32_t kind;         // kPrefixItem or kSuffixItem
+  int32_t kv_head;
+  int32_t ncols;        // query columns: rows * G (<= 64)
+  int32_t nsteps;       // 32-key steps of the segment
+  int32_t k0;           // key of the first step, within the item
+  int32_t kend;         // keys of the item (the last step is masked past it)
+  int32_t causal_base;  // suffix items: key k visible to token t iff k <= t + causal_base
+  int32_t slot;         // partial slot of the piece in each of its rows; -1: final rows
+  int32_t item;         // decode item
+  int32_t piece;        // index of the segment among the item's pieces
+  int32_t causal;       // 1: some row sees only part of the keys (multi-row suffix)
+  int32_t pad[5];
+};
+struct alignas(16) Seg {
+  SegHead h;
+  int32_t tok[kSegRows];  // query token of row j
+  int32_t out[kSegRows];  // row j, query head g of the KV head -> output row out[j] + g:
+                          // o/lse row (final) or o_part/l_part row (partial)
+};
+static_assert(sizeof(Seg) == 576, "Seg is 144 int32");
+
+struct Worker {
+  int32_t step_begin;  // first step (index into the step table)
+  int32_t nsteps;
+  int32_t seg_begin;   // first segment
+  int32_t nseg;
+};
+
+// Partial results of one (decode token, KV head): nparts slots of G rows at
+// o_part/l_part rows (base + slot) * G + g.  nparts < 2: written directly.
+struct MergeHead {
+  int32_t base;
+  int32_t nparts;
 };
 
 // Device pointers into an uploaded workspace.
 struct DevPlan {
-  const Item* items;
+  const Item* items;            // extend blocks
   const int32_t* row_tok;
   const int32_t* page_list;
-  const int32_t* tok_req;
-  const ReqInfo* req;
-  const int32_t* tok_slot;  // page * 16 + slot of every new token (append)
-  const int32_t* merge_tok; // tokens whose rows merge several partial results
-  float* o_part;            // [num_part_rows][hq][d]
-  float* l_part;            // [num_part_rows][hq]
+  const int32_t* tok_slot;      // page * 16 + slot of every new token (append)
+  const Seg* segs;
+  const int32_t* steps;         // per decode step: (page * Hkv + head) of its two 16-key pages
+  const Worker* workers;
+  const int32_t* merge_tok;     // decode tokens whose rows merge several pieces
+  const MergeHead* merge_head;  // [merge token][KV head]
+  float* o_part;                // [partial row][d]
+  float* l_part;                // [partial row]
+};
+
+// Per-request bookkeeping (host).
+struct ReqInfo {
+  int32_t q_start;  // first query row
+  int32_t n;        // query rows
 };
 
 }  // namespace pfx
@@ -84,19 +129,21 @@ struct DevPlan {
 struct pfx_plan {
   int32_t num_pages = 0, hkv = 0, d = 0, hq = 0, group = 0, mode = 0;
   int32_t num_reqs = 0, num_tokens = 0;
-  // items[0, n_decode): decode pieces (prefix chunks and suffix chunks,
-  // writing partials or single-piece rows); then n_extend extend blocks.
-  int32_t n_decode = 0, n_extend = 0;
-  std::vector<int32_t> merge_tok;  // tokens whose rows merge several pieces
-  std::vector<pfx::Item> items;
+  std::vector<pfx::Item> items;  // extend blocks
   std::vector<int32_t> row_tok, page_list, tok_req, tok_slot;
   std::vector<pfx::ReqInfo> req;
+  std::vector<pfx::Seg> segs;
+  std::vector<int32_t> steps;
+  std::vector<pfx::Worker> workers;
+  std::vector<int32_t> merge_tok;
+  std::vector<pfx::MergeHead> merge_head;
   int64_t num_part_rows = 0;
   int32_t n_prefix_items = 0, n_suffix_items = 0, n_extend_items = 0;
   int32_t pages_needed = 0;
   // byte offsets inside the workspace
-  size_t off_items = 0, off_row_tok = 0, off_page_list = 0, off_tok_req = 0, off_req = 0,
-         off_tok_slot = 0, off_merge_tok = 0, off_opart = 0, off_lpart = 0, total_bytes = 0, blob_bytes = 0;
+  size_t off_items = 0, off_row_tok = 0, off_page_list = 0, off_tok_slot = 0, off_segs = 0, off_steps = 0,
+         off_workers = 0, off_merge_tok = 0, off_merge_head = 0, off_opart = 0, off_lpart = 0, total_bytes = 0,
+         blob_bytes = 0;
   std::vector<unsigned char> blob;  // host image of [0, blob_bytes)
   void* dev_ws = nullptr;
   size_t dev_ws_bytes = 0;

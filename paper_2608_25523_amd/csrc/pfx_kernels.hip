@@ -13,17 +13,19 @@
 // neither operand; each lane loads 8 keys x (D/16) dims and transposes them
 // in registers with byte permutes.
 //
-// Work is a list of items (see pfx_internal.h), run in stream-ordered
-// launches.  Phase A: a workgroup of four waves runs one item; the item's
-// K/V streams once through an LDS ring and every wave multiplies it against
-// its own query columns (16 or 32 of them); the item writes either final
-// rows (extend) or a partial result over its key range (a prefix chunk
-// shared by an agent's decode rows, or an early suffix chunk).
-// Phase B: one workgroup per (decode request, KV head) streams the last
-// suffix chunk, its four waves splitting the steps, and merges their states
-// with the request's phase-A partials (log-sum-exp merge) through LDS
-// before writing the final rows.  The launch boundary
-// orders the two phases, so no atomics or device-wide fences are needed.
+// Three launches per call, in stream order:
+//   extend blocks: one workgroup per block of <= 128 query columns of one
+//     request and one KV head, streaming the prefix and the causal suffix
+//     through an LDS ring; rows written directly.
+//   decode: persistent workers.  The decode items (an agent's prefix against
+//     a block of its decode rows, a request's suffix against its own rows;
+//     one KV head each) are cut into 32-key steps, and every workgroup takes
+//     an equal contiguous run of the step list.  A worker's runs of steps
+//     flow through one LDS ring without a break at item boundaries; each
+//     piece of an item ends in final rows or a partial result.
+//   merge: rows seen by several pieces combine their partial results by
+//     log-sum-exp weights.
+// The launch boundaries order the phases: no atomics or device-wide fences.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -39,6 +41,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
@@ -55,6 +58,43 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Max / sum over the four lanes l, l ^ 16, l ^ 32, l ^ 48 (the lanes holding
+// one query column), with the gfx950 row-swap instructions instead of LDS
+// permutes.  v_permlane16_swap a, b exchanges the odd 16-lane rows of a with
+// the even rows of b, v_permlane32_swap the upper half of a with the lower
+// half of b; applied to two copies of x, the pair holds {own, partner} in
+// every lane, so all four lanes end with the same value.  Issued through asm:
+// the compiler's builtins for these instructions return the first register
+// for both results.  The nops keep clear of VALU-to-permlane hazards.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void row_swap16(uint32_t& a, uint32_t& b) {
+  asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+}
+__device__ __forceinline__ void row_swap32(uint32_t& a, uint32_t& b) {
+  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+}
+#pragma clang diagnostic pop
+
+__device__ __forceinline__ float column_max(float x) {
+  uint32_t a = __builtin_bit_cast(uint32_t, x), b = a;
+  row_swap16(a, b);
+  x = fmaxf(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b));
+  a = __builtin_bit_cast(uint32_t, x);
+  b = a;
+  row_swap32(a, b);
+  return fmaxf(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b));
+}
+__device__ __forceinline__ float column_sum(float x) {
+  uint32_t a = __builtin_bit_cast(uint32_t, x), b = a;
+  row_swap16(a, b);
+  x = __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);
+  a = __builtin_bit_cast(uint32_t, x);
+  b = a;
+  row_swap32(a, b);
+  return __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);
+}
 
 // V chunk held by one lane for one key: D/16 bf16 values.
 template <int D> struct VecCH;
@@ -75,8 +115,8 @@ struct AttnArgs {
   uint16_t* o;
   float* lse;
   DevPlan plan;
-  int32_t item_base;
   int32_t hq, hkv, group, group_shift;
+  int32_t num_workers, num_cus;  // decode launch: workers, compute units of the device
   float scale_log2;  // sm_scale * log2(e)
 };
 
@@ -101,56 +141,6 @@ __device__ __forceinline__ StepPos step_pos(const Item& it, int st, int s0_steps
     p.seg = 1;
   }
   return p;
-}
-
-// 64 consecutive page ids of a segment, one per lane, so a step finds its
-// pages with v_readlane instead of a dependent scalar load.
-struct PageWindow {
-  int32_t vpage;  // lane i: page id at list position base + i (i < count)
-  int32_t seg;    // segment held (-1: none)
-  int32_t base;
-  int32_t count;
-};
-
-__device__ __forceinline__ void window_for(PageWindow& w, const int32_t* page_list, const StepPos& p, int lane) {
-  const int pos = p.k0 >> 4;  // even: steps start on 32-key boundaries
-  if (p.seg != w.seg || pos < w.base || pos + 1 >= w.base + w.count) {
-    const int npages = (p.kend + 15) >> 4;
-    w.seg = p.seg;
-    w.base = pos;
-    w.count = 64;
-    w.vpage = (pos + lane < npages) ? page_list[p.list_off + pos + lane] : 0;
-  }
-}
-
-template <int D>
-__device__ __forceinline__ void load_kv(KVRegs<D>& r, const AttnArgs& a, PageWindow& w, const StepPos& p, int h,
-                                        int lane) {
-  constexpr int KS = D / 32;
-  constexpr int CH = D / 16;
-  const int col = lane & 15, grp = lane >> 4;
-  window_for(w, a.plan.page_list, p, lane);
-  const int pos = (p.k0 >> 4) - w.base;
-  const int page0 = __builtin_amdgcn_readlane(w.vpage, pos);
-  const bool has1 = p.k0 + 16 < p.kend;
-  const int page1 = has1 ? __builtin_amdgcn_readlane(w.vpage, pos + 1) : page0;
-  const size_t head_elems = size_t(16) * D;
-  const size_t b0 = (size_t(page0) * a.hkv + h) * head_elems;
-  const size_t b1 = (size_t(page1) * a.hkv + h) * head_elems;
-  const uint16_t* k0p = a.kpool + b0 + col * D + 8 * grp;
-  const uint16_t* k1p = a.kpool + b1 + col * D + 8 * grp;
-#pragma unroll
-  for (int s = 0; s < KS; ++s) {
-    r.k[0][s] = *reinterpret_cast<const u32x4*>(k0p + 32 * s);
-    r.k[1][s] = *reinterpret_cast<const u32x4*>(k1p + 32 * s);
-  }
-  const uint16_t* v0p = a.vpool + b0 + (4 * grp) * D + CH * col;
-  const uint16_t* v1p = a.vpool + b1 + (4 * grp) * D + CH * col;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    r.v[0][i] = *reinterpret_cast<const typename VecCH<D>::T*>(v0p + i * D);
-    r.v[1][i] = *reinterpret_cast<const typename VecCH<D>::T*>(v1p + i * D);
-  }
 }
 
 // bf16 element e (0..D/16-1) of a lane's V chunk, as the low 16 bits.
@@ -251,8 +241,7 @@ __device__ __forceinline__ void compute_steps(WaveState<D, QB>& ws, KVRegs<D>* c
       mx = fmaxf(mx, fmaxf(fmaxf(fmaxf(sc[u][0], sc[u][1]), fmaxf(sc[u][2], sc[u][3])),
                            fmaxf(fmaxf(sc[u][4], sc[u][5]), fmaxf(sc[u][6], sc[u][7]))));
     }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    mx = column_max(mx);
     mx *= scale_log2;  // scale > 0: max of the scaled scores
     const bool raise = mx > ws.m[b] + kRescaleSlack;
     if (__any(raise)) {
@@ -325,7 +314,7 @@ __device__ __forceinline__ void merge_row8(const float* o_row, size_t o_stride, 
 }
 
 // ---------------------------------------------------------------------------
-// Phase A: LDS-staged tiles shared by the four waves of a workgroup.
+// LDS-staged K/V shared by the four waves of a workgroup.
 //
 // A step's K/V (two 16-token pages of one KV head, K and V) is copied from
 // the pool straight into LDS with global_load_lds_dwordx4 -- no registers
@@ -337,11 +326,8 @@ __device__ __forceinline__ void merge_row8(const float* o_row, size_t o_stride, 
 // t * chunks + (c ^ t): the MFMA operand reads (16 tokens at one chunk, or
 // one token's 16 chunks) then fall in 16 different bank groups.
 // ---------------------------------------------------------------------------
-// Stages of the LDS ring: extend workgroups (one wave group) keep 3 steps in
-// flight; decode prefix workgroups (two groups taking alternate steps) keep
-// two rounds of two steps in flight.
+// Stages of the LDS ring: three in flight while one is consumed.
 constexpr int kStages = 4;
-constexpr int kDecodeStages = 6;
 
 template <int D>
 struct TileGeom {
@@ -415,30 +401,6 @@ __device__ __forceinline__ uint32_t lds_address(const unsigned char* p) {
   return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_bytes)(p)));
 }
 
-// Issue this wave's share of step st into a stage buffer.
-template <int D>
-__device__ __forceinline__ void issue_tile(unsigned char* stage, const AttnArgs& a, const Item& it, const int* ptab,
-                                           int lead, int p0n, int st, int s0_steps, int h, int wave, int lane) {
-  using TG = TileGeom<D>;
-  const StepPos p = step_pos(it, st, s0_steps);
-  const int t = wave & 1;
-  const bool is_v = wave >> 1;
-  const int seg_base = p.seg == 0 ? it.s0_kbeg : it.s1_kbeg;
-  int idx = (p.seg == 0 ? 0 : p0n) + ((p.k0 - seg_base) >> 4);
-  if (t == 1 && p.k0 + 16 < p.kend) idx += 1;  // a missing second page re-reads the first (masked later)
-  // The item's leading page ids sit one per lane in `lead`; later ones in the LDS table.
-  const int page = idx < kItemPages ? __builtin_amdgcn_readlane(lead, idx) : ptab[idx];
-  const uint16_t* base = (is_v ? a.vpool : a.kpool) + (size_t(page) * a.hkv + h) * (16 * D);
-  const uint32_t dst = lds_address(stage) + wave * TG::page_bytes;
-#pragma unroll
-  for (int j = 0; j < TG::loads_per_wave; ++j) {
-    const int q = 64 * j + lane;
-    const int tt = q / TG::chunks;
-    const int cc = (q % TG::chunks) ^ (tt & (TG::chunks - 1));
-    copy16_to_lds(base + tt * D + cc * 8, dst + 1024 * j);
-  }
-}
-
 // Read a stage into the register layout compute_step expects.
 template <int D>
 __device__ __forceinline__ void read_tile(KVRegs<D>& r, const unsigned char* stage, int col, int grp) {
@@ -464,25 +426,23 @@ __device__ __forceinline__ void read_tile(KVRegs<D>& r, const unsigned char* sta
     }
 }
 
-// Normalise a wave's block and write it: final bf16 rows, or an fp32 partial.
+// Normalise a wave's block and write it: lane (col, grp) holds dims
+// CH*(4*grp + i) + jj of its column.  Final rows go to o (bf16) and lse;
+// partial rows to the plan's o_part and l_part (fp32).  The column's output
+// row is orow; invalid columns (padding) write nothing.
 template <int D>
-__device__ __forceinline__ void write_block(const AttnArgs& a, const Item& it, const f32x4 (&acc)[D / 16], float m,
-                                            float l_lane, int c, int tok, int grp) {
+__device__ __forceinline__ void write_rows(const AttnArgs& a, const f32x4 (&acc)[D / 16], float m, float l_lane,
+                                           int orow, bool valid, bool final_rows, int grp) {
   constexpr int CH = D / 16;
-  float l = l_lane;
-  l += __shfl_xor(l, 16);
-  l += __shfl_xor(l, 32);
-  const int j = c >> a.group_shift;
-  if (j >= it.row_count) return;
-  const int g = c & (a.group - 1);
-  const int qh = it.kv_head * a.group + g;
+  const float l = column_sum(l_lane);
+  if (!valid) return;
   const float inv = l > 0.f ? 1.0f / l : 0.f;
-  // A row can see none of a chunk's keys (a multi-row decode request whose
-  // later suffix chunk starts after its first row): O = 0, LSE = -inf,
-  // which the merge weighs with exp(-inf) = 0.
+  // A row can see none of a piece's keys (a multi-row decode request whose
+  // later suffix piece starts after its first row): O = 0, LSE = -inf, which
+  // the merge weighs with exp(-inf) = 0.
   const float lse_nat = l > 0.f ? (m + log2f(l)) * kLn2 : -INFINITY;
-  if (it.out_slot < 0) {
-    uint16_t* out = a.o + (size_t(tok) * a.hq + qh) * D + 4 * CH * grp;
+  if (final_rows) {
+    uint16_t* out = a.o + size_t(orow) * D + 4 * CH * grp;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       if constexpr (CH == 8) {
@@ -494,12 +454,9 @@ __device__ __forceinline__ void write_block(const AttnArgs& a, const Item& it, c
         *reinterpret_cast<u32x2*>(out + CH * i) = w;
       }
     }
-    if (a.lse && grp == 0) a.lse[size_t(tok) * a.hq + qh] = lse_nat;
+    if (a.lse && grp == 0) a.lse[orow] = lse_nat;
   } else {
-    const int r = a.plan.tok_req[tok];
-    const ReqInfo ri = a.plan.req[r];
-    const size_t prow = size_t(ri.part_base) + size_t(it.out_slot) * ri.n + (tok - ri.q_start);
-    float* out = a.plan.o_part + (prow * a.hq + qh) * D + 4 * CH * grp;
+    float* out = a.plan.o_part + size_t(orow) * D + 4 * CH * grp;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -507,90 +464,91 @@ __device__ __forceinline__ void write_block(const AttnArgs& a, const Item& it, c
         f32x4 v = {acc[jj][i] * inv, acc[jj + 1][i] * inv, acc[jj + 2][i] * inv, acc[jj + 3][i] * inv};
         *reinterpret_cast<f32x4*>(out + CH * i + jj) = v;
       }
-    if (grp == 0) a.plan.l_part[prow * a.hq + qh] = lse_nat;
+    if (grp == 0) a.plan.l_part[orow] = lse_nat;
   }
 }
 
-// One step of a phase-A item: wait for this wave's copies of step st, meet
-// the other waves (stage st complete everywhere, stage st-1 consumed), refill
-// that freed stage with step st + kStages - 1, then multiply stage st.
-// One round of a phase-A item: every wave waits for its own copies of the
-// round, all waves meet (the round's stages complete everywhere, the previous
-// round's stages consumed), the freed stages are refilled with the round
-// R - 1 ahead, and each wave group multiplies its own step of the round.
-template <int D, int QBW, int NS, int NG>
-__device__ __forceinline__ void tile_round(WaveState<D, QBW>& ws, const bf16x8 (&qf)[QBW][D / 32],
-                                           const int (&lim)[QBW], unsigned char (*ring)[TileGeom<D>::stage_bytes],
-                                           const AttnArgs& a, const Item& it, const int* ptab, int lead, int p0n, int r,
-                                           int s0_steps, int nsteps, int nb, int h, int g, int wq, int lane) {
+// ---------------------------------------------------------------------------
+// Extend blocks.
+// ---------------------------------------------------------------------------
+
+// Issue this wave's share of an extend block's step st into a stage buffer:
+// tile (wave & 1) of K (waves 0, 1) or of V (waves 2, 3).
+template <int D>
+__device__ __forceinline__ void issue_block_step(unsigned char* stage, const AttnArgs& a, const Item& it,
+                                                 const int* ptab, int lead, int p0n, int st, int s0_steps, int h,
+                                                 int wave, int lane) {
   using TG = TileGeom<D>;
-  constexpr int R = NS / NG;  // rounds held by the ring
-  const int st = NG * r + g;  // this group's step in round r
-  const int last = (nsteps - 1 - g) / NG;  // this group's last round (negative: none)
-  const int ahead = last - r < R - 2 ? last - r : R - 2;
-  wait_vmcnt(ahead > 0 ? ahead * TG::loads_per_wave : 0);
-  __syncthreads();
-  const int nxt = st + NG * (R - 1);
-  if (nxt < nsteps) issue_tile<D>(ring[nxt % NS], a, it, ptab, lead, p0n, nxt, s0_steps, h, wq, lane);
-  if (nb > 0 && st < nsteps) {
-    KVRegs<D> kv;
-    read_tile<D>(kv, ring[st % NS], lane & 15, lane >> 4);
-    compute_step<D, QBW>(ws, kv, qf, lim, step_pos(it, st, s0_steps), nb, lane >> 4, a.scale_log2);
+  const StepPos p = step_pos(it, st, s0_steps);
+  const int t = wave & 1;
+  const bool is_v = wave >> 1;
+  const int seg_base = p.seg == 0 ? it.s0_kbeg : it.s1_kbeg;
+  int idx = (p.seg == 0 ? 0 : p0n) + ((p.k0 - seg_base) >> 4);
+  if (t == 1 && p.k0 + 16 < p.kend) idx += 1;  // a missing second page re-reads the first (masked later)
+  // The block's leading page ids sit one per lane in `lead`; later ones in the LDS table.
+  const int page = idx < kItemPages ? __builtin_amdgcn_readlane(lead, idx) : ptab[idx];
+  const uint16_t* base = (is_v ? a.vpool : a.kpool) + (size_t(page) * a.hkv + h) * (16 * D);
+  const uint32_t dst = lds_address(stage) + wave * TG::page_bytes;
+#pragma unroll
+  for (int j = 0; j < TG::loads_per_wave; ++j) {
+    const int q = 64 * j + lane;
+    const int tt = q / TG::chunks;
+    const int cc = (q % TG::chunks) ^ (tt & (TG::chunks - 1));
+    copy16_to_lds(base + tt * D + cc * 8, dst + 1024 * j);
   }
 }
 
-// LDS bytes of a tile item: the ring, then the page table.
-template <int D, int NS>
-constexpr int tile_smem_bytes() { return NS * TileGeom<D>::stage_bytes + kMaxTilePages * 4; }
+// LDS bytes of an extend block: the ring, then the page table.
+template <int D>
+constexpr int extend_smem_bytes() { return kStages * TileGeom<D>::stage_bytes + kMaxTilePages * 4; }
 
-// An item whose K/V streams through an LDS ring shared by the workgroup.
-// NG groups of four waves: the four waves of a group own different query
-// columns; the groups take alternate 32-key steps of the item and merge
-// their softmax states through LDS before the rows are written.
-template <int D, int QBW, int NS, int NG>
-__device__ __forceinline__ void tile_item(const AttnArgs& a, const Item* itp, unsigned char* smem) {
+// One extend block (QBW blocks of 16 columns per wave): its K/V streams once
+// through the LDS ring; at every step each wave waits for its own copies,
+// all waves meet (the step's stage complete everywhere, the previous stage
+// consumed), the freed stage is refilled kStages - 1 steps ahead, and every
+// wave multiplies the step against its own columns.
+template <int D, int QBW>
+__device__ __forceinline__ void extend_block(const AttnArgs& a, const Item* itp, unsigned char* smem) {
   using TG = TileGeom<D>;
   constexpr int KS = D / 32;
   constexpr int CH = D / 16;
-  static_assert(NS % NG == 0 && NS / NG >= 2, "the ring holds whole rounds");
+  constexpr int NS = kStages;
   auto ring = reinterpret_cast<unsigned char (*)[TG::stage_bytes]>(smem);
   int* ptab = reinterpret_cast<int*>(smem + NS * TG::stage_bytes);
-  const int lead = itp->first_pages[threadIdx.x & (kItemPages - 1)];  // issued before the item's scalar load
+  const int lead = itp->first_pages[threadIdx.x & (kItemPages - 1)];  // issued before the block's scalar load
   const Item it = *itp;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int g = wave / kTileWaves;   // wave group: which steps
-  const int wq = wave % kTileWaves;  // role inside the group: which columns, which quarter of a stage
   const int lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
   const int h = it.kv_head;
   const int G = a.group;
 
-  // Page ids of both segments, staged once per item.
+  // Page ids of both segments, staged once per block.
   const int p0b = it.s0_kbeg >> 4;
   const int p0n = it.s0_kend > it.s0_kbeg ? ((it.s0_kend + 15) >> 4) - p0b : 0;
   const int p1b = it.s1_kbeg >> 4;
   const int p1n = it.s1_kend > it.s1_kbeg ? ((it.s1_kend + 15) >> 4) - p1b : 0;
-  for (int i = threadIdx.x; i < p0n + p1n; i += 256 * NG)
+  for (int i = threadIdx.x; i < p0n + p1n; i += 256)
     ptab[i] = i < p0n ? a.plan.page_list[it.s0_page_off + p0b + i] : a.plan.page_list[it.s1_page_off + p1b + i - p0n];
 
-  // This wave's query columns: blocks wq*QBW .. wq*QBW + QBW - 1.
+  // This wave's query columns: blocks wave*QBW .. wave*QBW + QBW - 1.
   const int ncols = it.row_count * G;
-  int nb = (ncols - wq * QBW * kTileCols + kTileCols - 1) / kTileCols;
+  int nb = (ncols - wave * QBW * kTileCols + kTileCols - 1) / kTileCols;
   nb = nb < 0 ? 0 : (nb > QBW ? QBW : nb);
   bf16x8 qf[QBW][KS];
   int lim[QBW];
-  int tok_of[QBW];
+  int orow[QBW];
 #pragma unroll
   for (int b = 0; b < QBW; ++b) {
-    const int c = (wq * QBW + b) * kTileCols + col;
+    const int c = (wave * QBW + b) * kTileCols + col;
     int j = c >> a.group_shift;
     const int gg = c & (G - 1);
     if (j >= it.row_count) j = 0;
-    const int tok = it.tok0 >= 0 ? it.tok0 + j : a.plan.row_tok[it.row_begin + j];
-    tok_of[b] = tok;
+    const int tok = it.tok0 + j;
     lim[b] = tok + it.causal_base;
+    orow[b] = tok * a.hq + h * G + gg;
     if (b < nb) {
-      const uint16_t* qp = a.q + (size_t(tok) * a.hq + h * G + gg) * D + 8 * grp;
+      const uint16_t* qp = a.q + size_t(orow[b]) * D + 8 * grp;
 #pragma unroll
       for (int s = 0; s < KS; ++s) qf[b][s] = *reinterpret_cast<const bf16x8*>(qp + 32 * s);
     } else {
@@ -609,200 +567,260 @@ __device__ __forceinline__ void tile_item(const AttnArgs& a, const Item* itp, un
   const int s0_steps = (it.s0_kend - it.s0_kbeg + kStepKeys - 1) / kStepKeys;
   const int s1_steps = (it.s1_kend - it.s1_kbeg + kStepKeys - 1) / kStepKeys;
   const int nsteps = s0_steps + s1_steps;
-  const int rounds = (nsteps + NG - 1) / NG;
-  // The first rounds' pages are among the leading ids: request them before
+  // The first steps' pages are among the leading ids: request them before
   // waiting for the page table.
-  constexpr int R = NS / NG;
-  for (int r = 0; r < R - 1; ++r) {
-    const int st = NG * r + g;
-    if (st < nsteps) issue_tile<D>(ring[st % NS], a, it, ptab, lead, p0n, st, s0_steps, h, wq, lane);
-  }
+  for (int st = 0; st < NS - 1 && st < nsteps; ++st)
+    issue_block_step<D>(ring[st], a, it, ptab, lead, p0n, st, s0_steps, h, wave, lane);
   __syncthreads();  // page table ready
-  for (int r = 0; r < rounds; ++r)
-    tile_round<D, QBW, NS, NG>(ws, qf, lim, ring, a, it, ptab, lead, p0n, r, s0_steps, nsteps, nb, h, g, wq, lane);
-
-  if constexpr (NG == 2) {
-    // Group 1 hands its state to group 0, lane for lane (same register layout).
-    constexpr int NV = QBW * (4 * CH + 2);
-    float* xch = reinterpret_cast<float*>(&ring[0][0]);  // kTileWaves * NV * 64 floats
-    static_assert(kTileWaves * NV * 64 * 4 <= NS * TG::stage_bytes, "exchange fits in the ring");
-    __syncthreads();  // ring no longer read
-    if (g == 1) {
-#pragma unroll
-      for (int b = 0; b < QBW; ++b) {
-        float* x = xch + ((wq * QBW + b) * (4 * CH + 2)) * 64 + lane;
-#pragma unroll
-        for (int jj = 0; jj < CH; ++jj)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) x[(4 * jj + i) * 64] = ws.acc[b][jj][i];
-        x[(4 * CH) * 64] = ws.m[b];
-        x[(4 * CH + 1) * 64] = ws.l[b];
-      }
-    }
+  for (int st = 0; st < nsteps; ++st) {
+    const int ahead = nsteps - 1 - st < NS - 2 ? nsteps - 1 - st : NS - 2;
+    wait_vmcnt(ahead * TG::loads_per_wave);
     __syncthreads();
-    if (g == 1) return;
-#pragma unroll
-    for (int b = 0; b < QBW; ++b) {
-      const float* x = xch + ((wq * QBW + b) * (4 * CH + 2)) * 64 + lane;
-      const float m1 = x[(4 * CH) * 64];
-      const float mn = fmaxf(ws.m[b], m1);
-      const float f0 = fast_exp2(ws.m[b] - mn), f1 = fast_exp2(m1 - mn);
-      ws.l[b] = ws.l[b] * f0 + x[(4 * CH + 1) * 64] * f1;
-#pragma unroll
-      for (int jj = 0; jj < CH; ++jj)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) ws.acc[b][jj][i] = ws.acc[b][jj][i] * f0 + x[(4 * jj + i) * 64] * f1;
-      ws.m[b] = mn;
+    const int nxt = st + NS - 1;
+    if (nxt < nsteps) issue_block_step<D>(ring[nxt % NS], a, it, ptab, lead, p0n, nxt, s0_steps, h, wave, lane);
+    if (nb > 0) {
+      KVRegs<D> kv;
+      read_tile<D>(kv, ring[st % NS], col, grp);
+      compute_step<D, QBW>(ws, kv, qf, lim, step_pos(it, st, s0_steps), nb, grp, a.scale_log2);
     }
   }
-
 #pragma unroll
   for (int b = 0; b < QBW; ++b) {
-    if (b >= nb) break;
-    write_block<D>(a, it, ws.acc[b], ws.m[b], ws.l[b], (wq * QBW + b) * kTileCols + col, tok_of[b], grp);
+    const int c = (wave * QBW + b) * kTileCols + col;
+    write_rows<D>(a, ws.acc[b], ws.m[b], ws.l[b], orow[b], b < nb && (c >> a.group_shift) < it.row_count, true,
+                  grp);
   }
 }
 
-// LDS bytes of a suffix unit: the four waves' states.
+// Extend blocks: final rows, 32 query columns per wave.
 template <int D>
-constexpr int unit_smem_bytes() { return kTileWaves * kTileCols * (D + 4) * 4 + 2 * kTileWaves * kTileCols * 4; }
+__global__ __launch_bounds__(256, 2) void extend_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[extend_smem_bytes<D>()];
+  extend_block<D, 2>(a, a.plan.items + blockIdx.x, smem);
+}
 
-// A decode request's suffix chunk for one KV head: the four waves take its
-// 32-key steps round-robin (each with the request's <= 16 query columns, two
-// register buffers and its own softmax state), then combine through LDS and
-// write the chunk's partial result, or the final rows when the chunk is all
-// the row sees.
+// ---------------------------------------------------------------------------
+// Decode workers.
+//
+// A worker runs its segments in order through one LDS ring.  Every segment
+// contributes a Q stage (the segment's query rows, each wave's 16 columns in
+// its quarter of the stage) followed by its K/V steps, so stage u of the
+// worker is refilled with stage u + kStages - 1 whatever segment that is: an
+// item boundary does not drain the ring.  The wait for stage u is "all but
+// the later stages' copies done" (copies complete in order); a wave counts
+// the copies it issued per stage, since a wave with no columns in a segment
+// copies no Q.
+// ---------------------------------------------------------------------------
 template <int D>
-__device__ __forceinline__ void suffix_unit(const AttnArgs& a, const Item* itp, unsigned char* smem) {
+constexpr int decode_smem_bytes() {
+  return kStages * TileGeom<D>::stage_bytes + kWorkerSegs * int(sizeof(Seg)) + kWorkerSteps * 8;
+}
+
+// Position in a worker's stage sequence: the Q stage of segment seg (k < 0)
+// or its K/V step k, which is the worker's step `step`; with the fields of
+// segment seg the sequence needs (read from LDS once per segment).
+struct Cursor {
+  int seg, k, step;
+  int nst, ncols, qh0;
+};
+
+__device__ __forceinline__ int lds_uniform(const int32_t& x) { return __builtin_amdgcn_readfirstlane(x); }
+
+__device__ __forceinline__ void enter(Cursor& c, const Seg* segs, int nseg, int group) {
+  if (c.seg >= nseg) return;
+  const i32x4 h = *reinterpret_cast<const i32x4*>(&segs[c.seg].h);  // kind, kv_head, ncols, nsteps
+  c.qh0 = __builtin_amdgcn_readfirstlane(h[1]) * group;
+  c.ncols = __builtin_amdgcn_readfirstlane(h[2]);
+  c.nst = __builtin_amdgcn_readfirstlane(h[3]);
+}
+
+__device__ __forceinline__ void advance(Cursor& c, const Seg* segs, int nseg, int group) {
+  if (c.k < 0) {
+    c.k = 0;
+    return;
+  }
+  ++c.step;
+  if (++c.k == c.nst) {
+    ++c.seg;
+    c.k = -1;
+    enter(c, segs, nseg, group);
+  }
+}
+
+// Block ids (page * Hkv + head) of this wave's tile for 64 consecutive
+// steps of the worker, one per lane: a step finds its page with v_readlane.
+struct StepWindow {
+  int blk;
+  int base;
+};
+
+__device__ __forceinline__ void load_window(StepWindow& w, const int32_t* stab, int base, int nsteps, int wave,
+                                            int lane) {
+  w.base = base;
+  w.blk = base + lane < nsteps ? stab[2 * (base + lane) + (wave & 1)] : 0;
+}
+
+// Issue this wave's copies of the stage at cursor c; returns how many
+// (a wave with no columns in a segment copies no Q).
+template <int D>
+__device__ __forceinline__ int issue_stage(unsigned char* stage, const AttnArgs& a, const Seg* segs,
+                                           const int32_t* stab, StepWindow& win, int nsteps, const Cursor& c,
+                                           int wave, int lane) {
+  using TG = TileGeom<D>;
+  const uint32_t dst = lds_address(stage) + wave * TG::page_bytes;
+  if (c.k >= 0) {
+    // K/V: tile (wave & 1) of K (waves 0, 1) or V (waves 2, 3), swizzled.
+    if (c.step - win.base >= 64) load_window(win, stab, win.base + 64, nsteps, wave, lane);
+    const int blk = __builtin_amdgcn_readlane(win.blk, c.step - win.base);
+    const uint16_t* base = ((wave >> 1) ? a.vpool : a.kpool) + size_t(blk) * (16 * D);
+#pragma unroll
+    for (int j = 0; j < TG::loads_per_wave; ++j) {
+      const int q = 64 * j + lane;
+      const int tt = q / TG::chunks;
+      const int cc = (q % TG::chunks) ^ (tt & (TG::chunks - 1));
+      copy16_to_lds(base + tt * D + cc * 8, dst + 1024 * j);
+    }
+    return TG::loads_per_wave;
+  }
+  // Q: chunk (p % chunks) of this wave's column p / chunks at 16 p; padding
+  // columns repeat the segment's first column.
+  if (16 * wave >= c.ncols) return 0;
+  const Seg& sg = segs[c.seg];
+#pragma unroll
+  for (int j = 0; j < TG::loads_per_wave; ++j) {
+    const int q = 64 * j + lane;
+    int cl = 16 * wave + q / TG::chunks;
+    cl = cl < c.ncols ? cl : 0;
+    const uint16_t* src =
+        a.q + (size_t(sg.tok[cl >> a.group_shift]) * a.hq + c.qh0 + (cl & (a.group - 1))) * D + 8 * (q % TG::chunks);
+    copy16_to_lds(src, dst + 1024 * j);
+  }
+  return TG::loads_per_wave;
+}
+
+// Wait until this wave's copies of all but its `later` most recent copying
+// stages are done (each such stage issued loads_per_wave copies).
+template <int D>
+__device__ __forceinline__ void wait_stages(int later) {
+  constexpr int L = TileGeom<D>::loads_per_wave;
+  static_assert(kStages - 2 <= 3 && 3 * L <= 63, "vmcnt immediates");
+#define PFX_VMCNT(N) __builtin_amdgcn_s_waitcnt(((N) & 15) | (7 << 4) | (15 << 8) | (((N) >> 4) << 14))
+  if (later <= 0)
+    PFX_VMCNT(0);
+  else if (later == 1)
+    PFX_VMCNT(L);
+  else if (later == 2)
+    PFX_VMCNT(2 * L);
+  else
+    PFX_VMCNT(3 * L);
+#undef PFX_VMCNT
+}
+
+// Workgroups are dispatched one per compute unit first (blocks 0 .. C-1),
+// then a second round on the same units (block b + C beside block b).  The
+// two workgroups of a unit are given adjacent workers, whose steps come from
+// the same region of the step list (same kind of item, same compute per
+// stage), so no unit pairs a light worker with a heavy one.  Any bijection
+// is correct; this one only shapes the timing.
+__device__ __forceinline__ int worker_of_block(int b, int nw, int ncu) {
+  if (nw <= ncu || b >= 2 * ncu) return b;
+  const int pairs = nw - ncu < ncu ? nw - ncu : ncu;
+  if (b >= ncu) return 2 * (b - ncu) + 1;
+  return b < pairs ? 2 * b : pairs + b;
+}
+
+template <int D>
+__global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
+  using TG = TileGeom<D>;
   constexpr int KS = D / 32;
   constexpr int CH = D / 16;
-  constexpr int DS = D / 16;  // dims per thread in the combine
-  auto red_o = reinterpret_cast<float (*)[kTileCols][D + 4]>(smem);
-  auto red_m = reinterpret_cast<float (*)[kTileCols]>(smem + kTileWaves * kTileCols * (D + 4) * 4);
-  auto red_l = red_m + kTileWaves;
-  // The item's leading page ids are requested before its scalar fields: the
-  // window they form covers the first steps of all four waves.
-  PageWindow win{itp->first_pages[threadIdx.x & (kItemPages - 1)], 1, 0, kItemPages};
-  const Item it = *itp;
-  win.base = it.s1_kbeg >> 4;
+  constexpr int NS = kStages;
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[decode_smem_bytes<D>()];
+  auto ring = reinterpret_cast<unsigned char (*)[TG::stage_bytes]>(smem);
+  Seg* segs = reinterpret_cast<Seg*>(smem + NS * TG::stage_bytes);
+  int32_t* stab = reinterpret_cast<int32_t*>(smem + NS * TG::stage_bytes + kWorkerSegs * sizeof(Seg));
+  const Worker wk = a.plan.workers[worker_of_block(blockIdx.x, a.num_workers, a.num_cus)];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
-  const int h = it.kv_head;
-  const int G = a.group;
-  const int nsteps = (it.s1_kend - it.s1_kbeg + kStepKeys - 1) / kStepKeys;
+
+  // The worker's segments (<= kWorkerSegs) and step table (<= kWorkerSteps)
+  // into LDS.
   {
-    KVRegs<D> bufA, bufB;
-    int st = wave;
-    if (st < nsteps) load_kv<D>(bufA, a, win, step_pos(it, st, 0), h, lane);
-    int j = col >> a.group_shift;
-    if (j >= it.row_count) j = 0;  // padding column: a copy of the first token, never stored
-    const int tok = it.tok0 + j;  // a suffix unit's tokens are consecutive
-    const int qh = h * G + (col & (G - 1));
-    bf16x8 qf[1][KS];
-    int lim[1] = {tok + it.causal_base};
-    const uint16_t* qp = a.q + (size_t(tok) * a.hq + qh) * D + 8 * grp;
-#pragma unroll
-    for (int s = 0; s < KS; ++s) qf[0][s] = *reinterpret_cast<const bf16x8*>(qp + 32 * s);
-    WaveState<D, 1> ws;
-    ws.m[0] = kNegBig;
-    ws.l[0] = 0.f;
-#pragma unroll
-    for (int jj = 0; jj < CH; ++jj) ws.acc[0][jj] = f32x4{0.f, 0.f, 0.f, 0.f};
-    while (st < nsteps) {
-      int nst = st + kTileWaves;
-      if (nst < nsteps) load_kv<D>(bufB, a, win, step_pos(it, nst, 0), h, lane);
-      compute_step<D, 1>(ws, bufA, qf, lim, step_pos(it, st, 0), 1, grp, a.scale_log2);
-      st = nst;
-      if (st >= nsteps) break;
-      nst = st + kTileWaves;
-      if (nst < nsteps) load_kv<D>(bufA, a, win, step_pos(it, nst, 0), h, lane);
-      compute_step<D, 1>(ws, bufB, qf, lim, step_pos(it, st, 0), 1, grp, a.scale_log2);
-      st = nst;
-    }
-    float l = ws.l[0];
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int jj = 0; jj < CH; ++jj) red_o[wave][col][CH * (4 * grp + i) + jj] = ws.acc[0][jj][i];
-    if (grp == 0) {
-      red_m[wave][col] = ws.m[0];
-      red_l[wave][col] = l;
-    }
+    const u32x4* src = reinterpret_cast<const u32x4*>(a.plan.segs + wk.seg_begin);
+    u32x4* dst = reinterpret_cast<u32x4*>(segs);
+    const int nvec = wk.nseg * int(sizeof(Seg) / 16);
+    for (int i = threadIdx.x; i < nvec; i += 256) dst[i] = src[i];
+    const u32x2* ss = reinterpret_cast<const u32x2*>(a.plan.steps) + wk.step_begin;
+    for (int i = threadIdx.x; i < wk.nsteps; i += 256) reinterpret_cast<u32x2*>(stab)[i] = ss[i];
   }
   __syncthreads();
 
-  // Combine: thread t owns column t / 16 and dims (t % 16) * D/16 .. +D/16.
-  const int c = threadIdx.x >> 4;
-  const int d0 = (threadIdx.x & 15) * DS;
-  const int j = c >> a.group_shift;
-  if (j >= it.row_count) return;
-  const int tok = it.tok0 + j;
-  const int qh = h * G + (c & (G - 1));
-  float mx = kNegBig;
-#pragma unroll
-  for (int w = 0; w < kTileWaves; ++w) mx = fmaxf(mx, red_m[w][c]);
-  float z = 0.f;
-  float o[DS];
-#pragma unroll
-  for (int e = 0; e < DS; ++e) o[e] = 0.f;
-#pragma unroll
-  for (int w = 0; w < kTileWaves; ++w) {
-    const float f = fast_exp2(red_m[w][c] - mx);
-    z += f * red_l[w][c];
-#pragma unroll
-    for (int e = 0; e < DS; ++e) o[e] += f * red_o[w][c][d0 + e];
+  const int nstages = wk.nsteps + wk.nseg;
+  StepWindow win;
+  load_window(win, stab, 0, wk.nsteps, wave, lane);
+  Cursor ic{0, -1, 0, 0, 0, 0};
+  enter(ic, segs, wk.nseg, a.group);
+  Cursor cc = ic;
+  // One bit per recent stage, newest lowest: did this wave copy anything?
+  uint32_t hist = 0;
+  for (int u = 0; u < NS - 1 && u < nstages; ++u) {
+    hist = (hist << 1) | uint32_t(issue_stage<D>(ring[u], a, segs, stab, win, wk.nsteps, ic, wave, lane) > 0);
+    advance(ic, segs, wk.nseg, a.group);
   }
-  // A row can see none of a chunk's keys (a multi-row decode request whose
-  // later suffix chunk starts after its first row): O = 0, LSE = -inf.
-  const float inv = z > 0.f ? 1.0f / z : 0.f;
-  const float lse_nat = z > 0.f ? (mx + log2f(z)) * kLn2 : -INFINITY;
-  if (it.out_slot < 0) {
-    uint16_t* out = a.o + (size_t(tok) * a.hq + qh) * D + d0;
-    if constexpr (DS == 8) {
-      u32x4 w = {pack_bf16(o[0] * inv, o[1] * inv), pack_bf16(o[2] * inv, o[3] * inv),
-                 pack_bf16(o[4] * inv, o[5] * inv), pack_bf16(o[6] * inv, o[7] * inv)};
-      *reinterpret_cast<u32x4*>(out) = w;
-    } else {
-      u32x2 w = {pack_bf16(o[0] * inv, o[1] * inv), pack_bf16(o[2] * inv, o[3] * inv)};
-      *reinterpret_cast<u32x2*>(out) = w;
+
+  WaveState<D, 1> ws;
+  bf16x8 qf[1][KS];
+  int lim[1] = {0};
+  int orow = 0, k0 = 0, kend = 0, causal = 0;
+  bool has_cols = false, valid = false, final_rows = false;
+  for (int u = 0; u < nstages; ++u) {
+    // Wait for stage u: only the copies of the stages issued after it
+    // (u + 1 .. u + ahead, the newest bits of hist) may still be pending.
+    const int ahead = nstages - 1 - u < NS - 2 ? nstages - 1 - u : NS - 2;
+    wait_stages<D>(__builtin_popcount(hist & ((1u << ahead) - 1u)));
+    __syncthreads();
+    if (u + NS - 1 < nstages) {
+      hist = (hist << 1) |
+             uint32_t(issue_stage<D>(ring[(u + NS - 1) % NS], a, segs, stab, win, wk.nsteps, ic, wave, lane) > 0);
+      advance(ic, segs, wk.nseg, a.group);
     }
-    if (a.lse && d0 == 0) a.lse[size_t(tok) * a.hq + qh] = lse_nat;
-  } else {
-    const ReqInfo ri = a.plan.req[it.req];
-    const size_t prow = size_t(ri.part_base) + size_t(it.out_slot) * ri.n + (tok - ri.q_start);
-    float* out = a.plan.o_part + (prow * a.hq + qh) * D + d0;
+    const unsigned char* stage = ring[u % NS];
+    if (cc.k < 0) {
+      // A segment starts: its columns, limits, output rows and Q.
+      const Seg& sg = segs[cc.seg];
+      const i32x4 h1 = *reinterpret_cast<const i32x4*>(&sg.h.k0);  // k0, kend, causal_base, slot
+      const i32x4 h2 = *reinterpret_cast<const i32x4*>(&sg.h.item);  // item, piece, causal, -
+      k0 = __builtin_amdgcn_readfirstlane(h1[0]);
+      kend = __builtin_amdgcn_readfirstlane(h1[1]);
+      final_rows = __builtin_amdgcn_readfirstlane(h1[3]) < 0;
+      causal = __builtin_amdgcn_readfirstlane(h2[2]);
+      has_cols = 16 * wave < cc.ncols;
+      const int c = 16 * wave + col;
+      valid = c < cc.ncols;
+      const int j = valid ? c >> a.group_shift : 0;
+      const int tok = sg.tok[j];
+      lim[0] = causal ? tok + __builtin_amdgcn_readfirstlane(h1[2]) : 0x7fffffff;
+      orow = sg.out[j] + (c & (a.group - 1));
+      if (has_cols) {
+        const unsigned char* qb = stage + wave * TG::page_bytes;
 #pragma unroll
-    for (int e = 0; e < DS; e += 4) {
-      f32x4 v = {o[e] * inv, o[e + 1] * inv, o[e + 2] * inv, o[e + 3] * inv};
-      *reinterpret_cast<f32x4*>(out + e) = v;
+        for (int s = 0; s < KS; ++s)
+          qf[0][s] = *reinterpret_cast<const bf16x8*>(qb + 16 * (col * TG::chunks + 4 * s + grp));
+      }
+      ws.m[0] = kNegBig;
+      ws.l[0] = 0.f;
+#pragma unroll
+      for (int jj = 0; jj < CH; ++jj) ws.acc[0][jj] = f32x4{0.f, 0.f, 0.f, 0.f};
+    } else if (has_cols) {
+      KVRegs<D> kv;
+      read_tile<D>(kv, stage, col, grp);
+      const StepPos p{0, k0 + kStepKeys * cc.k, kend, causal};
+      compute_step<D, 1>(ws, kv, qf, lim, p, 1, grp, a.scale_log2);
+      if (cc.k == cc.nst - 1) write_rows<D>(a, ws.acc[0], ws.m[0], ws.l[0], orow, valid, final_rows, grp);
     }
-    if (d0 == 0) a.plan.l_part[prow * a.hq + qh] = lse_nat;
+    advance(cc, segs, wk.nseg, a.group);
   }
-}
-
-// Extend blocks: final rows, 32 query columns per wave, one wave group.
-template <int D>
-__global__ __launch_bounds__(256, 2) void extend_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[tile_smem_bytes<D, kStages>()];
-  tile_item<D, 2, kStages, 1>(a, a.plan.items + a.item_base + blockIdx.x, smem);
-}
-
-// Decode pieces in one launch: prefix chunks shared by an agent's decode
-// rows (LDS tiles, 16 columns per wave) and suffix chunks (four-wave units);
-// none depends on another.
-template <int D>
-__global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
-  constexpr int kSmem = tile_smem_bytes<D, kStages>() > unit_smem_bytes<D>() ? tile_smem_bytes<D, kStages>()
-                                                                             : unit_smem_bytes<D>();
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[kSmem];
-  const Item* itp = a.plan.items + a.item_base + blockIdx.x;
-  if (itp->kind == kPrefixItem)
-    tile_item<D, 1, kStages, 1>(a, itp, smem);
-  else
-    suffix_unit<D>(a, itp, smem);
 }
 
 // The rows of decode requests seen by several pieces: log-sum-exp merge of
@@ -818,18 +836,20 @@ __global__ __launch_bounds__(256) void merge_rows_kernel(AttnArgs a, int n_tok) 
   if (t >= size_t(n_tok) * a.hq * SL) return;
   const int sl = int(t % SL);
   const int qh = int((t / SL) % a.hq);
-  const int tok = a.plan.merge_tok[t / (size_t(SL) * a.hq)];
-  const ReqInfo ri = a.plan.req[a.plan.tok_req[tok]];
-  const size_t row0 = size_t(ri.part_base) + (tok - ri.q_start);
-  const size_t lstride = size_t(ri.n) * a.hq;
-  const float* lp = a.plan.l_part + row0 * a.hq + qh;
-  const float* op = a.plan.o_part + (row0 * a.hq + qh) * D + sl * 8;
+  const int m = int(t / (size_t(SL) * a.hq));
+  const MergeHead mh = a.plan.merge_head[size_t(m) * a.hkv + (qh >> a.group_shift)];
+  if (mh.nparts < 2) return;  // written directly by its only piece
+  const int tok = a.plan.merge_tok[m];
+  const size_t row0 = size_t(mh.base) * a.group + (qh & (a.group - 1));
+  const size_t lstride = size_t(a.group);
+  const float* lp = a.plan.l_part + row0;
+  const float* op = a.plan.o_part + row0 * D + sl * 8;
   const size_t ostride = lstride * D;
   float lv[kMergeBatch];
   f32x4 ov[kMergeBatch][2];
 #pragma unroll
   for (int k = 0; k < kMergeBatch; ++k) {
-    if (k < ri.nparts) {
+    if (k < mh.nparts) {
       lv[k] = lp[k * lstride];
       ov[k][0] = *reinterpret_cast<const f32x4*>(op + k * ostride);
       ov[k][1] = *reinterpret_cast<const f32x4*>(op + k * ostride + 4);
@@ -841,7 +861,7 @@ __global__ __launch_bounds__(256) void merge_rows_kernel(AttnArgs a, int n_tok) 
   float mx = -INFINITY;
 #pragma unroll
   for (int k = 0; k < kMergeBatch; ++k) mx = fmaxf(mx, lv[k]);
-  for (int k = kMergeBatch; k < ri.nparts; ++k) mx = fmaxf(mx, lp[k * lstride]);
+  for (int k = kMergeBatch; k < mh.nparts; ++k) mx = fmaxf(mx, lp[k * lstride]);
   float z = 0.f;
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -854,7 +874,7 @@ __global__ __launch_bounds__(256) void merge_rows_kernel(AttnArgs a, int n_tok) 
       acc[4 + e] += w * ov[k][1][e];
     }
   }
-  for (int k = kMergeBatch; k < ri.nparts; ++k) {
+  for (int k = kMergeBatch; k < mh.nparts; ++k) {
     const float w = fast_exp2((lp[k * lstride] - mx) * kLog2e);
     z += w;
     const f32x4 x = *reinterpret_cast<const f32x4*>(op + k * ostride);
@@ -940,14 +960,8 @@ static int check_pool_matches(const pfx_pool* pool, const pfx_plan* p, const cha
 
 template <int D>
 static void launch_all(AttnArgs a, const pfx_plan* p, hipStream_t s) {
-  if (p->n_extend) {
-    a.item_base = p->n_decode;
-    hipLaunchKernelGGL((extend_kernel<D>), dim3(p->n_extend), dim3(256), 0, s, a);
-  }
-  if (p->n_decode) {
-    a.item_base = 0;
-    hipLaunchKernelGGL((decode_kernel<D>), dim3(p->n_decode), dim3(256), 0, s, a);
-  }
+  if (!p->items.empty()) hipLaunchKernelGGL((extend_kernel<D>), dim3(p->items.size()), dim3(256), 0, s, a);
+  if (!p->workers.empty()) hipLaunchKernelGGL((decode_kernel<D>), dim3(p->workers.size()), dim3(256), 0, s, a);
   const int n_tok = static_cast<int>(p->merge_tok.size());
   if (n_tok) {
     const size_t threads = size_t(n_tok) * p->hq * (D / 8);
@@ -999,7 +1013,7 @@ extern "C" int pfx_attention(const pfx_pool* pool, const pfx_plan* p, const void
                              float sm_scale, void* stream) {
   int rc = check_pool_matches(pool, p, "pfx_attention");
   if (rc) return rc;
-  if (p->items.empty()) return PFX_OK;
+  if (p->items.empty() && p->workers.empty()) return PFX_OK;
   if (!q || !o) return fail(PFX_EINVAL, "pfx_attention: q or o is NULL");
   if (!(sm_scale > 0.f)) sm_scale = 1.0f / sqrtf(float(p->d));
   AttnArgs a;
@@ -1014,6 +1028,15 @@ extern "C" int pfx_attention(const pfx_pool* pool, const pfx_plan* p, const void
   a.group = p->group;
   a.group_shift = __builtin_ctz(static_cast<unsigned>(p->group));
   a.scale_log2 = sm_scale * kLog2e;
+  a.num_workers = static_cast<int32_t>(p->workers.size());
+  a.num_cus = 0;
+  {
+    int dev = 0, ncu = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess)
+      a.num_cus = ncu;
+  }
+  if (a.num_cus <= 0) a.num_cus = a.num_workers;  // identity mapping
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (p->d == 128) launch_all<128>(a, p, s); else launch_all<64>(a, p, s);
   return check_launch("pfx_attention");

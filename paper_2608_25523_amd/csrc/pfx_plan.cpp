@@ -35,10 +35,12 @@ DevPlan dev_plan(const pfx_plan* p) {
   d.items = reinterpret_cast<const Item*>(base + p->off_items);
   d.row_tok = reinterpret_cast<const int32_t*>(base + p->off_row_tok);
   d.page_list = reinterpret_cast<const int32_t*>(base + p->off_page_list);
-  d.tok_req = reinterpret_cast<const int32_t*>(base + p->off_tok_req);
-  d.req = reinterpret_cast<const ReqInfo*>(base + p->off_req);
   d.tok_slot = reinterpret_cast<const int32_t*>(base + p->off_tok_slot);
+  d.segs = reinterpret_cast<const Seg*>(base + p->off_segs);
+  d.steps = reinterpret_cast<const int32_t*>(base + p->off_steps);
+  d.workers = reinterpret_cast<const Worker*>(base + p->off_workers);
   d.merge_tok = reinterpret_cast<const int32_t*>(base + p->off_merge_tok);
+  d.merge_head = reinterpret_cast<const MergeHead*>(base + p->off_merge_head);
   d.o_part = reinterpret_cast<float*>(base + p->off_opart);
   d.l_part = reinterpret_cast<float*>(base + p->off_lpart);
   return d;
@@ -125,8 +127,6 @@ extern "C" void pfx_alloc_destroy(pfx_alloc* a) { delete a; }
 
 namespace {
 
-constexpr int32_t kDefaultPrefixChunk = 512;
-constexpr int32_t kDefaultSuffixChunk = 512;
 
 int check_pool_shape(const pfx_pool* pool, const char* who) {
   if (!pool) return fail(PFX_EINVAL, "%s: pool is NULL", who);
@@ -160,21 +160,16 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
     return fail(PFX_EUNSUPPORTED, "pfx_plan_create: query group %d (1, 2, 4, 8 or 16 supported)", G);
   if (mode != PFX_MODE_EXTEND && mode != PFX_MODE_DECODE && mode != PFX_MODE_MIXED)
     return fail(PFX_EINVAL, "pfx_plan_create: mode %d", mode);
-  int32_t pchunk = kDefaultPrefixChunk, schunk = kDefaultSuffixChunk;
+  int32_t workers_hint = kDefaultWorkers;
   if (opts) {
-    for (int i = 0; i < 6; ++i)
+    for (int i = 0; i < 7; ++i)
       if (opts->reserved[i]) return fail(PFX_EINVAL, "pfx_plan_create: opts.reserved[%d] != 0", i);
-    if (opts->prefix_chunk < 0 || opts->prefix_chunk % kStepKeys)
-      return fail(PFX_EINVAL, "pfx_plan_create: prefix_chunk %d is not a multiple of %d", opts->prefix_chunk,
-                  kStepKeys);
-    if (opts->suffix_chunk < 0 || opts->suffix_chunk % kStepKeys)
-      return fail(PFX_EINVAL, "pfx_plan_create: suffix_chunk %d is not a multiple of %d", opts->suffix_chunk,
-                  kStepKeys);
-    if (opts->prefix_chunk > kMaxTilePages * PFX_PAGE_SIZE || opts->suffix_chunk > kMaxTilePages * PFX_PAGE_SIZE)
-      return fail(PFX_EUNSUPPORTED, "pfx_plan_create: chunks are limited to %d keys", kMaxTilePages * PFX_PAGE_SIZE);
-    if (opts->prefix_chunk) pchunk = opts->prefix_chunk;
-    if (opts->suffix_chunk) schunk = opts->suffix_chunk;
+    if (opts->decode_workers < 0 || opts->decode_workers > (1 << 20))
+      return fail(PFX_EINVAL, "pfx_plan_create: decode_workers %d outside [0, %d]", opts->decode_workers, 1 << 20);
+    if (opts->decode_workers) workers_hint = opts->decode_workers;
   }
+  if (int64_t(pool->num_pages) * hkv > INT32_MAX)
+    return fail(PFX_EUNSUPPORTED, "pfx_plan_create: num_pages * num_kv_heads must stay below 2^31");
 
   // ---- prefix table ----
   const int32_t A = pt->num_agents;
@@ -290,7 +285,7 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   p->req.resize(R);
   for (int32_t r = 0; r < R; ++r) {
     const int32_t q0 = b->q_indptr[r], n = b->q_indptr[r + 1] - q0, L = b->suffix_len[r];
-    p->req[r] = ReqInfo{q0, n, 0, 0};
+    p->req[r] = ReqInfo{q0, n};
     for (int32_t i = 0; i < n; ++i) {
       int32_t pos = L - n + i;
       int32_t page = b->suffix_page_ids[b->suffix_indptr[r] + pos / PFX_PAGE_SIZE];
@@ -303,106 +298,200 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
     int32_t n = p->req[r].n;
     return n >= 1 && n * G <= kTileCols;
   };
-  auto nchunks = [](int32_t len, int32_t chunk) { return len <= 0 ? 0 : (len + chunk - 1) / chunk; };
   auto blocks_for = [&](int32_t tokens) { return (tokens * G + kTileCols - 1) / kTileCols; };
 
-  std::vector<Item> items;
-  std::vector<int32_t> prefix_chunks(R, 0);
-
-  // Grouped decode over each agent's prefix: the agent's decode rows are
-  // packed into items of up to 64 query columns; every prefix chunk is read
-  // once per (row block, KV head) and shared by all the rows in the block.
+  // ---- decode items (Sec. 3): each agent's prefix once per block of its
+  // decode rows and KV head, then each request's own suffix per KV head ----
+  struct DItem {
+    int32_t kind, h, keys, page_off, causal_base;
+    int32_t row_first, rows;  // tokens drow_tok[row_first .. + rows)
+    int64_t step_first;
+    int32_t npieces;
+  };
+  std::vector<DItem> dit;
+  std::vector<int32_t> drow_tok;
+  std::vector<int32_t> pf_item(size_t(R) * hkv, -1), sf_item(size_t(R) * hkv, -1);
   for (int32_t a = 0; a < A; ++a) {
-    if (!referenced[a]) continue;
-    const int32_t P = pt->prefix_len[a];
+    if (!referenced[a] || pt->prefix_len[a] == 0) continue;
     std::vector<int32_t> members;
     for (int32_t r = 0; r < R; ++r)
       if (b->agent[r] == a && is_decode_class(r)) members.push_back(r);
-    if (members.empty() || P == 0) continue;
-    const int32_t nc = nchunks(P, pchunk);
-    struct RowBlock { int32_t begin, tokens; };
-    std::vector<RowBlock> blocks;
-    int32_t cols = kDecodeTileCols;  // forces a new block at the first member
-    for (int32_t r : members) {
-      int32_t n = p->req[r].n;
-      if (cols + n * G > kDecodeTileCols) {
-        blocks.push_back(RowBlock{static_cast<int32_t>(p->row_tok.size()), 0});
-        cols = 0;
+    size_t i = 0;
+    while (i < members.size()) {
+      // A block of rows whose columns (rows x G) fit one 64-column item.
+      const int32_t first = static_cast<int32_t>(drow_tok.size());
+      int32_t cols = 0;
+      std::vector<int32_t> in_block;
+      while (i < members.size() && cols + p->req[members[i]].n * G <= kDecodeTileCols) {
+        const int32_t r = members[i++];
+        for (int32_t t = 0; t < p->req[r].n; ++t) drow_tok.push_back(p->req[r].q_start + t);
+        cols += p->req[r].n * G;
+        in_block.push_back(r);
       }
-      for (int32_t i = 0; i < n; ++i) p->row_tok.push_back(p->req[r].q_start + i);
-      blocks.back().tokens += n;
-      cols += n * G;
-      prefix_chunks[r] = nc;
+      const int32_t rows = static_cast<int32_t>(drow_tok.size()) - first;
+      for (int32_t h = 0; h < hkv; ++h) {
+        for (int32_t r : in_block) pf_item[size_t(r) * hkv + h] = static_cast<int32_t>(dit.size());
+        dit.push_back(DItem{kPrefixItem, h, pt->prefix_len[a], prefix_off[a], 0, first, rows, 0, 0});
+        ++p->n_prefix_items;
+      }
     }
-    for (int32_t c = 0; c < nc; ++c)
-      for (int32_t h = 0; h < hkv; ++h)
-        for (const RowBlock& rb : blocks) {
-          Item it{};
-          it.kv_head = h;
-          it.row_begin = rb.begin;
-          it.row_count = rb.tokens;
-          it.nblk = blocks_for(rb.tokens);
-          it.s0_page_off = prefix_off[a];
-          it.s0_kbeg = c * pchunk;
-          it.s0_kend = std::min(P, (c + 1) * pchunk);
-          it.s1_page_off = 0;
-          it.s1_kbeg = it.s1_kend = 0;
-          it.causal_base = 0;
-          it.out_slot = c;
-          it.kind = kPrefixItem;
-          it.req = -1;
-          items.push_back(it);
-          ++p->n_prefix_items;
-        }
   }
-
-  // Decode rows against each request's own suffix, in chunks of up to
-  // schunk keys, one four-wave unit per (chunk, KV head).  A row seen by
-  // more than one piece (prefix chunks, suffix chunks) gets one partial
-  // result per piece, merged by the last launch; a row seen by a single
-  // piece is written directly.
-  int64_t part_rows = 0;
   for (int32_t r = 0; r < R; ++r) {
     if (!is_decode_class(r)) continue;
     const ReqInfo ri = p->req[r];
-    const int32_t L = b->suffix_len[r];
-    const int32_t ns = nchunks(L, schunk);
-    const int32_t pieces = prefix_chunks[r] + ns;
-    p->req[r].nparts = pieces > 1 ? pieces : 0;
-    if (pieces > 1) {
-      p->req[r].part_base = static_cast<int32_t>(part_rows);
-      part_rows += int64_t(pieces) * ri.n;
-      for (int32_t i = 0; i < ri.n; ++i) p->merge_tok.push_back(ri.q_start + i);
+    const int32_t L = b->suffix_len[r];  // >= n >= 1: the suffix holds the new tokens
+    const int32_t first = static_cast<int32_t>(drow_tok.size());
+    for (int32_t t = 0; t < ri.n; ++t) drow_tok.push_back(ri.q_start + t);
+    for (int32_t h = 0; h < hkv; ++h) {
+      sf_item[size_t(r) * hkv + h] = static_cast<int32_t>(dit.size());
+      dit.push_back(DItem{kSuffixItem, h, L, suffix_off[r], L - ri.n - ri.q_start, first, ri.n, 0, 0});
+      ++p->n_suffix_items;
     }
-    const int32_t rb = static_cast<int32_t>(p->row_tok.size());
-    for (int32_t i = 0; i < ri.n; ++i) p->row_tok.push_back(ri.q_start + i);
-    for (int32_t j = 0; j < ns; ++j)
-      for (int32_t h = 0; h < hkv; ++h) {
-        Item it{};
-        it.kv_head = h;
-        it.row_begin = rb;
-        it.row_count = ri.n;
-        it.nblk = 1;
-        it.s0_page_off = 0;
-        it.s0_kbeg = it.s0_kend = 0;
-        it.s1_page_off = suffix_off[r];
-        it.s1_kbeg = j * schunk;
-        it.s1_kend = std::min(L, (j + 1) * schunk);
-        it.causal_base = L - ri.n - ri.q_start;
-        it.kind = kSuffixItem;
-        it.req = r;
-        it.out_slot = pieces > 1 ? prefix_chunks[r] + j : -1;
-        items.push_back(it);
-        ++p->n_suffix_items;
-      }
   }
 
-  // Extend rows: blocks of up to 64 query columns of one request, over the
-  // whole prefix (no mask) then the suffix (causal).  Written directly.
+  // ---- decode steps: 32 keys = two 16-key pages of one KV head ----
+  int64_t T = 0;
+  for (DItem& x : dit) {
+    x.step_first = T;
+    T += (x.keys + kStepKeys - 1) / kStepKeys;
+  }
+  if (T > INT32_MAX / 2) return delete p, fail(PFX_ERANGE, "pfx_plan_create: too many decode steps");
+  p->steps.resize(size_t(2 * T));
+  for (const DItem& x : dit) {
+    const int32_t npages = static_cast<int32_t>(pages_for(x.keys));
+    const int32_t ns = (x.keys + kStepKeys - 1) / kStepKeys;
+    for (int32_t i = 0; i < ns; ++i) {
+      const int32_t pg0 = 2 * i, pg1 = 2 * i + 1 < npages ? 2 * i + 1 : 2 * i;  // a missing page repeats (masked)
+      p->steps[size_t(2 * (x.step_first + i))] = p->page_list[x.page_off + pg0] * hkv + x.h;
+      p->steps[size_t(2 * (x.step_first + i)) + 1] = p->page_list[x.page_off + pg1] * hkv + x.h;
+    }
+  }
+
+  // ---- workers: contiguous runs of the step list, each costing at most B
+  // ring stages (one per step, plus one per segment for its query rows) and
+  // holding at most kWorkerSegs segments and kWorkerSteps steps.  Runs are
+  // filled greedily, so each is full but the last; B is the smallest budget
+  // that needs no more than the requested number of workers. ----
+  // Stage costs in tenths: a prefix step multiplies 64 query columns, a
+  // suffix step at most 16, so a prefix step keeps its workgroup a little
+  // longer; a Q stage moves little data.
+  constexpr int64_t kPrefixStepCost = 11, kSuffixStepCost = 10, kQStageCost = 10;
+  std::vector<int32_t> npieces(dit.size(), 0);
+  if (T > 0) {
+    const int64_t W = std::max<int64_t>(std::min<int64_t>(workers_hint, T), (T + kWorkerSteps - 1) / kWorkerSteps);
+    auto item_end = [&](size_t x) { return dit[x].step_first + (dit[x].keys + kStepKeys - 1) / kStepKeys; };
+    auto fill = [&](int64_t B, bool build) {
+      int64_t g = 0, count = 0;
+      size_t x = 0;
+      if (build) {
+        p->workers.clear();
+        p->segs.clear();
+        std::fill(npieces.begin(), npieces.end(), 0);
+      }
+      while (g < T) {
+        Worker wk{static_cast<int32_t>(g), 0, static_cast<int32_t>(p->segs.size()), 0};
+        int64_t cost = 0;
+        while (g < T && wk.nseg < kWorkerSegs && wk.nsteps < kWorkerSteps) {
+          while (item_end(x) <= g) ++x;
+          const int64_t step_cost = dit[x].kind == kPrefixItem ? kPrefixStepCost : kSuffixStepCost;
+          const int64_t room = (B - cost - kQStageCost) / step_cost;  // steps that still fit
+          if (wk.nseg > 0 && room < 1) break;
+          const int64_t take =
+              std::min({item_end(x) - g, std::max<int64_t>(room, 1), int64_t(kWorkerSteps - wk.nsteps)});
+          if (build) {
+            const DItem& it = dit[x];
+            Seg sg{};
+            sg.h.kind = it.kind;
+            sg.h.kv_head = it.h;
+            sg.h.ncols = it.rows * G;
+            sg.h.nsteps = static_cast<int32_t>(take);
+            sg.h.k0 = static_cast<int32_t>(g - it.step_first) * kStepKeys;
+            sg.h.kend = it.keys;
+            sg.h.causal_base = it.causal_base;
+            sg.h.causal = it.kind == kSuffixItem && it.rows > 1;
+            sg.h.item = static_cast<int32_t>(x);
+            sg.h.piece = npieces[x]++;
+            p->segs.push_back(sg);
+          }
+          ++wk.nseg;
+          wk.nsteps += static_cast<int32_t>(take);
+          g += take;
+          cost += kQStageCost + take * step_cost;
+        }
+        if (build) p->workers.push_back(wk);
+        ++count;
+      }
+      return count;
+    };
+    int64_t lo = 1, hi = (kWorkerSteps + kWorkerSegs) * 20;  // hi: the caps alone bound a run
+    while (lo < hi) {
+      const int64_t mid = (lo + hi) / 2;
+      if (fill(mid, false) <= W) hi = mid; else lo = mid + 1;
+    }
+    fill(lo, true);
+  }
+  for (size_t x = 0; x < dit.size(); ++x) dit[x].npieces = npieces[x];
+
+  // ---- partial slots: a decode row of KV head h is seen by the pieces of
+  // its prefix item (slots 0 ..) and then of its suffix item; with one piece
+  // in all the row is written directly, otherwise the merge (Sec. 4.2,
+  // Eq. (8)) combines the slots ----
+  std::vector<int32_t> tok_base(size_t(total_tokens) * hkv, -1), np_prefix(size_t(R) * hkv, 0),
+      np_total(size_t(R) * hkv, 0);
+  int64_t part_units = 0;
+  for (int32_t r = 0; r < R; ++r) {
+    if (!is_decode_class(r)) continue;
+    bool any = false;
+    for (int32_t h = 0; h < hkv; ++h) {
+      const size_t rh = size_t(r) * hkv + h;
+      np_prefix[rh] = pf_item[rh] >= 0 ? dit[pf_item[rh]].npieces : 0;
+      np_total[rh] = np_prefix[rh] + dit[sf_item[rh]].npieces;
+      any |= np_total[rh] >= 2;
+    }
+    if (!any) continue;
+    for (int32_t t = 0; t < p->req[r].n; ++t) {
+      const int32_t tok = p->req[r].q_start + t;
+      p->merge_tok.push_back(tok);
+      for (int32_t h = 0; h < hkv; ++h) {
+        const int32_t np = np_total[size_t(r) * hkv + h];
+        if (np >= 2) {
+          tok_base[size_t(tok) * hkv + h] = static_cast<int32_t>(part_units);
+          p->merge_head.push_back(MergeHead{static_cast<int32_t>(part_units), np});
+          part_units += np;
+        } else {
+          p->merge_head.push_back(MergeHead{0, 0});
+        }
+      }
+    }
+  }
+  if (part_units * G > (int64_t(1) << 31) / std::max(1, p->d))
+    return delete p, fail(PFX_ERANGE, "pfx_plan_create: too many partial rows");
+  p->num_part_rows = part_units * G;
+  for (Seg& sg : p->segs) {
+    const DItem& it = dit[sg.h.item];
+    for (int32_t j = 0; j < it.rows; ++j) {
+      const int32_t tok = drow_tok[it.row_first + j];
+      const int32_t r = p->tok_req[tok];
+      const size_t rh = size_t(r) * hkv + it.h;
+      sg.tok[j] = tok;
+      if (np_total[rh] >= 2) {
+        const int32_t slot = (it.kind == kPrefixItem ? 0 : np_prefix[rh]) + sg.h.piece;
+        sg.h.slot = slot;  // the same for every row of the piece
+        sg.out[j] = (tok_base[size_t(tok) * hkv + it.h] + slot) * G;
+      } else {
+        sg.h.slot = -1;
+        sg.out[j] = tok * hq + it.h * G;
+      }
+    }
+  }
+
+  // ---- extend blocks (Sec. 3): up to 128 query columns of one request,
+  // over the whole prefix (no mask) then the suffix (causal), written
+  // directly ----
+  std::vector<Item> items;
   for (int32_t r = 0; r < R; ++r) {
     const ReqInfo ri = p->req[r];
     if (ri.n == 0 || is_decode_class(r)) continue;
-    p->req[r].nparts = 0;
     const int32_t a = b->agent[r];
     const int32_t P = a >= 0 ? pt->prefix_len[a] : 0;
     const int32_t L = b->suffix_len[r];
@@ -432,40 +521,18 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
       }
     }
   }
-  if (part_rows > (int64_t(1) << 31) / std::max(1, hq))
-    return delete p, fail(PFX_ERANGE, "pfx_plan_create: too many partial rows");
-  p->num_part_rows = part_rows;
-
-  // Two launches, then the merge: decode pieces (prefix chunks shared by an
-  // agent's rows, and suffix chunks) all write partial results and depend on
-  // nothing, so they share one launch; extend blocks (final rows) are the
-  // other; the merge of rows with several pieces runs last on the same
-  // stream.  Longest key ranges first inside a launch keeps the tail short.
-  auto cost = [](const Item& it) {
-    const int64_t keys = it.s0_kend - it.s0_kbeg + it.s1_kend - it.s1_kbeg;
-    return it.kind == kPrefixItem ? keys * 2 : keys;  // prefix pieces also carry 4x the columns
-  };
-  auto by_cost = [&](const Item& x, const Item& y) { return cost(x) > cost(y); };
-  std::vector<Item> dec, ext;
-  for (const Item& it : items) (it.kind == kExtendItem ? ext : dec).push_back(it);
-  std::stable_sort(dec.begin(), dec.end(), by_cost);
-  std::stable_sort(ext.begin(), ext.end(), by_cost);
-  // Each item's leading page ids and, for single-request items, its first token.
-  auto fill_head = [&](Item& it) {
+  // Longest key ranges first keeps the tail of the launch short.
+  auto cost = [](const Item& it) { return int64_t(it.s0_kend - it.s0_kbeg) + (it.s1_kend - it.s1_kbeg); };
+  std::stable_sort(items.begin(), items.end(), [&](const Item& x, const Item& y) { return cost(x) > cost(y); });
+  // Each block's leading page ids and first token.
+  for (Item& it : items) {
     int32_t k = 0;
     for (int32_t pg = it.s0_kbeg >> 4; it.s0_kend > it.s0_kbeg && pg < (it.s0_kend + 15) >> 4 && k < kItemPages; ++pg)
       it.first_pages[k++] = p->page_list[it.s0_page_off + pg];
     for (int32_t pg = it.s1_kbeg >> 4; it.s1_kend > it.s1_kbeg && pg < (it.s1_kend + 15) >> 4 && k < kItemPages; ++pg)
       it.first_pages[k++] = p->page_list[it.s1_page_off + pg];
-    it.tok0 = it.req >= 0 ? p->row_tok[it.row_begin] : -1;
-  };
-  for (Item& it : dec) fill_head(it);
-  for (Item& it : ext) fill_head(it);
-  p->n_decode = static_cast<int32_t>(dec.size());
-  p->n_extend = static_cast<int32_t>(ext.size());
-  items.clear();
-  items.insert(items.end(), dec.begin(), dec.end());
-  items.insert(items.end(), ext.begin(), ext.end());
+    it.tok0 = p->row_tok[it.row_begin];
+  }
   p->items = std::move(items);
 
   // ---- workspace layout ----
@@ -473,13 +540,15 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   p->off_items = off;      off = align256(off + p->items.size() * sizeof(Item));
   p->off_row_tok = off;    off = align256(off + p->row_tok.size() * 4);
   p->off_page_list = off;  off = align256(off + p->page_list.size() * 4);
-  p->off_tok_req = off;    off = align256(off + p->tok_req.size() * 4);
-  p->off_req = off;        off = align256(off + p->req.size() * sizeof(ReqInfo));
   p->off_tok_slot = off;   off = align256(off + p->tok_slot.size() * 4);
+  p->off_segs = off;       off = align256(off + p->segs.size() * sizeof(Seg));
+  p->off_steps = off;      off = align256(off + p->steps.size() * 4);
+  p->off_workers = off;    off = align256(off + p->workers.size() * sizeof(Worker));
   p->off_merge_tok = off;  off = align256(off + p->merge_tok.size() * 4);
+  p->off_merge_head = off; off = align256(off + p->merge_head.size() * sizeof(MergeHead));
   p->blob_bytes = off;
-  p->off_opart = off;      off = align256(off + size_t(part_rows) * hq * p->d * 4);
-  p->off_lpart = off;      off = align256(off + size_t(part_rows) * hq * 4);
+  p->off_opart = off;      off = align256(off + size_t(p->num_part_rows) * p->d * 4);
+  p->off_lpart = off;      off = align256(off + size_t(p->num_part_rows) * 4);
   p->total_bytes = std::max<size_t>(off, 256);
 
   p->blob.assign(p->blob_bytes, 0);
@@ -489,10 +558,12 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   put(p->off_items, p->items.data(), p->items.size() * sizeof(Item));
   put(p->off_row_tok, p->row_tok.data(), p->row_tok.size() * 4);
   put(p->off_page_list, p->page_list.data(), p->page_list.size() * 4);
-  put(p->off_tok_req, p->tok_req.data(), p->tok_req.size() * 4);
-  put(p->off_req, p->req.data(), p->req.size() * sizeof(ReqInfo));
   put(p->off_tok_slot, p->tok_slot.data(), p->tok_slot.size() * 4);
+  put(p->off_segs, p->segs.data(), p->segs.size() * sizeof(Seg));
+  put(p->off_steps, p->steps.data(), p->steps.size() * 4);
+  put(p->off_workers, p->workers.data(), p->workers.size() * sizeof(Worker));
   put(p->off_merge_tok, p->merge_tok.data(), p->merge_tok.size() * 4);
+  put(p->off_merge_head, p->merge_head.data(), p->merge_head.size() * sizeof(MergeHead));
 
   *out = p;
   return PFX_OK;
@@ -508,12 +579,16 @@ extern "C" int pfx_plan_get_stats(const pfx_plan* p, pfx_plan_stats* s) {
   if (!p || !s) return fail(PFX_EINVAL, "pfx_plan_get_stats: NULL argument");
   s->num_requests = p->num_reqs;
   s->num_tokens = p->num_tokens;
-  s->num_items = static_cast<int32_t>(p->items.size());
+  s->num_items = p->n_prefix_items + p->n_suffix_items + p->n_extend_items;
   s->num_prefix_items = p->n_prefix_items;
   s->num_suffix_items = p->n_suffix_items;
   s->num_extend_items = p->n_extend_items;
   s->num_partial_rows = static_cast<int32_t>(p->num_part_rows);
   s->pages_needed = p->pages_needed;
+  s->num_decode_steps = static_cast<int32_t>(p->steps.size() / 2);
+  s->num_decode_workers = static_cast<int32_t>(p->workers.size());
+  s->num_decode_segments = static_cast<int32_t>(p->segs.size());
+  s->reserved = 0;
   s->workspace_bytes = static_cast<int64_t>(p->total_bytes);
   return PFX_OK;
 }
@@ -526,6 +601,11 @@ extern "C" int pfx_plan_export(const pfx_plan* p, int32_t which, int32_t* out, i
     case 0: src = reinterpret_cast<const int32_t*>(p->items.data()); n = int64_t(p->items.size()) * 32; break;
     case 1: src = p->row_tok.data(); n = int64_t(p->row_tok.size()); break;
     case 2: src = p->page_list.data(); n = int64_t(p->page_list.size()); break;
+    case 3: src = reinterpret_cast<const int32_t*>(p->segs.data()); n = int64_t(p->segs.size()) * 144; break;
+    case 4: src = p->steps.data(); n = int64_t(p->steps.size()); break;
+    case 5: src = reinterpret_cast<const int32_t*>(p->workers.data()); n = int64_t(p->workers.size()) * 4; break;
+    case 6: src = p->merge_tok.data(); n = int64_t(p->merge_tok.size()); break;
+    case 7: src = reinterpret_cast<const int32_t*>(p->merge_head.data()); n = int64_t(p->merge_head.size()) * 2; break;
     default: return fail(PFX_EINVAL, "pfx_plan_export: which = %d", which);
   }
   *count = n;

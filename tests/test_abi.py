@@ -35,7 +35,7 @@ def test_library_exports_every_declared_function():
 
 
 def test_version_and_error_text():
-    assert B.pfx_version() == 10000
+    assert B.pfx_version() == 20000
     with pytest.raises(B.PfxError):
         B.Allocator(-1)
     assert "num_pages" in B.pfx_last_error()
@@ -101,7 +101,7 @@ def test_plan_validation_error_codes():
     expect_error(B.PFX_EUNSUPPORTED, lambda: raw_create(b, hq=6))              # G = 3
     expect_error(B.PFX_EINVAL, lambda: raw_create(b, mode=7))
     expect_error(B.PFX_EINVAL, lambda: raw_create(b, mode=B.PFX_MODE_DECODE))  # request with 33 rows
-    expect_error(B.PFX_EINVAL, lambda: raw_create(b, prefix_chunk=48))
+    expect_error(B.PFX_EINVAL, lambda: raw_create(b, decode_workers=-1))
     # Eq. (2): pool of 10 pages cannot hold 3 + 2 prefix pages and 1+2+3+1+1 suffix pages
     msg = expect_error(B.PFX_ENOMEM, lambda: raw_create(b, pool=pool(n=12)))
     assert "13 pages" in msg
@@ -149,65 +149,121 @@ def test_empty_batch_and_zero_row_requests():
 
 
 def enumerate_coverage(plan, batch):
-    """Count, from the exported work list, how often each (token, q head,
-    logical key) triple is attended, and by how many partial slots."""
-    items = plan.export(0)
-    row_tok = plan.export(1)
-    page_list = plan.export(2)
-    G = batch.group
+    """Count, from the exported work lists, how often each (token, q head,
+    logical key) triple is attended, and which output row each piece of a
+    row writes: ('final', row) or ('part', slot, row)."""
+    G, hkv, hq = batch.group, batch.num_kv_heads, batch.num_q_heads
     q_indptr = batch.q_indptr()
     tok_req = np.repeat(np.arange(len(batch.agent)), batch.n_rows)
-    counts = {}
-    slots = {}
+    counts, outs = {}, {}
+
+    def req_info(tok):
+        r = int(tok_req[tok])
+        a = int(batch.agent[r])
+        plen = int(batch.prefix_len[a]) if a >= 0 else 0
+        n, L = int(batch.n_rows[r]), int(batch.suffix_len[r])
+        return r, a, plen, L - n + (tok - int(q_indptr[r]))
+
+    def hit(tok, qh, k):
+        counts[(tok, qh, k)] = counts.get((tok, qh, k), 0) + 1
+
+    # Extend blocks: prefix then causal suffix, final rows.
+    items, row_tok, page_list = plan.export(0), plan.export(1), plan.export(2)
     for it in items:
         (h, rb, rc, nblk, s0p, s0b, s0e, s1p, s1b, s1e, cbase, slot, kind, req, tok0, _) = it[:16]
+        assert kind == 2 and slot == -1
         first = [int(x) for x in it[16:32]]
         lead = [int(page_list[s0p + k]) for k in range(s0b // 16, (s0e + 15) // 16)] if s0e > s0b else []
         lead += [int(page_list[s1p + k]) for k in range(s1b // 16, (s1e + 15) // 16)] if s1e > s1b else []
         assert first[:min(16, len(lead))] == lead[:16]
-        assert tok0 == (int(row_tok[rb]) if req >= 0 else -1)
+        assert tok0 == int(row_tok[rb])
         assert 1 <= nblk <= 8 and rc * G <= nblk * 16 and (rc * G > (nblk - 1) * 16)
         for j in range(rc):
             tok = int(row_tok[rb + j])
-            r = int(tok_req[tok])
-            a = int(batch.agent[r])
-            plen = int(batch.prefix_len[a]) if a >= 0 else 0
-            n, L = int(batch.n_rows[r]), int(batch.suffix_len[r])
-            pos_in_suffix = L - n + (tok - q_indptr[r])
+            assert tok == tok0 + j
+            r, a, plen, pos = req_info(tok)
             for g in range(G):
                 qh = h * G + g
                 for k in range(s0b, s0e):
-                    page = int(page_list[s0p + k // 16])
-                    assert page == int(batch.prefix_pages[a][k // 16])
-                    counts[(tok, qh, k)] = counts.get((tok, qh, k), 0) + 1
+                    assert int(page_list[s0p + k // 16]) == int(batch.prefix_pages[a][k // 16])
+                    hit(tok, qh, k)
                 for k in range(s1b, s1e):
-                    page = int(page_list[s1p + k // 16])
-                    assert page == int(batch.suffix_pages[r][k // 16])
+                    assert int(page_list[s1p + k // 16]) == int(batch.suffix_pages[r][k // 16])
                     if k <= tok + cbase:
-                        assert tok + cbase == pos_in_suffix
-                        counts[(tok, qh, plen + k)] = counts.get((tok, qh, plen + k), 0) + 1
-                slots.setdefault((tok, qh), []).append(int(slot))
-    return counts, slots
+                        assert tok + cbase == pos
+                        hit(tok, qh, plen + k)
+                outs.setdefault((tok, qh), []).append(("final", tok * hq + qh))
+
+    # Decode: workers split the step list into contiguous runs of segments.
+    segs, steps, workers = plan.export(3), plan.export(4), plan.export(5)
+    mtok, mhead = plan.export(6), plan.export(7).reshape(-1, hkv, 2)
+    midx = {int(t): i for i, t in enumerate(mtok)}
+    g_next, s_next = 0, 0
+    pieces = {}
+    for (sb, ns, segb, nseg) in workers:
+        assert sb == g_next and segb == s_next and 1 <= nseg <= 16 and 1 <= ns <= 256
+        at = sb
+        for sg in segs[segb:segb + nseg]:
+            kind, h, ncols, nst, k0, kend, cbase, slot, item, piece = (int(x) for x in sg[:10])
+            assert kind in (0, 1) and 1 <= ncols <= 64 and ncols % G == 0 and k0 % 32 == 0
+            lst = pieces.setdefault(item, [])
+            assert piece == len(lst)  # pieces appear in order
+            lst.append((piece, k0, nst, kend))
+            for j in range(ncols // G):
+                tok = int(sg[16 + j])
+                r, a, plen, pos = req_info(tok)
+                src = batch.prefix_pages[a] if kind == 0 else batch.suffix_pages[r]
+                for i in range(nst):
+                    kk = k0 + 32 * i
+                    assert kk < kend
+                    blk0, blk1 = (int(x) for x in steps[at + i])
+                    assert blk0 == int(src[kk // 16]) * hkv + h
+                    assert blk1 == (int(src[kk // 16 + 1]) if kk + 16 < kend else int(src[kk // 16])) * hkv + h
+                    for g in range(G):
+                        for k in range(kk, min(kk + 32, kend)):
+                            if kind == 0:
+                                hit(tok, h * G + g, k)
+                            elif k <= tok + cbase:
+                                assert tok + cbase == pos
+                                hit(tok, h * G + g, plen + k)
+                for g in range(G):
+                    row = int(sg[80 + j]) + g
+                    if slot < 0:
+                        assert row == tok * hq + h * G + g
+                        outs.setdefault((tok, h * G + g), []).append(("final", row))
+                    else:
+                        base, np_ = mhead[midx[tok], h]
+                        assert 0 <= slot < np_ and row == (base + slot) * G + g
+                        outs.setdefault((tok, h * G + g), []).append(("part", slot, row))
+            at += nst
+        assert at == sb + ns
+        g_next, s_next = sb + ns, segb + nseg
+    assert g_next == len(steps) and s_next == len(segs)
+    # Each item's pieces tile its key range in order.
+    for item, ps in pieces.items():
+        ends = [(k0, k0 + 32 * n) for (_, k0, n, _) in ps]
+        assert ends[0][0] == 0 and all(ends[i][1] == ends[i + 1][0] for i in range(len(ends) - 1))
+        assert ends[-1][1] >= ps[0][3] > ends[-1][1] - 32
+    return counts, outs
 
 
-@pytest.mark.parametrize("case", ["small", "small_chunks", "g1", "g16", "decode_only"])
+@pytest.mark.parametrize("case", ["small", "split", "g1", "g16", "decode_only", "decode_tiny_workers"])
 def test_plan_covers_every_visible_key_once(case):
     if case == "small":
         b, kw = small_batch(), {}
-    elif case == "small_chunks":
-        b, kw = small_batch(prefix_len=[100, 17], suffix_len=[70, 20, 33, 3, 40]), dict(prefix_chunk=32, suffix_chunk=32)
+    elif case == "split":
+        b, kw = small_batch(prefix_len=[100, 17], suffix_len=[70, 20, 33, 3, 40]), dict(decode_workers=7)
     elif case == "g1":
         b, kw = small_batch(num_q_heads=2), {}
     elif case == "g16":
-        b, kw = small_batch(num_q_heads=32, n_rows=[1, 1, 33, 1, 1]), dict(prefix_chunk=32)
+        b, kw = small_batch(num_q_heads=32, n_rows=[1, 1, 33, 1, 1]), dict(decode_workers=5)
     else:
         agents = np.arange(70) % 3 - 1
         b = W.make_batch(5, num_q_heads=8, num_kv_heads=2, head_dim=128, num_pages=512, prefix_len=[64, 300],
                          agent=agents, suffix_len=(np.arange(70) % 40) + 1, n_rows=np.ones(70, np.int32))
-        kw = dict(prefix_chunk=64, suffix_chunk=32)
+        kw = dict(decode_workers=64 if case == "decode_only" else 3)
     p = plan_for(b, **kw)
-    counts, slots = enumerate_coverage(p, b)
-    G = b.group
+    counts, outs = enumerate_coverage(p, b)
     q_indptr = b.q_indptr()
     expected = 0
     for r in range(len(b.agent)):
@@ -222,17 +278,23 @@ def test_plan_covers_every_visible_key_once(case):
                     assert counts.get((tok, qh, k), 0) == 1, (tok, qh, k)
                 expected += vis
     assert sum(counts.values()) == expected            # nothing invisible is attended
-    # A row is written either by exactly one item (slot -1), or as partial
-    # slots 0 .. k-1 (k >= 2), each written once, merged afterwards.
-    items = p.export(0)
-    for (tok, qh), ss in slots.items():
-        if -1 in ss:
-            assert ss == [-1], (tok, qh, ss)
+    # A row is written either once, final, or as partial slots 0 .. k-1
+    # (k >= 2), each once, merged afterwards; no two rows share a partial row.
+    part_rows = []
+    mtok = set(int(t) for t in p.export(6))
+    for (tok, qh), ws in outs.items():
+        if ws[0][0] == "final":
+            assert len(ws) == 1, (tok, qh, ws)
         else:
-            assert len(ss) >= 2 and sorted(ss) == list(range(len(ss))), (tok, qh, ss)
-    # Decode pieces (kinds 0, 1) form one launch before the extend blocks (kind 2).
-    kinds = [int(it[12]) == 2 for it in items]
-    assert kinds == sorted(kinds)
+            slots = sorted(w[1] for w in ws)
+            assert all(w[0] == "part" for w in ws) and len(ws) >= 2 and slots == list(range(len(ws)))
+            assert tok in mtok
+            part_rows += [w[2] for w in ws]
+    assert len(part_rows) == len(set(part_rows)) == p.stats().num_partial_rows
+    s = p.stats()
+    assert s.num_decode_steps == len(p.export(4)) and s.num_decode_workers == len(p.export(5))
+    if case == "decode_tiny_workers":
+        assert s.num_decode_workers > 3  # the 16-segment limit adds workers
 
 
 def test_plan_is_deterministic_and_placement_independent():
@@ -244,9 +306,11 @@ def test_plan_is_deterministic_and_placement_independent():
                       num_pages=b.num_pages, prefix_len=b.prefix_len, agent=b.agent, suffix_len=b.suffix_len,
                       n_rows=b.n_rows)
     p3 = plan_for(b2)
-    # Columns 16.. of an item are its leading page ids: placement-dependent.
-    np.testing.assert_array_equal(p1.export(0)[:, :16], p3.export(0)[:, :16])
-    assert not np.array_equal(p1.export(0)[:, 16:], p3.export(0)[:, 16:])
+    # Segments, workers and merge lists do not depend on placement; the
+    # step table (page ids) does.
+    for which in (3, 5, 6, 7):
+        np.testing.assert_array_equal(p1.export(which), p3.export(which))
+    assert not np.array_equal(p1.export(4), p3.export(4))
     np.testing.assert_array_equal(p1.export(1), p3.export(1))
     assert not np.array_equal(p1.export(2), p3.export(2))
 
@@ -258,10 +322,15 @@ def test_config_plans_build_and_group_prefixes():
         assert s.num_tokens == b.num_tokens
         assert s.pages_needed <= b.num_pages
         if cfg == 2:
-            # 4 agents x 8 KV heads x 4 chunks of 512 keys, one 64-column row block each
-            assert s.num_prefix_items == 4 * 8 * 4
+            # 4 agents x 8 KV heads, one 64-column row block each; 64 requests x 8 KV heads
+            assert s.num_prefix_items == 4 * 8
             assert s.num_suffix_items == 64 * 8
             assert s.num_extend_items == 0
+            steps = 4 * 8 * 2048 // 32 + 8 * sum((int(L) + 31) // 32 for L in b.suffix_len)
+            assert s.num_decode_steps == steps and 480 <= s.num_decode_workers <= 512
+            w = plan_for(b).export(5)
+            cost = w[:, 1] + w[:, 3]  # ring stages: steps + one per segment
+            assert cost[:-1].max() - cost[:-1].min() <= 1
         if cfg == 3:
             assert s.num_prefix_items == 0 and s.num_suffix_items == 0
             assert s.num_extend_items == sum((int(n) + 31) // 32 for n in b.n_rows) * 8

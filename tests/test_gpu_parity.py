@@ -109,11 +109,13 @@ SMALL_CASES = [
     # (seed, Hq, Hkv, d, prefix_len, reqs [(agent, L, n)], opts)
     (1, 8, 2, 64, [40, 17], [(0, 5, 1), (1, 20, 1), (0, 33, 33), (-1, 3, 3), (1, 16, 2)], {}),
     (2, 32, 8, 128, [100, 0, 37], [(0, 70, 1), (2, 1, 1), (1, 40, 40), (0, 65, 1), (2, 17, 4), (-1, 31, 1)],
-     dict(prefix_chunk=32, suffix_chunk=32)),
+     dict(decode_workers=17)),
     (3, 16, 16, 128, [64], [(0, 90, 90), (0, 1, 1), (0, 48, 1)], {}),                 # G = 1
-    (4, 16, 1, 64, [300], [(0, 9, 1), (0, 200, 1), (0, 40, 40), (-1, 5, 1)], dict(prefix_chunk=64)),  # G = 16
-    (5, 64, 8, 128, [129, 500], [(i % 2, 10 + 7 * i, 1) for i in range(20)] + [(1, 77, 2)], dict(suffix_chunk=64)),
+    (4, 16, 1, 64, [300], [(0, 9, 1), (0, 200, 1), (0, 40, 40), (-1, 5, 1)], dict(decode_workers=3)),  # G = 16
+    (5, 64, 8, 128, [129, 500], [(i % 2, 10 + 7 * i, 1) for i in range(20)] + [(1, 77, 2)], dict(decode_workers=100)),
     (6, 32, 8, 128, [16], [(0, 1, 0), (0, 33, 1), (-1, 64, 64)], {}),                 # a request with no rows
+    # two workers asked for; the 16-segment limit of a worker adds more
+    (7, 32, 8, 128, [50], [(0, 1 + i % 20, 1) for i in range(40)] + [(-1, 7, 4)], dict(decode_workers=2)),
 ]
 
 
@@ -126,14 +128,14 @@ def test_small_batches(case):
     run_and_check(b, hv, f"small{seed}", **opts)
 
 
-def test_many_partials_merge_in_kernel():
-    """Long prefix cut into 32-key chunks: 40+ partials per row merged by the
-    last-arriving workgroup."""
+def test_many_partials_merge():
+    """Thousands of workers for a small batch: prefix items cut into pieces of
+    one or two steps, 40+ partial results per row, merged by the merge launch."""
     b = W.make_batch(9, num_q_heads=32, num_kv_heads=8, head_dim=128, num_pages=2048, prefix_len=[1300, 700],
                      agent=[i % 2 for i in range(40)], suffix_len=[100 + 13 * i for i in range(40)],
                      n_rows=[1] * 40)
     hv = W.host_values_fast(b, 10)
-    run_and_check(b, hv, "many-partials", prefix_chunk=32, suffix_chunk=64)
+    run_and_check(b, hv, "many-partials", decode_workers=4096)
 
 
 # --------------------------------------------------------------------------- the five workloads
