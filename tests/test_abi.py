@@ -328,9 +328,13 @@ def test_config_plans_build_and_group_prefixes():
             assert s.num_extend_items == 0
             steps = 4 * 8 * 2048 // 32 + 8 * sum((int(L) + 31) // 32 for L in b.suffix_len)
             assert s.num_decode_steps == steps and 480 <= s.num_decode_workers <= 512
-            w = plan_for(b).export(5)
-            cost = w[:, 1] + w[:, 3]  # ring stages: steps + one per segment
-            assert cost[:-1].max() - cost[:-1].min() <= 1
+            pl = plan_for(b)
+            w, segs = pl.export(5), pl.export(3)
+            # Ring stages weighted as the plan builder does: 1.1 per prefix
+            # step, 1.0 per suffix step and per segment (its Q stage).
+            cost = np.array([10 * n + sum(int(sg[3]) * (11 if sg[0] == 0 else 10) for sg in segs[s0:s0 + n])
+                             for (_, _, s0, n) in w])
+            assert cost[:-1].max() - cost[:-1].min() <= 11
         if cfg == 3:
             assert s.num_prefix_items == 0 and s.num_suffix_items == 0
             assert s.num_extend_items == sum((int(n) + 31) // 32 for n in b.n_rows) * 8
