@@ -334,7 +334,7 @@ def test_config_plans_build_and_group_prefixes():
             # step, 1.0 per suffix step and per segment (its Q stage).
             cost = np.array([10 * n + sum(int(sg[3]) * (11 if sg[0] == 0 else 10) for sg in segs[s0:s0 + n])
                              for (_, _, s0, n) in w])
-            assert cost[:-1].max() - cost[:-1].min() <= 11
+            assert cost[:-1].max() - cost[:-1].min() <= 21  # one step and one Q stage
         if cfg == 3:
             assert s.num_prefix_items == 0 and s.num_suffix_items == 0
             assert s.num_extend_items == sum((int(n) + 31) // 32 for n in b.n_rows) * 8
