@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define PFX_VERSION 20000 /* 2.0.0 */
+#define PFX_VERSION 20100 /* 2.1.0 */
 
 #define PFX_OK 0
 #define PFX_EINVAL (-1)       /* malformed argument (null pointer, bad CSR, overlapping pages, ...) */
@@ -160,11 +160,15 @@ void pfx_alloc_destroy(pfx_alloc* alloc);
 typedef struct pfx_plan pfx_plan;
 
 typedef struct pfx_plan_opts {
-  /* Workgroups the decode steps are divided among (0 = automatic: 512, two
-   * per compute unit of a 256-CU device).  More workers cut decode items into
-   * more pieces; fewer leave compute units idle. */
+  /* Persistent workgroups of the decode launch (0 = automatic: two per
+   * compute unit of the device; never more than there are decode pieces).
+   * The work division does not depend on it, only its timing. */
   int32_t decode_workers;
-  int32_t reserved[7]; /* must be zero */
+  /* Longest decode piece, in 32-key steps (0 = automatic; at most 16).
+   * Shorter pieces balance the workgroups better but give each decode row
+   * more partial results to merge. */
+  int32_t piece_steps;
+  int32_t reserved[6]; /* must be zero */
 } pfx_plan_opts;
 
 typedef struct pfx_plan_stats {
@@ -177,9 +181,8 @@ typedef struct pfx_plan_stats {
   int32_t num_partial_rows;    /* partial result rows (one query head each) kept in the workspace */
   int32_t pages_needed;        /* left-hand side of the Eq. (2) check, in pages */
   int32_t num_decode_steps;    /* 32-key steps of all decode items */
-  int32_t num_decode_workers;  /* decode workgroups */
-  int32_t num_decode_segments; /* pieces of decode items, one per (item, worker) */
-  int32_t reserved;
+  int32_t num_decode_pieces;   /* runs of at most 16 steps of one decode item */
+  int32_t reserved[2];
   int64_t workspace_bytes;
 } pfx_plan_stats;
 
@@ -194,9 +197,9 @@ int pfx_plan_get_stats(const pfx_plan* plan, pfx_plan_stats* out);
 
 /* Copy one of the plan's host arrays out, for inspection and tests:
  * which = 0: extend blocks, 32 int32 each; 1: their row-token list;
- * 2: page list; 3: decode segments, 144 int32 each; 4: decode step table,
- * 2 int32 per step; 5: decode workers, 4 int32 each; 6: tokens whose rows
- * are merged; 7: their (base, count) of partial slots per KV head.
+ * 2: page list; 3: decode pieces, 176 int32 each (header, row tokens,
+ * output rows, page blocks of the steps); 6: tokens whose rows are merged;
+ * 7: their (base, count) of partial slots per KV head.
  * Writes min(cap, size) values and sets *count to the full size. */
 int pfx_plan_export(const pfx_plan* plan, int32_t which, int32_t* out, int64_t cap, int64_t* count);
 

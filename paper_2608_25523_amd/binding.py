@@ -62,19 +62,19 @@ class pfx_batch(C.Structure):
 
 
 class pfx_plan_opts(C.Structure):
-    _fields_ = [("decode_workers", C.c_int32), ("reserved", C.c_int32 * 7)]
+    _fields_ = [("decode_workers", C.c_int32), ("piece_steps", C.c_int32), ("reserved", C.c_int32 * 6)]
 
 
 class pfx_plan_stats(C.Structure):
     _fields_ = [("num_requests", C.c_int32), ("num_tokens", C.c_int32), ("num_items", C.c_int32),
                 ("num_prefix_items", C.c_int32), ("num_suffix_items", C.c_int32),
                 ("num_extend_items", C.c_int32), ("num_partial_rows", C.c_int32),
-                ("pages_needed", C.c_int32), ("num_decode_steps", C.c_int32), ("num_decode_workers", C.c_int32),
-                ("num_decode_segments", C.c_int32), ("reserved", C.c_int32), ("workspace_bytes", C.c_int64)]
+                ("pages_needed", C.c_int32), ("num_decode_steps", C.c_int32), ("num_decode_pieces", C.c_int32),
+                ("reserved", C.c_int32 * 2), ("workspace_bytes", C.c_int64)]
 
 
 # Shapes of the arrays pfx_plan_export returns (int32 columns per record).
-EXPORT_WIDTH = {0: 32, 1: 1, 2: 1, 3: 144, 4: 2, 5: 4, 6: 1, 7: 2}
+EXPORT_WIDTH = {0: 32, 1: 1, 2: 1, 3: 176, 6: 1, 7: 2}
 
 
 def _load(path: str = LIB_PATH):
@@ -235,7 +235,7 @@ class Plan:
 
 def pfx_plan_create(pool: pfx_pool, prefix_page_indptr, prefix_page_ids, prefix_len, agent, suffix_indptr,
                     suffix_page_ids, suffix_len, q_indptr, num_q_heads: int, mode: int,
-                    decode_workers: int = 0) -> Plan:
+                    decode_workers: int = 0, piece_steps: int = 0) -> Plan:
     keep = []
 
     def arr(x):
@@ -247,7 +247,7 @@ def pfx_plan_create(pool: pfx_pool, prefix_page_indptr, prefix_page_ids, prefix_
     pt = pfx_prefix_table(num_agents, arr(prefix_page_indptr), arr(prefix_page_ids), arr(prefix_len))
     num_reqs = len(agent)
     b = pfx_batch(num_reqs, arr(agent), arr(suffix_indptr), arr(suffix_page_ids), arr(suffix_len), arr(q_indptr))
-    opts = pfx_plan_opts(decode_workers)
+    opts = pfx_plan_opts(decode_workers, piece_steps)
     h = C.c_void_p()
     _check(LIB.pfx_plan_create(C.byref(pool), C.byref(pt), C.byref(b), num_q_heads, mode, C.byref(opts),
                                C.byref(h)))

@@ -58,46 +58,45 @@ static_assert(sizeof(Item) == 128, "Item is 32 int32");
 // Decode work.  A decode item is one KV head's whole key range for a set of
 // query rows: an agent's prefix against a block of its decode rows (<= 64
 // columns), or one request's suffix against its own rows.  Items are cut
-// into 32-key steps; the concatenated step list is divided into contiguous,
-// equal runs, one per workgroup ("worker").  The part of an item inside one
-// worker is a segment; an item cut by worker boundaries has several
-// segments ("pieces"), each giving a partial result of its rows.
-constexpr int kSegRows = kDecodeTileCols;  // rows of a segment (columns / G)
-constexpr int kWorkerSegs = 16;            // segments of one worker (held in LDS)
-constexpr int kWorkerSteps = 256;          // steps of one worker (its LDS step table)
-constexpr int kDefaultWorkers = 512;       // two resident workgroups on each of 256 CUs
+// into 32-key steps and then into pieces of at most kPieceSteps steps; each
+// piece leaves its unnormalised state for the merge.  Pieces are stored
+// longest first and dealt to the persistent workgroups in rounds (forward,
+// then backward), so the longest run first and the shortest fill the tail.
+constexpr int kSegRows = kDecodeTileCols;  // rows of a piece (columns / G)
+constexpr int kPieceSteps = 16;            // steps of a piece
+constexpr int kPieceSlots = 4;             // pieces a workgroup holds in LDS
 
 struct alignas(16) SegHead {
   int32_t kind;         // kPrefixItem or kSuffixItem
   int32_t kv_head;
   int32_t ncols;        // query columns: rows * G (<= 64)
-  int32_t nsteps;       // 32-key steps of the segment
+  int32_t nsteps;       // 32-key steps of the piece (<= kPieceSteps)
   int32_t k0;           // key of the first step, within the item
   int32_t kend;         // keys of the item (the last step is masked past it)
   int32_t causal_base;  // suffix items: key k visible to token t iff k <= t + causal_base
   int32_t slot;         // partial slot of the piece in each of its rows; -1: final rows
   int32_t item;         // decode item
-  int32_t piece;        // index of the segment among the item's pieces
+  int32_t piece;        // index of the piece within its item
   int32_t causal;       // 1: some row sees only part of the keys (multi-row suffix)
   int32_t pad[5];
 };
+// One piece as stored in the workspace and, unchanged, in a workgroup's LDS
+// slot.
 struct alignas(16) Seg {
   SegHead h;
-  int32_t tok[kSegRows];  // query token of row j
-  int32_t out[kSegRows];  // row j, query head g of the KV head -> output row out[j] + g:
-                          // o/lse row (final) or o_part/l_part row (partial)
+  int32_t tok[kSegRows];          // query token of row j
+  int32_t out[kSegRows];          // row j, query head g -> output row out[j] + g:
+                                  // o/lse row (final) or o_part/l_part row (partial)
+  int32_t steps[2 * kPieceSteps]; // per step: (page * Hkv + head) of its two 16-key pages
 };
-static_assert(sizeof(Seg) == 576, "Seg is 144 int32");
-
-struct Worker {
-  int32_t step_begin;  // first step (index into the step table)
-  int32_t nsteps;
-  int32_t seg_begin;   // first segment
-  int32_t nseg;
-};
+static_assert(sizeof(Seg) == 704, "Seg is 176 int32");
 
 // Partial results of one (decode token, KV head): nparts slots of G rows at
-// o_part/l_part rows (base + slot) * G + g.  nparts < 2: written directly.
+// o_part/l_part rows (base + slot) * G + g.  A partial row holds a piece's
+// unnormalised state: o_part the D accumulators sum_k p_k v_k in the order
+// the MFMA layout leaves them in (lane group grp, then block blk, then
+// element i: dim 16 blk + 4 grp + i), l_part the pair (m, l) of the
+// running maximum (log2 units, scaled) and the sum of 2^(s - m).
 struct MergeHead {
   int32_t base;
   int32_t nparts;
@@ -109,13 +108,11 @@ struct DevPlan {
   const int32_t* row_tok;
   const int32_t* page_list;
   const int32_t* tok_slot;      // page * 16 + slot of every new token (append)
-  const Seg* segs;
-  const int32_t* steps;         // per decode step: (page * Hkv + head) of its two 16-key pages
-  const Worker* workers;
-  const int32_t* merge_tok;     // decode tokens whose rows merge several pieces
+  const Seg* segs;              // decode pieces, longest first
+  const int32_t* merge_tok;     // decode tokens (their rows are merged from pieces)
   const MergeHead* merge_head;  // [merge token][KV head]
   float* o_part;                // [partial row][d]
-  float* l_part;                // [partial row]
+  float* l_part;                // [partial row][2]
 };
 
 // Per-request bookkeeping (host).
@@ -128,22 +125,21 @@ struct ReqInfo {
 
 struct pfx_plan {
   int32_t num_pages = 0, hkv = 0, d = 0, hq = 0, group = 0, mode = 0;
+  int32_t decode_workers = 0;  // decode workgroups requested (0: two per compute unit)
   int32_t num_reqs = 0, num_tokens = 0;
   std::vector<pfx::Item> items;  // extend blocks
   std::vector<int32_t> row_tok, page_list, tok_req, tok_slot;
   std::vector<pfx::ReqInfo> req;
-  std::vector<pfx::Seg> segs;
-  std::vector<int32_t> steps;
-  std::vector<pfx::Worker> workers;
+  std::vector<pfx::Seg> segs;  // decode pieces
+  int64_t num_decode_steps = 0;
   std::vector<int32_t> merge_tok;
   std::vector<pfx::MergeHead> merge_head;
   int64_t num_part_rows = 0;
   int32_t n_prefix_items = 0, n_suffix_items = 0, n_extend_items = 0;
   int32_t pages_needed = 0;
   // byte offsets inside the workspace
-  size_t off_items = 0, off_row_tok = 0, off_page_list = 0, off_tok_slot = 0, off_segs = 0, off_steps = 0,
-         off_workers = 0, off_merge_tok = 0, off_merge_head = 0, off_opart = 0, off_lpart = 0, total_bytes = 0,
-         blob_bytes = 0;
+  size_t off_items = 0, off_row_tok = 0, off_page_list = 0, off_tok_slot = 0, off_segs = 0,
+         off_merge_tok = 0, off_merge_head = 0, off_opart = 0, off_lpart = 0, total_bytes = 0, blob_bytes = 0;
   std::vector<unsigned char> blob;  // host image of [0, blob_bytes)
   void* dev_ws = nullptr;
   size_t dev_ws_bytes = 0;

@@ -116,7 +116,8 @@ struct AttnArgs {
   float* lse;
   DevPlan plan;
   int32_t hq, hkv, group, group_shift;
-  int32_t num_workers, num_cus;  // decode launch: workers, compute units of the device
+  int32_t num_workers;  // decode launch: persistent workgroups
+  int32_t num_pieces;   // decode pieces in the plan
   float scale_log2;  // sm_scale * log2(e)
 };
 
@@ -167,7 +168,7 @@ __device__ __forceinline__ bf16x8 v_operand(const KVRegs<D>& r, int jj) {
 template <int D, int QB>
 struct WaveState {
   static constexpr int CH = D / 16;
-  f32x4 acc[QB][CH];  // O^T: lane holds dims CH*(4*grp + i) + jj of its column, [jj][i]
+  f32x4 acc[QB][CH];  // O^T: lane holds dims 16 blk + 4 grp + i of its column, [blk][i]
   float m[QB];        // running max (log2 units), same in the 4 lanes of a column
   float l[QB];        // this lane's share of the running sum
 };
@@ -284,6 +285,17 @@ __device__ __forceinline__ void compute_step(WaveState<D, QB>& ws, KVRegs<D>& r,
   compute_steps<D, QB, 1>(ws, one, qf, lim, pos, 1, nblk, grp, scale_log2);
 }
 
+template <int D, int QB>
+__device__ __forceinline__ void reset_state(WaveState<D, QB>& ws) {
+#pragma unroll
+  for (int b = 0; b < QB; ++b) {
+    ws.m[b] = kNegBig;
+    ws.l[b] = 0.f;
+#pragma unroll
+    for (int jj = 0; jj < D / 16; ++jj) ws.acc[b][jj] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+}
+
 // Merge `nparts` partial results for 8 consecutive dims of one row:
 //   lse = ln sum_k exp(lse_k),  O = sum_k exp(lse_k - lse) O_k.
 // o_row points at dims d0..d0+7 of partial 0; partial k is o_stride floats
@@ -337,7 +349,17 @@ struct TileGeom {
   static constexpr int loads_per_wave = page_bytes / 1024;
 };
 
-__device__ __forceinline__ int swizzled_slot(int t, int c, int chunks) { return t * chunks + (c ^ (t & (chunks - 1))); }
+// Chunk c of token row t sits at slot t * chunks + (c ^ row_key(t)): the
+// K operand reads (16 rows at one chunk) and the transposing V reads (four
+// consecutive rows at two adjacent chunks, per 16 lanes) then touch
+// distinct bank groups.
+template <int chunks>
+__device__ __forceinline__ int row_key(int t) {
+  if constexpr (chunks == 16) return ((t & 3) << 2) | ((t >> 2) & 3);
+  else return (((t >> 1) & 3) << 1) | ((t >> 3) & 1);
+}
+template <int chunks>
+__device__ __forceinline__ int swizzled_slot(int t, int c) { return t * chunks + (c ^ row_key<chunks>(t)); }
 
 // Wait until at most n of this wave's vector-memory operations are pending.
 __device__ __forceinline__ void wait_vmcnt(int n) {
@@ -401,6 +423,125 @@ __device__ __forceinline__ uint32_t lds_address(const unsigned char* p) {
   return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_bytes)(p)));
 }
 
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4* lds_s16x4;
+
+// V^T operand of output block blk (dims 16 blk .. 16 blk + 15 as the MFMA
+// rows) for the step's 32 keys in score order (tile 0 keys 4 grp + e, then
+// tile 1 keys 4 grp + e): two ds_read_b64_tr_b16.  Within a 16-lane group
+// that instruction hands output lane i element e of what input lane
+// 4 e + i / 4 addressed, element i % 4; so lane 4 e + q addresses key
+// 4 grp + e, dims 16 blk + 4 q .. + 3, and lane i receives dim 16 blk + i
+// of the four keys.  Elements of keys at or past kend are zeroed (their
+// slots may hold anything, and 0 * NaN is NaN).
+template <int D>
+__device__ __forceinline__ bf16x8 v_operand_tr(const unsigned char* v0, const unsigned char* v1, int blk, int lane,
+                                               uint64_t keep0, uint64_t keep1) {
+  constexpr int chunks = D / 8;
+  const int s = lane & 15;
+  const int row = 4 * (lane >> 4) + (s >> 2);
+  const int q = s & 3;
+  const int off = 16 * swizzled_slot<chunks>(row, 2 * blk + (q >> 1)) + 8 * (q & 1);
+  const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(v0 + off));
+  const s16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(v1 + off));
+  const uint64_t ua = __builtin_bit_cast(uint64_t, a) & keep0;
+  const uint64_t ub = __builtin_bit_cast(uint64_t, b) & keep1;
+  u32x4 w = {uint32_t(ua), uint32_t(ua >> 32), uint32_t(ub), uint32_t(ub >> 32)};
+  return __builtin_bit_cast(bf16x8, w);
+}
+
+// One 32-key step (two 16-key pages staged in LDS: K tile 0, K tile 1,
+// V tile 0, V tile 1) against the wave's QB blocks of 16 query columns
+// (the first nblk of them in use):
+//   S^T = K Q^T: lane (col, grp) gets the scores of keys 16 t + 4 grp + i;
+//   online softmax in log2 units, the running maximum raised lazily;
+//   O^T += V^T P^T with P straight from the lane's own scores.
+// Keys at or past kend, and (causal) keys past a column's limit, are masked.
+template <int D, int QB>
+__device__ __forceinline__ void attend_step(WaveState<D, QB>& ws, const unsigned char* stage,
+                                            const bf16x8 (&qf)[QB][D / 32], const int (&lim)[QB], int k0,
+                                            int kend, bool causal, int nblk, int lane, float scale_log2) {
+  using TG = TileGeom<D>;
+  constexpr int KS = D / 32;
+  constexpr int CH = D / 16;
+  const int col = lane & 15, grp = lane >> 4;
+  const bool tail = k0 + kStepKeys > kend;
+  f32x4 sc[QB][2];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    u32x4 kf[KS];
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+      kf[s] = *reinterpret_cast<const u32x4*>(stage + t * TG::page_bytes +
+                                              16 * swizzled_slot<TG::chunks>(col, 4 * s + grp));
+#pragma unroll
+    for (int b = 0; b < QB; ++b) {
+      if (b >= nblk) break;
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < KS; ++s)
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf[s]), qf[b][s], acc, 0, 0, 0);
+      sc[b][t] = acc;
+    }
+  }
+  bf16x8 pb[QB];
+#pragma unroll
+  for (int b = 0; b < QB; ++b) {
+    if (b >= nblk) break;
+    float v[8] = {sc[b][0][0], sc[b][0][1], sc[b][0][2], sc[b][0][3], sc[b][1][0], sc[b][1][1], sc[b][1][2], sc[b][1][3]};
+    if (tail || causal) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int key = k0 + 16 * t + 4 * grp + i;
+          if (key >= kend || (causal && key > lim[b])) v[4 * t + i] = -INFINITY;
+        }
+    }
+    float mx = fmaxf(fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])), fmaxf(fmaxf(v[4], v[5]), fmaxf(v[6], v[7])));
+    mx = column_max(mx) * scale_log2;  // scale > 0: max of the scaled scores
+    const bool raise = mx > ws.m[b] + kRescaleSlack;
+    if (__any(raise)) {
+      const float mnew = raise ? mx : ws.m[b];
+      const float alpha = fast_exp2(ws.m[b] - mnew);
+      ws.l[b] *= alpha;
+#pragma unroll
+      for (int jj = 0; jj < CH; ++jj) ws.acc[b][jj] *= alpha;
+      ws.m[b] = mnew;
+    }
+    const float neg_m = -ws.m[b];
+    float pr[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      pr[j] = fast_exp2(fmaf(v[j], scale_log2, neg_m));
+      ws.l[b] += pr[j];
+    }
+    u32x4 pw = {pack_bf16(pr[0], pr[1]), pack_bf16(pr[2], pr[3]), pack_bf16(pr[4], pr[5]), pack_bf16(pr[6], pr[7])};
+    pb[b] = __builtin_bit_cast(bf16x8, pw);
+  }
+  uint64_t keep0 = ~uint64_t(0), keep1 = ~uint64_t(0);
+  if (tail) {
+    // Element e of a lane's V quarter is key 16 t + 4 grp + e.
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (k0 + 4 * grp + e >= kend) keep0 &= ~(uint64_t(0xFFFF) << (16 * e));
+      if (k0 + 16 + 4 * grp + e >= kend) keep1 &= ~(uint64_t(0xFFFF) << (16 * e));
+    }
+  }
+  const unsigned char* v0 = stage + 2 * TG::page_bytes;
+  const unsigned char* v1 = stage + 3 * TG::page_bytes;
+#pragma unroll
+  for (int blk = 0; blk < CH; ++blk) {
+    const bf16x8 op = v_operand_tr<D>(v0, v1, blk, lane, keep0, keep1);
+#pragma unroll
+    for (int b = 0; b < QB; ++b) {
+      if (b >= nblk) break;
+      ws.acc[b][blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(op, pb[b], ws.acc[b][blk], 0, 0, 0);
+    }
+  }
+}
+
 // Read a stage into the register layout compute_step expects.
 template <int D>
 __device__ __forceinline__ void read_tile(KVRegs<D>& r, const unsigned char* stage, int col, int grp) {
@@ -411,66 +552,66 @@ __device__ __forceinline__ void read_tile(KVRegs<D>& r, const unsigned char* sta
 #pragma unroll
     for (int s = 0; s < KS; ++s)
       r.k[t][s] = *reinterpret_cast<const u32x4*>(stage + t * TG::page_bytes +
-                                                  16 * swizzled_slot(col, 4 * s + grp, TG::chunks));
+                                                  16 * swizzled_slot<TG::chunks>(col, 4 * s + grp));
 #pragma unroll
   for (int t = 0; t < 2; ++t)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const unsigned char* vb = stage + (2 + t) * TG::page_bytes;
       if constexpr (D == 128) {
-        r.v[t][i] = *reinterpret_cast<const u32x4*>(vb + 16 * swizzled_slot(4 * grp + i, col, TG::chunks));
+        r.v[t][i] = *reinterpret_cast<const u32x4*>(vb + 16 * swizzled_slot<TG::chunks>(4 * grp + i, col));
       } else {
-        r.v[t][i] = *reinterpret_cast<const u32x2*>(vb + 16 * swizzled_slot(4 * grp + i, col >> 1, TG::chunks) +
+        r.v[t][i] = *reinterpret_cast<const u32x2*>(vb + 16 * swizzled_slot<TG::chunks>(4 * grp + i, col >> 1) +
                                                     8 * (col & 1));
       }
     }
 }
 
-// Normalise a wave's block and write it: lane (col, grp) holds dims
-// CH*(4*grp + i) + jj of its column.  Final rows go to o (bf16) and lse;
-// partial rows to the plan's o_part and l_part (fp32).  The column's output
-// row is orow; invalid columns (padding) write nothing.
+// Final rows from the register path's layout: lane (col, grp) holds dims
+// CH (4 grp + i) + jj of its column, eight consecutive dims per i.
 template <int D>
-__device__ __forceinline__ void write_rows(const AttnArgs& a, const f32x4 (&acc)[D / 16], float m, float l_lane,
-                                           int orow, bool valid, bool final_rows, int grp) {
+__device__ __forceinline__ void write_rows_jj(const AttnArgs& a, const f32x4 (&acc)[D / 16], float m, float l_lane,
+                                              int orow, bool valid, int grp) {
   constexpr int CH = D / 16;
   const float l = column_sum(l_lane);
   if (!valid) return;
   const float inv = l > 0.f ? 1.0f / l : 0.f;
-  // A row can see none of a piece's keys (a multi-row decode request whose
-  // later suffix piece starts after its first row): O = 0, LSE = -inf, which
-  // the merge weighs with exp(-inf) = 0.
   const float lse_nat = l > 0.f ? (m + log2f(l)) * kLn2 : -INFINITY;
-  if (final_rows) {
-    uint16_t* out = a.o + size_t(orow) * D + 4 * CH * grp;
+  uint16_t* out = a.o + size_t(orow) * D + 4 * CH * grp;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      if constexpr (CH == 8) {
-        u32x4 w = {pack_bf16(acc[0][i] * inv, acc[1][i] * inv), pack_bf16(acc[2][i] * inv, acc[3][i] * inv),
-                   pack_bf16(acc[4][i] * inv, acc[5][i] * inv), pack_bf16(acc[6][i] * inv, acc[7][i] * inv)};
-        *reinterpret_cast<u32x4*>(out + CH * i) = w;
-      } else {
-        u32x2 w = {pack_bf16(acc[0][i] * inv, acc[1][i] * inv), pack_bf16(acc[2][i] * inv, acc[3][i] * inv)};
-        *reinterpret_cast<u32x2*>(out + CH * i) = w;
-      }
+  for (int i = 0; i < 4; ++i) {
+    if constexpr (CH == 8) {
+      u32x4 w = {pack_bf16(acc[0][i] * inv, acc[1][i] * inv), pack_bf16(acc[2][i] * inv, acc[3][i] * inv),
+                 pack_bf16(acc[4][i] * inv, acc[5][i] * inv), pack_bf16(acc[6][i] * inv, acc[7][i] * inv)};
+      *reinterpret_cast<u32x4*>(out + CH * i) = w;
+    } else {
+      u32x2 w = {pack_bf16(acc[0][i] * inv, acc[1][i] * inv), pack_bf16(acc[2][i] * inv, acc[3][i] * inv)};
+      *reinterpret_cast<u32x2*>(out + CH * i) = w;
     }
-    if (a.lse && grp == 0) a.lse[orow] = lse_nat;
-  } else {
-    float* out = a.plan.o_part + size_t(orow) * D + 4 * CH * grp;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int jj = 0; jj < CH; jj += 4) {
-        f32x4 v = {acc[jj][i] * inv, acc[jj + 1][i] * inv, acc[jj + 2][i] * inv, acc[jj + 3][i] * inv};
-        *reinterpret_cast<f32x4*>(out + CH * i + jj) = v;
-      }
-    if (grp == 0) a.plan.l_part[orow] = lse_nat;
   }
+  if (a.lse && grp == 0) a.lse[orow] = lse_nat;
 }
 
-// ---------------------------------------------------------------------------
-// Extend blocks.
-// ---------------------------------------------------------------------------
+// Normalise a wave's block and write it as final rows (bf16 o, lse): lane
+// (col, grp) holds dims 16 blk + 4 grp + i of its column, four consecutive
+// dims per block.  The column's output row is orow; invalid columns
+// (padding) write nothing.
+template <int D>
+__device__ __forceinline__ void write_rows(const AttnArgs& a, const f32x4 (&acc)[D / 16], float m, float l_lane,
+                                           int orow, bool valid, int grp) {
+  constexpr int CH = D / 16;
+  const float l = column_sum(l_lane);
+  if (!valid) return;
+  const float inv = l > 0.f ? 1.0f / l : 0.f;
+  const float lse_nat = l > 0.f ? (m + log2f(l)) * kLn2 : -INFINITY;
+  uint16_t* out = a.o + size_t(orow) * D + 4 * grp;
+#pragma unroll
+  for (int blk = 0; blk < CH; ++blk) {
+    u32x2 w = {pack_bf16(acc[blk][0] * inv, acc[blk][1] * inv), pack_bf16(acc[blk][2] * inv, acc[blk][3] * inv)};
+    *reinterpret_cast<u32x2*>(out + 16 * blk) = w;
+  }
+  if (a.lse && grp == 0) a.lse[orow] = lse_nat;
+}
 
 // Issue this wave's share of an extend block's step st into a stage buffer:
 // tile (wave & 1) of K (waves 0, 1) or of V (waves 2, 3).
@@ -493,7 +634,7 @@ __device__ __forceinline__ void issue_block_step(unsigned char* stage, const Att
   for (int j = 0; j < TG::loads_per_wave; ++j) {
     const int q = 64 * j + lane;
     const int tt = q / TG::chunks;
-    const int cc = (q % TG::chunks) ^ (tt & (TG::chunks - 1));
+    const int cc = (q % TG::chunks) ^ row_key<TG::chunks>(tt);
     copy16_to_lds(base + tt * D + cc * 8, dst + 1024 * j);
   }
 }
@@ -587,8 +728,7 @@ __device__ __forceinline__ void extend_block(const AttnArgs& a, const Item* itp,
 #pragma unroll
   for (int b = 0; b < QBW; ++b) {
     const int c = (wave * QBW + b) * kTileCols + col;
-    write_rows<D>(a, ws.acc[b], ws.m[b], ws.l[b], orow[b], b < nb && (c >> a.group_shift) < it.row_count, true,
-                  grp);
+    write_rows_jj<D>(a, ws.acc[b], ws.m[b], ws.l[b], orow[b], b < nb && (c >> a.group_shift) < it.row_count, grp);
   }
 }
 
@@ -600,133 +740,66 @@ __global__ __launch_bounds__(256, 2) void extend_kernel(AttnArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Decode workers.
+// Decode.
 //
-// A worker runs its segments in order through one LDS ring.  Every segment
-// contributes a Q stage (the segment's query rows, each wave's 16 columns in
-// its quarter of the stage) followed by its K/V steps, so stage u of the
-// worker is refilled with stage u + kStages - 1 whatever segment that is: an
-// item boundary does not drain the ring.  The wait for stage u is "all but
-// the later stages' copies done" (copies complete in order); a wave counts
-// the copies it issued per stage, since a wave with no columns in a segment
-// copies no Q.
+// Persistent workgroups, each running a fixed list of pieces (round r of the
+// longest-first list gives workgroup b piece r S + b on even rounds and
+// r S + S - 1 - b on odd ones) through one LDS ring: every piece contributes
+// a Q stage (its query rows, each wave's 16 columns in its quarter of the
+// stage) and then its K/V steps, and stage u is refilled with stage
+// u + kStages - 1 whatever piece that belongs to, so a piece boundary does
+// not drain the ring.  A piece's descriptor (header, rows, page blocks)
+// comes into one of kPieceSlots LDS slots by a direct copy that wave 0
+// issues with the Q stage two pieces earlier; it is complete once that stage
+// has been waited for, long before the issue reaches the piece.
 // ---------------------------------------------------------------------------
 template <int D>
 constexpr int decode_smem_bytes() {
-  return kStages * TileGeom<D>::stage_bytes + kWorkerSegs * int(sizeof(Seg)) + kWorkerSteps * 8;
+  return kStages * TileGeom<D>::stage_bytes + kPieceSlots * int(sizeof(Seg));
 }
 
-// Position in a worker's stage sequence: the Q stage of segment seg (k < 0)
-// or its K/V step k, which is the worker's step `step`; with the fields of
-// segment seg the sequence needs (read from LDS once per segment).
-struct Cursor {
-  int seg, k, step;
-  int nst, ncols, qh0;
-};
+// Piece of workgroup b at position n of its list (>= num_pieces: none).
+__device__ __forceinline__ int piece_of(int b, int n, int S) { return n * S + ((n & 1) ? S - 1 - b : b); }
 
-__device__ __forceinline__ int lds_uniform(const int32_t& x) { return __builtin_amdgcn_readfirstlane(x); }
-
-__device__ __forceinline__ void enter(Cursor& c, const Seg* segs, int nseg, int group) {
-  if (c.seg >= nseg) return;
-  const i32x4 h = *reinterpret_cast<const i32x4*>(&segs[c.seg].h);  // kind, kv_head, ncols, nsteps
-  c.qh0 = __builtin_amdgcn_readfirstlane(h[1]) * group;
-  c.ncols = __builtin_amdgcn_readfirstlane(h[2]);
-  c.nst = __builtin_amdgcn_readfirstlane(h[3]);
+// Block ids of this wave's tile (wave & 1) for the steps of a piece, one per
+// lane: a step finds its page with v_readlane.
+__device__ __forceinline__ int piece_window(const Seg& sg, int wave, int lane) {
+  return lane < kPieceSteps ? sg.steps[2 * lane + (wave & 1)] : 0;
 }
 
-__device__ __forceinline__ void advance(Cursor& c, const Seg* segs, int nseg, int group) {
-  if (c.k < 0) {
-    c.k = 0;
-    return;
-  }
-  ++c.step;
-  if (++c.k == c.nst) {
-    ++c.seg;
-    c.k = -1;
-    enter(c, segs, nseg, group);
-  }
-}
-
-// Block ids (page * Hkv + head) of this wave's tile for 64 consecutive
-// steps of the worker, one per lane: a step finds its page with v_readlane.
-struct StepWindow {
-  int blk;
-  int base;
-};
-
-__device__ __forceinline__ void load_window(StepWindow& w, const int32_t* stab, int base, int nsteps, int wave,
-                                            int lane) {
-  w.base = base;
-  w.blk = base + lane < nsteps ? stab[2 * (base + lane) + (wave & 1)] : 0;
-}
-
-// Issue this wave's copies of the stage at cursor c; returns how many
-// (a wave with no columns in a segment copies no Q).
+// Issue this wave's copies of stage k of a piece (k < 0: its Q stage);
+// returns how many copies it issued (a wave with no columns copies no Q).
 template <int D>
-__device__ __forceinline__ int issue_stage(unsigned char* stage, const AttnArgs& a, const Seg* segs,
-                                           const int32_t* stab, StepWindow& win, int nsteps, const Cursor& c,
-                                           int wave, int lane) {
+__device__ __forceinline__ int issue_piece_stage(unsigned char* stage, const AttnArgs& a, const Seg& sg, int win,
+                                                 int k, int ncols, int qh0, int wave, int lane) {
   using TG = TileGeom<D>;
   const uint32_t dst = lds_address(stage) + wave * TG::page_bytes;
-  if (c.k >= 0) {
+  if (k >= 0) {
     // K/V: tile (wave & 1) of K (waves 0, 1) or V (waves 2, 3), swizzled.
-    if (c.step - win.base >= 64) load_window(win, stab, win.base + 64, nsteps, wave, lane);
-    const int blk = __builtin_amdgcn_readlane(win.blk, c.step - win.base);
+    const int blk = __builtin_amdgcn_readlane(win, k);
     const uint16_t* base = ((wave >> 1) ? a.vpool : a.kpool) + size_t(blk) * (16 * D);
 #pragma unroll
     for (int j = 0; j < TG::loads_per_wave; ++j) {
       const int q = 64 * j + lane;
       const int tt = q / TG::chunks;
-      const int cc = (q % TG::chunks) ^ (tt & (TG::chunks - 1));
+      const int cc = (q % TG::chunks) ^ row_key<TG::chunks>(tt);
       copy16_to_lds(base + tt * D + cc * 8, dst + 1024 * j);
     }
     return TG::loads_per_wave;
   }
   // Q: chunk (p % chunks) of this wave's column p / chunks at 16 p; padding
-  // columns repeat the segment's first column.
-  if (16 * wave >= c.ncols) return 0;
-  const Seg& sg = segs[c.seg];
+  // columns repeat the piece's first column.
+  if (16 * wave >= ncols) return 0;
 #pragma unroll
   for (int j = 0; j < TG::loads_per_wave; ++j) {
     const int q = 64 * j + lane;
     int cl = 16 * wave + q / TG::chunks;
-    cl = cl < c.ncols ? cl : 0;
+    cl = cl < ncols ? cl : 0;
     const uint16_t* src =
-        a.q + (size_t(sg.tok[cl >> a.group_shift]) * a.hq + c.qh0 + (cl & (a.group - 1))) * D + 8 * (q % TG::chunks);
+        a.q + (size_t(sg.tok[cl >> a.group_shift]) * a.hq + qh0 + (cl & (a.group - 1))) * D + 8 * (q % TG::chunks);
     copy16_to_lds(src, dst + 1024 * j);
   }
   return TG::loads_per_wave;
-}
-
-// Wait until this wave's copies of all but its `later` most recent copying
-// stages are done (each such stage issued loads_per_wave copies).
-template <int D>
-__device__ __forceinline__ void wait_stages(int later) {
-  constexpr int L = TileGeom<D>::loads_per_wave;
-  static_assert(kStages - 2 <= 3 && 3 * L <= 63, "vmcnt immediates");
-#define PFX_VMCNT(N) __builtin_amdgcn_s_waitcnt(((N) & 15) | (7 << 4) | (15 << 8) | (((N) >> 4) << 14))
-  if (later <= 0)
-    PFX_VMCNT(0);
-  else if (later == 1)
-    PFX_VMCNT(L);
-  else if (later == 2)
-    PFX_VMCNT(2 * L);
-  else
-    PFX_VMCNT(3 * L);
-#undef PFX_VMCNT
-}
-
-// Workgroups are dispatched one per compute unit first (blocks 0 .. C-1),
-// then a second round on the same units (block b + C beside block b).  The
-// two workgroups of a unit are given adjacent workers, whose steps come from
-// the same region of the step list (same kind of item, same compute per
-// stage), so no unit pairs a light worker with a heavy one.  Any bijection
-// is correct; this one only shapes the timing.
-__device__ __forceinline__ int worker_of_block(int b, int nw, int ncu) {
-  if (nw <= ncu || b >= 2 * ncu) return b;
-  const int pairs = nw - ncu < ncu ? nw - ncu : ncu;
-  if (b >= ncu) return 2 * (b - ncu) + 1;
-  return b < pairs ? 2 * b : pairs + b;
 }
 
 template <int D>
@@ -735,161 +808,207 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
   constexpr int KS = D / 32;
   constexpr int CH = D / 16;
   constexpr int NS = kStages;
+  constexpr int K = kPieceSlots;
+  constexpr int kVecs = int(sizeof(Seg)) / 16;
+  static_assert(kVecs <= 64, "a descriptor is one copy instruction");
   __shared__ __attribute__((aligned(1024))) unsigned char smem[decode_smem_bytes<D>()];
   auto ring = reinterpret_cast<unsigned char (*)[TG::stage_bytes]>(smem);
-  Seg* segs = reinterpret_cast<Seg*>(smem + NS * TG::stage_bytes);
-  int32_t* stab = reinterpret_cast<int32_t*>(smem + NS * TG::stage_bytes + kWorkerSegs * sizeof(Seg));
-  const Worker wk = a.plan.workers[worker_of_block(blockIdx.x, a.num_workers, a.num_cus)];
+  Seg* slots = reinterpret_cast<Seg*>(smem + NS * TG::stage_bytes);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
+  const int S = gridDim.x, b = blockIdx.x;
+  const int np = a.num_pieces;
 
-  // The worker's segments (<= kWorkerSegs) and step table (<= kWorkerSteps)
-  // into LDS.
-  {
-    const u32x4* src = reinterpret_cast<const u32x4*>(a.plan.segs + wk.seg_begin);
-    u32x4* dst = reinterpret_cast<u32x4*>(segs);
-    const int nvec = wk.nseg * int(sizeof(Seg) / 16);
-    for (int i = threadIdx.x; i < nvec; i += 256) dst[i] = src[i];
-    const u32x2* ss = reinterpret_cast<const u32x2*>(a.plan.steps) + wk.step_begin;
-    for (int i = threadIdx.x; i < wk.nsteps; i += 256) reinterpret_cast<u32x2*>(stab)[i] = ss[i];
+  // The first two descriptors.
+  for (int i = threadIdx.x; i < 2 * kVecs; i += 256) {
+    const int piece = piece_of(b, i / kVecs, S);
+    if (piece < np)
+      reinterpret_cast<u32x4*>(&slots[i / kVecs])[i % kVecs] =
+          reinterpret_cast<const u32x4*>(&a.plan.segs[piece])[i % kVecs];
   }
   __syncthreads();
 
-  const int nstages = wk.nsteps + wk.nseg;
-  StepWindow win;
-  load_window(win, stab, 0, wk.nsteps, wave, lane);
-  Cursor ic{0, -1, 0, 0, 0, 0};
-  enter(ic, segs, wk.nseg, a.group);
-  Cursor cc = ic;
-  // One bit per recent stage, newest lowest: did this wave copy anything?
-  uint32_t hist = 0;
-  for (int u = 0; u < NS - 1 && u < nstages; ++u) {
-    hist = (hist << 1) | uint32_t(issue_stage<D>(ring[u], a, segs, stab, win, wk.nsteps, ic, wave, lane) > 0);
-    advance(ic, segs, wk.nseg, a.group);
-  }
+  // Issue side: piece iord of the list, its next stage ik (-1: Q), and what
+  // the issue needs of it.
+  int iord = 0, ik = -1, inst = 0, incols = 0, iqh0 = 0, iwin = 0;
+  bool in_piece = false, ended = false;
+  // Per ring stage, what was issued into it: bit 7 valid, bits 5-6 slot,
+  // bits 0-4 step + 1 (0: Q).  ops: copies this wave issued per issue
+  // opportunity, 8 bits each, newest lowest.
+  uint32_t ent = 0, ops = 0;
+  int pending = 0;
+
+  auto issue_next = [&](int r) {
+    uint32_t code = 0;
+    int n_ops = 0;
+    if (!in_piece && !ended) {
+      if (piece_of(b, iord, S) >= np) {
+        ended = true;
+      } else {
+        const Seg& sg = slots[iord % K];
+        const i32x4 h = *reinterpret_cast<const i32x4*>(&sg.h);  // kind, kv_head, ncols, nsteps
+        iqh0 = __builtin_amdgcn_readfirstlane(h[1]) * a.group;
+        incols = __builtin_amdgcn_readfirstlane(h[2]);
+        inst = __builtin_amdgcn_readfirstlane(h[3]);
+        iwin = piece_window(sg, wave, lane);
+        ik = -1;
+        in_piece = true;
+      }
+    }
+    if (in_piece) {
+      const int q = iord % K;
+      n_ops = issue_piece_stage<D>(ring[r], a, slots[q], iwin, ik, incols, iqh0, wave, lane);
+      if (ik < 0 && wave == 0) {
+        // The descriptor two pieces ahead, into the slot of the piece two back.
+        const int nxt = piece_of(b, iord + 2, S);
+        if (nxt < np) {
+          if (lane < kVecs)
+            copy16_to_lds(reinterpret_cast<const unsigned char*>(&a.plan.segs[nxt]) + 16 * lane,
+                          lds_address(reinterpret_cast<const unsigned char*>(&slots[(iord + 2) % K])));
+          ++n_ops;
+        }
+      }
+      code = 0x80u | (uint32_t(q) << 5) | uint32_t(ik + 1);
+      ++pending;
+      if (++ik == inst) {
+        ++iord;
+        in_piece = false;
+      }
+    }
+    ent = (ent & ~(0xFFu << (8 * r))) | (code << (8 * r));
+    ops = (ops << 8) | uint32_t(n_ops);
+  };
+  for (int u = 0; u < NS - 1; ++u) issue_next(u);
 
   WaveState<D, 1> ws;
+  reset_state(ws);
   bf16x8 qf[1][KS];
   int lim[1] = {0};
-  int orow = 0, k0 = 0, kend = 0, causal = 0;
-  bool has_cols = false, valid = false, final_rows = false;
-  for (int u = 0; u < nstages; ++u) {
-    // Wait for stage u: only the copies of the stages issued after it
-    // (u + 1 .. u + ahead, the newest bits of hist) may still be pending.
-    const int ahead = nstages - 1 - u < NS - 2 ? nstages - 1 - u : NS - 2;
-    wait_stages<D>(__builtin_popcount(hist & ((1u << ahead) - 1u)));
+  int orow = 0, k0 = 0, kend = 0, causal = 0, cnst = 0;
+  bool has_cols = false, valid = false;
+  for (int u = 0; !(ended && pending == 0); ++u) {
+    // Stage u: only the copies of the issue opportunities after it (the
+    // newest NS - 2 entries of ops) may still be pending.
+    int later = 0;
+#pragma unroll
+    for (int i = 0; i < NS - 2; ++i) later += (ops >> (8 * i)) & 0xFFu;
+    wait_vmcnt(later);
     __syncthreads();
-    if (u + NS - 1 < nstages) {
-      hist = (hist << 1) |
-             uint32_t(issue_stage<D>(ring[(u + NS - 1) % NS], a, segs, stab, win, wk.nsteps, ic, wave, lane) > 0);
-      advance(ic, segs, wk.nseg, a.group);
-    }
-    const unsigned char* stage = ring[u % NS];
-    if (cc.k < 0) {
-      // A segment starts: its columns, limits, output rows and Q.
-      const Seg& sg = segs[cc.seg];
-      const i32x4 h1 = *reinterpret_cast<const i32x4*>(&sg.h.k0);  // k0, kend, causal_base, slot
-      const i32x4 h2 = *reinterpret_cast<const i32x4*>(&sg.h.item);  // item, piece, causal, -
-      k0 = __builtin_amdgcn_readfirstlane(h1[0]);
-      kend = __builtin_amdgcn_readfirstlane(h1[1]);
-      final_rows = __builtin_amdgcn_readfirstlane(h1[3]) < 0;
-      causal = __builtin_amdgcn_readfirstlane(h2[2]);
-      has_cols = 16 * wave < cc.ncols;
-      const int c = 16 * wave + col;
-      valid = c < cc.ncols;
-      const int j = valid ? c >> a.group_shift : 0;
-      const int tok = sg.tok[j];
-      lim[0] = causal ? tok + __builtin_amdgcn_readfirstlane(h1[2]) : 0x7fffffff;
-      orow = sg.out[j] + (c & (a.group - 1));
-      if (has_cols) {
-        const unsigned char* qb = stage + wave * TG::page_bytes;
+    issue_next((u + NS - 1) % NS);
+
+    const int r = u % NS;
+    const uint32_t code = (ent >> (8 * r)) & 0xFFu;
+    const unsigned char* stage = ring[r];
+    if (code & 0x80u) {
+      --pending;
+      const Seg& sg = slots[(code >> 5) & 3u];
+      const int k = int(code & 31u) - 1;
+      if (k < 0) {
+        // A piece starts: its columns, limits, output rows and Q.
+        const i32x4 h0 = *reinterpret_cast<const i32x4*>(&sg.h);       // kind, kv_head, ncols, nsteps
+        const i32x4 h1 = *reinterpret_cast<const i32x4*>(&sg.h.k0);    // k0, kend, causal_base, slot
+        const i32x4 h2 = *reinterpret_cast<const i32x4*>(&sg.h.item);  // item, piece, causal, -
+        const int ncols = __builtin_amdgcn_readfirstlane(h0[2]);
+        cnst = __builtin_amdgcn_readfirstlane(h0[3]);
+        k0 = __builtin_amdgcn_readfirstlane(h1[0]);
+        kend = __builtin_amdgcn_readfirstlane(h1[1]);
+        causal = __builtin_amdgcn_readfirstlane(h2[2]);
+        has_cols = 16 * wave < ncols;
+        const int c = 16 * wave + col;
+        valid = c < ncols;
+        const int j = valid ? c >> a.group_shift : 0;
+        const int tok = sg.tok[j];
+        lim[0] = causal ? tok + __builtin_amdgcn_readfirstlane(h1[2]) : 0x7fffffff;
+        orow = sg.out[j] + (c & (a.group - 1));
+        if (has_cols) {
+          const unsigned char* qb = stage + wave * TG::page_bytes;
 #pragma unroll
-        for (int s = 0; s < KS; ++s)
-          qf[0][s] = *reinterpret_cast<const bf16x8*>(qb + 16 * (col * TG::chunks + 4 * s + grp));
+          for (int s = 0; s < KS; ++s)
+            qf[0][s] = *reinterpret_cast<const bf16x8*>(qb + 16 * (col * TG::chunks + 4 * s + grp));
+        }
+      } else if (has_cols) {
+        attend_step<D, 1>(ws, stage, qf, lim, k0 + kStepKeys * k, kend, causal != 0, 1, lane, a.scale_log2);
+        if (k == cnst - 1) {
+          // The piece's state goes out as it stands: accumulators in their
+          // register order (group, block, element), (m, l) once per column.
+          const float l = column_sum(ws.l[0]);
+          if (valid) {
+            float* out = a.plan.o_part + size_t(orow) * D + grp * (4 * CH);
+#pragma unroll
+            for (int jj = 0; jj < CH; ++jj) *reinterpret_cast<f32x4*>(out + 4 * jj) = ws.acc[0][jj];
+            if (grp == 0) *reinterpret_cast<f32x2*>(a.plan.l_part + 2 * size_t(orow)) = f32x2{ws.m[0], l};
+          }
+          reset_state(ws);
+        }
       }
-      ws.m[0] = kNegBig;
-      ws.l[0] = 0.f;
-#pragma unroll
-      for (int jj = 0; jj < CH; ++jj) ws.acc[0][jj] = f32x4{0.f, 0.f, 0.f, 0.f};
-    } else if (has_cols) {
-      KVRegs<D> kv;
-      read_tile<D>(kv, stage, col, grp);
-      const StepPos p{0, k0 + kStepKeys * cc.k, kend, causal};
-      compute_step<D, 1>(ws, kv, qf, lim, p, 1, grp, a.scale_log2);
-      if (cc.k == cc.nst - 1) write_rows<D>(a, ws.acc[0], ws.m[0], ws.l[0], orow, valid, final_rows, grp);
     }
-    advance(cc, segs, wk.nseg, a.group);
   }
 }
 
-// The rows of decode requests seen by several pieces: log-sum-exp merge of
-// their partial results.  One thread per (token, query head, 8 dims); the
-// first kMergeBatch partials of the row are all requested before any is
-// used, so a row pays one memory latency rather than one per partial.
+// Decode rows: the log-sum-exp merge of the pieces' states (Sec. 4.2,
+// Eq. (8)).  One thread per (token, query head, group grp, block pair): it
+// reads elements i = 0..3 of blocks blk, blk + 1 of every piece, i.e. dims
+// 16 blk + 4 grp + i and 16 (blk + 1) + 4 grp + i, and writes them as two
+// runs of four bf16.  The first kMergeBatch pieces are all requested before
+// any is used.
 constexpr int kMergeBatch = 8;
 
 template <int D>
 __global__ __launch_bounds__(256) void merge_rows_kernel(AttnArgs a, int n_tok) {
-  constexpr int SL = D / 8;
+  constexpr int CH = D / 16;
+  constexpr int SL = D / 8;  // threads per row: 4 groups x CH/2 pairs
   const size_t t = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
   if (t >= size_t(n_tok) * a.hq * SL) return;
   const int sl = int(t % SL);
+  const int grp = sl / (CH / 2), blk = 2 * (sl % (CH / 2));
   const int qh = int((t / SL) % a.hq);
   const int m = int(t / (size_t(SL) * a.hq));
   const MergeHead mh = a.plan.merge_head[size_t(m) * a.hkv + (qh >> a.group_shift)];
-  if (mh.nparts < 2) return;  // written directly by its only piece
   const int tok = a.plan.merge_tok[m];
   const size_t row0 = size_t(mh.base) * a.group + (qh & (a.group - 1));
-  const size_t lstride = size_t(a.group);
-  const float* lp = a.plan.l_part + row0;
-  const float* op = a.plan.o_part + row0 * D + sl * 8;
-  const size_t ostride = lstride * D;
-  float lv[kMergeBatch];
+  const size_t stride = size_t(a.group);  // rows between slots
+  const float* op = a.plan.o_part + row0 * D + grp * (4 * CH) + 4 * blk;
+  const f32x2* lp = reinterpret_cast<const f32x2*>(a.plan.l_part) + row0;
+  f32x2 ml[kMergeBatch];
   f32x4 ov[kMergeBatch][2];
 #pragma unroll
   for (int k = 0; k < kMergeBatch; ++k) {
     if (k < mh.nparts) {
-      lv[k] = lp[k * lstride];
-      ov[k][0] = *reinterpret_cast<const f32x4*>(op + k * ostride);
-      ov[k][1] = *reinterpret_cast<const f32x4*>(op + k * ostride + 4);
+      ml[k] = lp[k * stride];
+      ov[k][0] = *reinterpret_cast<const f32x4*>(op + k * stride * D);
+      ov[k][1] = *reinterpret_cast<const f32x4*>(op + k * stride * D + 4);
     } else {
-      lv[k] = -INFINITY;
+      ml[k] = f32x2{kNegBig, 0.f};
       ov[k][0] = ov[k][1] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
   }
-  float mx = -INFINITY;
+  float mx = kNegBig;
 #pragma unroll
-  for (int k = 0; k < kMergeBatch; ++k) mx = fmaxf(mx, lv[k]);
-  for (int k = kMergeBatch; k < mh.nparts; ++k) mx = fmaxf(mx, lp[k * lstride]);
+  for (int k = 0; k < kMergeBatch; ++k) mx = fmaxf(mx, ml[k][0]);
+  for (int k = kMergeBatch; k < mh.nparts; ++k) mx = fmaxf(mx, lp[k * stride][0]);
   float z = 0.f;
-  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int k = 0; k < kMergeBatch; ++k) {
-    const float w = fast_exp2((lv[k] - mx) * kLog2e);  // 0 for unused slots
-    z += w;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      acc[e] += w * ov[k][0][e];
-      acc[4 + e] += w * ov[k][1][e];
-    }
+    const float w = fast_exp2(ml[k][0] - mx);  // 0 for unused slots and for pieces that saw no key
+    z += w * ml[k][1];
+    acc0 += w * ov[k][0];
+    acc1 += w * ov[k][1];
   }
   for (int k = kMergeBatch; k < mh.nparts; ++k) {
-    const float w = fast_exp2((lp[k * lstride] - mx) * kLog2e);
-    z += w;
-    const f32x4 x = *reinterpret_cast<const f32x4*>(op + k * ostride);
-    const f32x4 y = *reinterpret_cast<const f32x4*>(op + k * ostride + 4);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      acc[e] += w * x[e];
-      acc[4 + e] += w * y[e];
-    }
+    const f32x2 x = lp[k * stride];
+    const float w = fast_exp2(x[0] - mx);
+    z += w * x[1];
+    acc0 += w * *reinterpret_cast<const f32x4*>(op + k * stride * D);
+    acc1 += w * *reinterpret_cast<const f32x4*>(op + k * stride * D + 4);
   }
   const float inv = 1.0f / z;
-  u32x4 w = {pack_bf16(acc[0] * inv, acc[1] * inv), pack_bf16(acc[2] * inv, acc[3] * inv),
-             pack_bf16(acc[4] * inv, acc[5] * inv), pack_bf16(acc[6] * inv, acc[7] * inv)};
-  *reinterpret_cast<u32x4*>(a.o + (size_t(tok) * a.hq + qh) * D + sl * 8) = w;
-  if (a.lse && sl == 0) a.lse[size_t(tok) * a.hq + qh] = mx + logf(z);
+  uint16_t* out = a.o + (size_t(tok) * a.hq + qh) * D + 16 * blk + 4 * grp;
+  *reinterpret_cast<u32x2*>(out) = u32x2{pack_bf16(acc0[0] * inv, acc0[1] * inv), pack_bf16(acc0[2] * inv, acc0[3] * inv)};
+  *reinterpret_cast<u32x2*>(out + 16) =
+      u32x2{pack_bf16(acc1[0] * inv, acc1[1] * inv), pack_bf16(acc1[2] * inv, acc1[3] * inv)};
+  if (a.lse && sl == 0) a.lse[size_t(tok) * a.hq + qh] = (mx + log2f(z)) * kLn2;
 }
 
 template <int D>
@@ -961,7 +1080,10 @@ static int check_pool_matches(const pfx_pool* pool, const pfx_plan* p, const cha
 template <int D>
 static void launch_all(AttnArgs a, const pfx_plan* p, hipStream_t s) {
   if (!p->items.empty()) hipLaunchKernelGGL((extend_kernel<D>), dim3(p->items.size()), dim3(256), 0, s, a);
-  if (!p->workers.empty()) hipLaunchKernelGGL((decode_kernel<D>), dim3(p->workers.size()), dim3(256), 0, s, a);
+  if (!p->segs.empty()) {
+    const int S = std::min<int>(a.num_workers, static_cast<int>(p->segs.size()));
+    hipLaunchKernelGGL((decode_kernel<D>), dim3(S), dim3(256), 0, s, a);
+  }
   const int n_tok = static_cast<int>(p->merge_tok.size());
   if (n_tok) {
     const size_t threads = size_t(n_tok) * p->hq * (D / 8);
@@ -1013,7 +1135,7 @@ extern "C" int pfx_attention(const pfx_pool* pool, const pfx_plan* p, const void
                              float sm_scale, void* stream) {
   int rc = check_pool_matches(pool, p, "pfx_attention");
   if (rc) return rc;
-  if (p->items.empty() && p->workers.empty()) return PFX_OK;
+  if (p->items.empty() && p->segs.empty()) return PFX_OK;
   if (!q || !o) return fail(PFX_EINVAL, "pfx_attention: q or o is NULL");
   if (!(sm_scale > 0.f)) sm_scale = 1.0f / sqrtf(float(p->d));
   AttnArgs a;
@@ -1028,15 +1150,15 @@ extern "C" int pfx_attention(const pfx_pool* pool, const pfx_plan* p, const void
   a.group = p->group;
   a.group_shift = __builtin_ctz(static_cast<unsigned>(p->group));
   a.scale_log2 = sm_scale * kLog2e;
-  a.num_workers = static_cast<int32_t>(p->workers.size());
-  a.num_cus = 0;
-  {
+  a.num_pieces = static_cast<int32_t>(p->segs.size());
+  a.num_workers = p->decode_workers;
+  if (a.num_workers <= 0) {
     int dev = 0, ncu = 0;
-    if (hipGetDevice(&dev) == hipSuccess &&
-        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess)
-      a.num_cus = ncu;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || ncu <= 0)
+      return fail(PFX_EHIP, "pfx_attention: cannot read the compute-unit count");
+    a.num_workers = 2 * ncu;
   }
-  if (a.num_cus <= 0) a.num_cus = a.num_workers;  // identity mapping
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (p->d == 128) launch_all<128>(a, p, s); else launch_all<64>(a, p, s);
   return check_launch("pfx_attention");

@@ -29,6 +29,9 @@ static size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 static int64_t pages_for(int64_t tokens) { return (tokens + PFX_PAGE_SIZE - 1) / PFX_PAGE_SIZE; }
 
+// Longest decode piece by default, in steps.
+constexpr int32_t kDefaultPieceSteps = 16;
+
 DevPlan dev_plan(const pfx_plan* p) {
   unsigned char* base = static_cast<unsigned char*>(p->dev_ws);
   DevPlan d;
@@ -37,8 +40,6 @@ DevPlan dev_plan(const pfx_plan* p) {
   d.page_list = reinterpret_cast<const int32_t*>(base + p->off_page_list);
   d.tok_slot = reinterpret_cast<const int32_t*>(base + p->off_tok_slot);
   d.segs = reinterpret_cast<const Seg*>(base + p->off_segs);
-  d.steps = reinterpret_cast<const int32_t*>(base + p->off_steps);
-  d.workers = reinterpret_cast<const Worker*>(base + p->off_workers);
   d.merge_tok = reinterpret_cast<const int32_t*>(base + p->off_merge_tok);
   d.merge_head = reinterpret_cast<const MergeHead*>(base + p->off_merge_head);
   d.o_part = reinterpret_cast<float*>(base + p->off_opart);
@@ -160,13 +161,16 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
     return fail(PFX_EUNSUPPORTED, "pfx_plan_create: query group %d (1, 2, 4, 8 or 16 supported)", G);
   if (mode != PFX_MODE_EXTEND && mode != PFX_MODE_DECODE && mode != PFX_MODE_MIXED)
     return fail(PFX_EINVAL, "pfx_plan_create: mode %d", mode);
-  int32_t workers_hint = kDefaultWorkers;
+  int32_t p_workers = 0, piece_steps = kDefaultPieceSteps;
   if (opts) {
-    for (int i = 0; i < 7; ++i)
+    for (int i = 0; i < 6; ++i)
       if (opts->reserved[i]) return fail(PFX_EINVAL, "pfx_plan_create: opts.reserved[%d] != 0", i);
     if (opts->decode_workers < 0 || opts->decode_workers > (1 << 20))
       return fail(PFX_EINVAL, "pfx_plan_create: decode_workers %d outside [0, %d]", opts->decode_workers, 1 << 20);
-    if (opts->decode_workers) workers_hint = opts->decode_workers;
+    if (opts->piece_steps < 0 || opts->piece_steps > kPieceSteps)
+      return fail(PFX_EINVAL, "pfx_plan_create: piece_steps %d outside [0, %d]", opts->piece_steps, kPieceSteps);
+    p_workers = opts->decode_workers;
+    if (opts->piece_steps) piece_steps = opts->piece_steps;
   }
   if (int64_t(pool->num_pages) * hkv > INT32_MAX)
     return fail(PFX_EUNSUPPORTED, "pfx_plan_create: num_pages * num_kv_heads must stay below 2^31");
@@ -265,6 +269,7 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   p->hq = hq;
   p->group = G;
   p->mode = mode;
+  p->decode_workers = p_workers;
   p->num_reqs = R;
   p->num_tokens = static_cast<int32_t>(total_tokens);
   p->pages_needed = static_cast<int32_t>(need);
@@ -349,93 +354,44 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
     }
   }
 
-  // ---- decode steps: 32 keys = two 16-key pages of one KV head ----
-  int64_t T = 0;
-  for (DItem& x : dit) {
-    x.step_first = T;
-    T += (x.keys + kStepKeys - 1) / kStepKeys;
-  }
-  if (T > INT32_MAX / 2) return delete p, fail(PFX_ERANGE, "pfx_plan_create: too many decode steps");
-  p->steps.resize(size_t(2 * T));
-  for (const DItem& x : dit) {
-    const int32_t npages = static_cast<int32_t>(pages_for(x.keys));
-    const int32_t ns = (x.keys + kStepKeys - 1) / kStepKeys;
-    for (int32_t i = 0; i < ns; ++i) {
-      const int32_t pg0 = 2 * i, pg1 = 2 * i + 1 < npages ? 2 * i + 1 : 2 * i;  // a missing page repeats (masked)
-      p->steps[size_t(2 * (x.step_first + i))] = p->page_list[x.page_off + pg0] * hkv + x.h;
-      p->steps[size_t(2 * (x.step_first + i)) + 1] = p->page_list[x.page_off + pg1] * hkv + x.h;
-    }
-  }
-
-  // ---- workers: contiguous runs of the step list, each costing at most B
-  // ring stages (one per step, plus one per segment for its query rows) and
-  // holding at most kWorkerSegs segments and kWorkerSteps steps.  Runs are
-  // filled greedily, so each is full but the last; B is the smallest budget
-  // that needs no more than the requested number of workers. ----
-  // Stage costs in tenths: a prefix step multiplies 64 query columns, a
-  // suffix step at most 16, so a prefix step keeps its workgroup a little
-  // longer; a Q stage moves little data.
-  constexpr int64_t kPrefixStepCost = 11, kSuffixStepCost = 10, kQStageCost = 10;
+  // ---- decode pieces: each item's 32-key steps (two 16-key pages of one
+  // KV head) cut into runs of at most kPieceSteps, as even as possible ----
+  auto page_blk = [&](const DItem& x, int32_t pg) { return p->page_list[x.page_off + pg] * hkv + x.h; };
   std::vector<int32_t> npieces(dit.size(), 0);
-  if (T > 0) {
-    const int64_t W = std::max<int64_t>(std::min<int64_t>(workers_hint, T), (T + kWorkerSteps - 1) / kWorkerSteps);
-    auto item_end = [&](size_t x) { return dit[x].step_first + (dit[x].keys + kStepKeys - 1) / kStepKeys; };
-    auto fill = [&](int64_t B, bool build) {
-      int64_t g = 0, count = 0;
-      size_t x = 0;
-      if (build) {
-        p->workers.clear();
-        p->segs.clear();
-        std::fill(npieces.begin(), npieces.end(), 0);
+  for (size_t xi = 0; xi < dit.size(); ++xi) {
+    const DItem& x = dit[xi];
+    const int32_t ns = (x.keys + kStepKeys - 1) / kStepKeys;
+    const int32_t npages = static_cast<int32_t>(pages_for(x.keys));
+    const int32_t np = (ns + piece_steps - 1) / piece_steps;
+    p->num_decode_steps += ns;
+    for (int32_t k = 0; k < np; ++k) {
+      const int32_t s0 = int32_t(int64_t(k) * ns / np), s1 = int32_t(int64_t(k + 1) * ns / np);
+      Seg sg{};
+      sg.h.kind = x.kind;
+      sg.h.kv_head = x.h;
+      sg.h.ncols = x.rows * G;
+      sg.h.nsteps = s1 - s0;
+      sg.h.k0 = s0 * kStepKeys;
+      sg.h.kend = x.keys;
+      sg.h.causal_base = x.causal_base;
+      sg.h.causal = x.kind == kSuffixItem && x.rows > 1;
+      sg.h.item = static_cast<int32_t>(xi);
+      sg.h.piece = k;
+      for (int32_t i = s0; i < s1; ++i) {
+        const int32_t pg0 = 2 * i, pg1 = 2 * i + 1 < npages ? 2 * i + 1 : 2 * i;  // a missing page repeats (masked)
+        sg.steps[2 * (i - s0)] = page_blk(x, pg0);
+        sg.steps[2 * (i - s0) + 1] = page_blk(x, pg1);
       }
-      while (g < T) {
-        Worker wk{static_cast<int32_t>(g), 0, static_cast<int32_t>(p->segs.size()), 0};
-        int64_t cost = 0;
-        while (g < T && wk.nseg < kWorkerSegs && wk.nsteps < kWorkerSteps) {
-          while (item_end(x) <= g) ++x;
-          const int64_t step_cost = dit[x].kind == kPrefixItem ? kPrefixStepCost : kSuffixStepCost;
-          const int64_t room = (B - cost - kQStageCost) / step_cost;  // steps that still fit
-          if (wk.nseg > 0 && room < 1) break;
-          const int64_t take =
-              std::min({item_end(x) - g, std::max<int64_t>(room, 1), int64_t(kWorkerSteps - wk.nsteps)});
-          if (build) {
-            const DItem& it = dit[x];
-            Seg sg{};
-            sg.h.kind = it.kind;
-            sg.h.kv_head = it.h;
-            sg.h.ncols = it.rows * G;
-            sg.h.nsteps = static_cast<int32_t>(take);
-            sg.h.k0 = static_cast<int32_t>(g - it.step_first) * kStepKeys;
-            sg.h.kend = it.keys;
-            sg.h.causal_base = it.causal_base;
-            sg.h.causal = it.kind == kSuffixItem && it.rows > 1;
-            sg.h.item = static_cast<int32_t>(x);
-            sg.h.piece = npieces[x]++;
-            p->segs.push_back(sg);
-          }
-          ++wk.nseg;
-          wk.nsteps += static_cast<int32_t>(take);
-          g += take;
-          cost += kQStageCost + take * step_cost;
-        }
-        if (build) p->workers.push_back(wk);
-        ++count;
-      }
-      return count;
-    };
-    int64_t lo = 1, hi = (kWorkerSteps + kWorkerSegs) * 20;  // hi: the caps alone bound a run
-    while (lo < hi) {
-      const int64_t mid = (lo + hi) / 2;
-      if (fill(mid, false) <= W) hi = mid; else lo = mid + 1;
+      p->segs.push_back(sg);
     }
-    fill(lo, true);
+    npieces[xi] = np;
   }
   for (size_t x = 0; x < dit.size(); ++x) dit[x].npieces = npieces[x];
 
   // ---- partial slots: a decode row of KV head h is seen by the pieces of
-  // its prefix item (slots 0 ..) and then of its suffix item; with one piece
-  // in all the row is written directly, otherwise the merge (Sec. 4.2,
-  // Eq. (8)) combines the slots ----
+  // its prefix item (slots 0 ..) and then of its suffix item; every piece
+  // leaves its unnormalised state in a slot and the merge (Sec. 4.2,
+  // Eq. (8)) combines them into the row (a lone piece is just normalised) ----
   std::vector<int32_t> tok_base(size_t(total_tokens) * hkv, -1), np_prefix(size_t(R) * hkv, 0),
       np_total(size_t(R) * hkv, 0);
   int64_t part_units = 0;
@@ -446,7 +402,7 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
       const size_t rh = size_t(r) * hkv + h;
       np_prefix[rh] = pf_item[rh] >= 0 ? dit[pf_item[rh]].npieces : 0;
       np_total[rh] = np_prefix[rh] + dit[sf_item[rh]].npieces;
-      any |= np_total[rh] >= 2;
+      any |= np_total[rh] >= 1;
     }
     if (!any) continue;
     for (int32_t t = 0; t < p->req[r].n; ++t) {
@@ -454,7 +410,7 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
       p->merge_tok.push_back(tok);
       for (int32_t h = 0; h < hkv; ++h) {
         const int32_t np = np_total[size_t(r) * hkv + h];
-        if (np >= 2) {
+        if (np >= 1) {
           tok_base[size_t(tok) * hkv + h] = static_cast<int32_t>(part_units);
           p->merge_head.push_back(MergeHead{static_cast<int32_t>(part_units), np});
           part_units += np;
@@ -474,16 +430,18 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
       const int32_t r = p->tok_req[tok];
       const size_t rh = size_t(r) * hkv + it.h;
       sg.tok[j] = tok;
-      if (np_total[rh] >= 2) {
-        const int32_t slot = (it.kind == kPrefixItem ? 0 : np_prefix[rh]) + sg.h.piece;
-        sg.h.slot = slot;  // the same for every row of the piece
-        sg.out[j] = (tok_base[size_t(tok) * hkv + it.h] + slot) * G;
-      } else {
-        sg.h.slot = -1;
-        sg.out[j] = tok * hq + it.h * G;
-      }
+      const int32_t slot = (it.kind == kPrefixItem ? 0 : np_prefix[rh]) + sg.h.piece;
+      sg.h.slot = slot;  // the same for every row of the piece
+      sg.out[j] = (tok_base[size_t(tok) * hkv + it.h] + slot) * G;
     }
   }
+
+  // Longest first: a prefix step multiplies 64 query columns, a suffix step
+  // at most 16, so prefix steps weigh a little more; every piece also has a
+  // stage for its query rows.
+  auto piece_cost = [](const Seg& sg) { return (sg.h.kind == kPrefixItem ? 11 : 10) * sg.h.nsteps + 10; };
+  std::stable_sort(p->segs.begin(), p->segs.end(),
+                   [&](const Seg& x, const Seg& y) { return piece_cost(x) > piece_cost(y); });
 
   // ---- extend blocks (Sec. 3): up to 128 query columns of one request,
   // over the whole prefix (no mask) then the suffix (causal), written
@@ -542,13 +500,11 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   p->off_page_list = off;  off = align256(off + p->page_list.size() * 4);
   p->off_tok_slot = off;   off = align256(off + p->tok_slot.size() * 4);
   p->off_segs = off;       off = align256(off + p->segs.size() * sizeof(Seg));
-  p->off_steps = off;      off = align256(off + p->steps.size() * 4);
-  p->off_workers = off;    off = align256(off + p->workers.size() * sizeof(Worker));
   p->off_merge_tok = off;  off = align256(off + p->merge_tok.size() * 4);
   p->off_merge_head = off; off = align256(off + p->merge_head.size() * sizeof(MergeHead));
   p->blob_bytes = off;
   p->off_opart = off;      off = align256(off + size_t(p->num_part_rows) * p->d * 4);
-  p->off_lpart = off;      off = align256(off + size_t(p->num_part_rows) * 4);
+  p->off_lpart = off;      off = align256(off + size_t(p->num_part_rows) * 8);
   p->total_bytes = std::max<size_t>(off, 256);
 
   p->blob.assign(p->blob_bytes, 0);
@@ -560,8 +516,6 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   put(p->off_page_list, p->page_list.data(), p->page_list.size() * 4);
   put(p->off_tok_slot, p->tok_slot.data(), p->tok_slot.size() * 4);
   put(p->off_segs, p->segs.data(), p->segs.size() * sizeof(Seg));
-  put(p->off_steps, p->steps.data(), p->steps.size() * 4);
-  put(p->off_workers, p->workers.data(), p->workers.size() * sizeof(Worker));
   put(p->off_merge_tok, p->merge_tok.data(), p->merge_tok.size() * 4);
   put(p->off_merge_head, p->merge_head.data(), p->merge_head.size() * sizeof(MergeHead));
 
@@ -585,10 +539,9 @@ extern "C" int pfx_plan_get_stats(const pfx_plan* p, pfx_plan_stats* s) {
   s->num_extend_items = p->n_extend_items;
   s->num_partial_rows = static_cast<int32_t>(p->num_part_rows);
   s->pages_needed = p->pages_needed;
-  s->num_decode_steps = static_cast<int32_t>(p->steps.size() / 2);
-  s->num_decode_workers = static_cast<int32_t>(p->workers.size());
-  s->num_decode_segments = static_cast<int32_t>(p->segs.size());
-  s->reserved = 0;
+  s->num_decode_steps = static_cast<int32_t>(p->num_decode_steps);
+  s->num_decode_pieces = static_cast<int32_t>(p->segs.size());
+  s->reserved[0] = s->reserved[1] = 0;
   s->workspace_bytes = static_cast<int64_t>(p->total_bytes);
   return PFX_OK;
 }
@@ -601,9 +554,7 @@ extern "C" int pfx_plan_export(const pfx_plan* p, int32_t which, int32_t* out, i
     case 0: src = reinterpret_cast<const int32_t*>(p->items.data()); n = int64_t(p->items.size()) * 32; break;
     case 1: src = p->row_tok.data(); n = int64_t(p->row_tok.size()); break;
     case 2: src = p->page_list.data(); n = int64_t(p->page_list.size()); break;
-    case 3: src = reinterpret_cast<const int32_t*>(p->segs.data()); n = int64_t(p->segs.size()) * 144; break;
-    case 4: src = p->steps.data(); n = int64_t(p->steps.size()); break;
-    case 5: src = reinterpret_cast<const int32_t*>(p->workers.data()); n = int64_t(p->workers.size()) * 4; break;
+    case 3: src = reinterpret_cast<const int32_t*>(p->segs.data()); n = int64_t(p->segs.size()) * 176; break;
     case 6: src = p->merge_tok.data(); n = int64_t(p->merge_tok.size()); break;
     case 7: src = reinterpret_cast<const int32_t*>(p->merge_head.data()); n = int64_t(p->merge_head.size()) * 2; break;
     default: return fail(PFX_EINVAL, "pfx_plan_export: which = %d", which);

@@ -35,7 +35,7 @@ def test_library_exports_every_declared_function():
 
 
 def test_version_and_error_text():
-    assert B.pfx_version() == 20000
+    assert B.pfx_version() == 20100
     with pytest.raises(B.PfxError):
         B.Allocator(-1)
     assert "num_pages" in B.pfx_last_error()
@@ -194,60 +194,60 @@ def enumerate_coverage(plan, batch):
                         hit(tok, qh, plen + k)
                 outs.setdefault((tok, qh), []).append(("final", tok * hq + qh))
 
-    # Decode: workers split the step list into contiguous runs of segments.
-    segs, steps, workers = plan.export(3), plan.export(4), plan.export(5)
+    # Decode: items cut into pieces of at most 16 steps, longest first.
+    segs = plan.export(3)
     mtok, mhead = plan.export(6), plan.export(7).reshape(-1, hkv, 2)
     midx = {int(t): i for i, t in enumerate(mtok)}
-    g_next, s_next = 0, 0
     pieces = {}
-    for (sb, ns, segb, nseg) in workers:
-        assert sb == g_next and segb == s_next and 1 <= nseg <= 16 and 1 <= ns <= 256
-        at = sb
-        for sg in segs[segb:segb + nseg]:
-            kind, h, ncols, nst, k0, kend, cbase, slot, item, piece = (int(x) for x in sg[:10])
-            assert kind in (0, 1) and 1 <= ncols <= 64 and ncols % G == 0 and k0 % 32 == 0
-            lst = pieces.setdefault(item, [])
-            assert piece == len(lst)  # pieces appear in order
-            lst.append((piece, k0, nst, kend))
-            for j in range(ncols // G):
-                tok = int(sg[16 + j])
-                r, a, plen, pos = req_info(tok)
-                src = batch.prefix_pages[a] if kind == 0 else batch.suffix_pages[r]
-                for i in range(nst):
-                    kk = k0 + 32 * i
-                    assert kk < kend
-                    blk0, blk1 = (int(x) for x in steps[at + i])
-                    assert blk0 == int(src[kk // 16]) * hkv + h
-                    assert blk1 == (int(src[kk // 16 + 1]) if kk + 16 < kend else int(src[kk // 16])) * hkv + h
-                    for g in range(G):
-                        for k in range(kk, min(kk + 32, kend)):
-                            if kind == 0:
-                                hit(tok, h * G + g, k)
-                            elif k <= tok + cbase:
-                                assert tok + cbase == pos
-                                hit(tok, h * G + g, plen + k)
+    costs = []
+    for sg in segs:
+        kind, h, ncols, nst, k0, kend, cbase, slot, item, piece, causal = (int(x) for x in sg[:11])
+        assert kind in (0, 1) and 1 <= ncols <= 64 and ncols % G == 0 and k0 % 32 == 0 and 1 <= nst <= 16
+        costs.append((11 if kind == 0 else 10) * nst + 10)
+        pieces.setdefault(item, []).append((piece, k0, nst, kend))
+        tok0 = int(sg[16])
+        r0 = int(tok_req[tok0])
+        assert causal == (kind == 1 and int(batch.n_rows[r0]) > 1)
+        for j in range(ncols // G):
+            tok = int(sg[16 + j])
+            r, a, plen, pos = req_info(tok)
+            src = batch.prefix_pages[a] if kind == 0 else batch.suffix_pages[r]
+            for i in range(nst):
+                kk = k0 + 32 * i
+                assert kk < kend
+                blk0, blk1 = int(sg[144 + 2 * i]), int(sg[145 + 2 * i])
+                assert blk0 == int(src[kk // 16]) * hkv + h
+                assert blk1 == (int(src[kk // 16 + 1]) if kk + 16 < kend else int(src[kk // 16])) * hkv + h
                 for g in range(G):
-                    row = int(sg[80 + j]) + g
-                    if slot < 0:
-                        assert row == tok * hq + h * G + g
-                        outs.setdefault((tok, h * G + g), []).append(("final", row))
-                    else:
-                        base, np_ = mhead[midx[tok], h]
-                        assert 0 <= slot < np_ and row == (base + slot) * G + g
-                        outs.setdefault((tok, h * G + g), []).append(("part", slot, row))
-            at += nst
-        assert at == sb + ns
-        g_next, s_next = sb + ns, segb + nseg
-    assert g_next == len(steps) and s_next == len(segs)
-    # Each item's pieces tile its key range in order.
+                    for k in range(kk, min(kk + 32, kend)):
+                        if kind == 0:
+                            hit(tok, h * G + g, k)
+                        elif k <= tok + cbase:
+                            assert tok + cbase == pos
+                            hit(tok, h * G + g, plen + k)
+            for g in range(G):
+                row = int(sg[80 + j]) + g
+                if slot < 0:
+                    assert row == tok * hq + h * G + g
+                    outs.setdefault((tok, h * G + g), []).append(("final", row))
+                else:
+                    base, np_ = mhead[midx[tok], h]
+                    assert 0 <= slot < np_ and row == (base + slot) * G + g
+                    outs.setdefault((tok, h * G + g), []).append(("part", slot, row))
+    assert costs == sorted(costs, reverse=True)  # longest first
+    # Each item's pieces tile its key range in order, as evenly as possible.
     for item, ps in pieces.items():
+        ps.sort()
+        assert [q[0] for q in ps] == list(range(len(ps)))
         ends = [(k0, k0 + 32 * n) for (_, k0, n, _) in ps]
         assert ends[0][0] == 0 and all(ends[i][1] == ends[i + 1][0] for i in range(len(ends) - 1))
         assert ends[-1][1] >= ps[0][3] > ends[-1][1] - 32
+        sizes = [n for (_, _, n, _) in ps]
+        assert max(sizes) - min(sizes) <= 1
     return counts, outs
 
 
-@pytest.mark.parametrize("case", ["small", "split", "g1", "g16", "decode_only", "decode_tiny_workers"])
+@pytest.mark.parametrize("case", ["small", "split", "g1", "g16", "decode_only"])
 def test_plan_covers_every_visible_key_once(case):
     if case == "small":
         b, kw = small_batch(), {}
@@ -261,7 +261,7 @@ def test_plan_covers_every_visible_key_once(case):
         agents = np.arange(70) % 3 - 1
         b = W.make_batch(5, num_q_heads=8, num_kv_heads=2, head_dim=128, num_pages=512, prefix_len=[64, 300],
                          agent=agents, suffix_len=(np.arange(70) % 40) + 1, n_rows=np.ones(70, np.int32))
-        kw = dict(decode_workers=64 if case == "decode_only" else 3)
+        kw = dict(decode_workers=64)
     p = plan_for(b, **kw)
     counts, outs = enumerate_coverage(p, b)
     q_indptr = b.q_indptr()
@@ -278,8 +278,9 @@ def test_plan_covers_every_visible_key_once(case):
                     assert counts.get((tok, qh, k), 0) == 1, (tok, qh, k)
                 expected += vis
     assert sum(counts.values()) == expected            # nothing invisible is attended
-    # A row is written either once, final, or as partial slots 0 .. k-1
-    # (k >= 2), each once, merged afterwards; no two rows share a partial row.
+    # A row is written either once, final (extend), or as partial slots
+    # 0 .. k-1 (decode, k >= 1), each once, merged afterwards; no two rows
+    # share a partial row.
     part_rows = []
     mtok = set(int(t) for t in p.export(6))
     for (tok, qh), ws in outs.items():
@@ -287,14 +288,13 @@ def test_plan_covers_every_visible_key_once(case):
             assert len(ws) == 1, (tok, qh, ws)
         else:
             slots = sorted(w[1] for w in ws)
-            assert all(w[0] == "part" for w in ws) and len(ws) >= 2 and slots == list(range(len(ws)))
+            assert all(w[0] == "part" for w in ws) and slots == list(range(len(ws)))
             assert tok in mtok
             part_rows += [w[2] for w in ws]
     assert len(part_rows) == len(set(part_rows)) == p.stats().num_partial_rows
     s = p.stats()
-    assert s.num_decode_steps == len(p.export(4)) and s.num_decode_workers == len(p.export(5))
-    if case == "decode_tiny_workers":
-        assert s.num_decode_workers > 3  # the 16-segment limit adds workers
+    segs = p.export(3)
+    assert s.num_decode_pieces == len(segs) and s.num_decode_steps == int(segs[:, 3].sum())
 
 
 def test_plan_is_deterministic_and_placement_independent():
@@ -306,11 +306,12 @@ def test_plan_is_deterministic_and_placement_independent():
                       num_pages=b.num_pages, prefix_len=b.prefix_len, agent=b.agent, suffix_len=b.suffix_len,
                       n_rows=b.n_rows)
     p3 = plan_for(b2)
-    # Segments, workers and merge lists do not depend on placement; the
-    # step table (page ids) does.
-    for which in (3, 5, 6, 7):
+    # Pieces and merge lists do not depend on placement, apart from the
+    # page blocks of the steps.
+    np.testing.assert_array_equal(p1.export(3)[:, :144], p3.export(3)[:, :144])
+    for which in (6, 7):
         np.testing.assert_array_equal(p1.export(which), p3.export(which))
-    assert not np.array_equal(p1.export(4), p3.export(4))
+    assert not np.array_equal(p1.export(3)[:, 144:], p3.export(3)[:, 144:])
     np.testing.assert_array_equal(p1.export(1), p3.export(1))
     assert not np.array_equal(p1.export(2), p3.export(2))
 
@@ -327,14 +328,9 @@ def test_config_plans_build_and_group_prefixes():
             assert s.num_suffix_items == 64 * 8
             assert s.num_extend_items == 0
             steps = 4 * 8 * 2048 // 32 + 8 * sum((int(L) + 31) // 32 for L in b.suffix_len)
-            assert s.num_decode_steps == steps and 480 <= s.num_decode_workers <= 512
-            pl = plan_for(b)
-            w, segs = pl.export(5), pl.export(3)
-            # Ring stages weighted as the plan builder does: 1.1 per prefix
-            # step, 1.0 per suffix step and per segment (its Q stage).
-            cost = np.array([10 * n + sum(int(sg[3]) * (11 if sg[0] == 0 else 10) for sg in segs[s0:s0 + n])
-                             for (_, _, s0, n) in w])
-            assert cost[:-1].max() - cost[:-1].min() <= 21  # one step and one Q stage
+            assert s.num_decode_steps == steps
+            # prefix items: 64 steps in 4 pieces; suffix items: one piece each (<= 16 steps)
+            assert s.num_decode_pieces == 4 * 8 * 4 + 64 * 8
         if cfg == 3:
             assert s.num_prefix_items == 0 and s.num_suffix_items == 0
             assert s.num_extend_items == sum((int(n) + 31) // 32 for n in b.n_rows) * 8

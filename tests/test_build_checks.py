@@ -21,10 +21,10 @@ def isa(tmp_path_factory):
     if not os.path.exists(HIPCC):
         pytest.skip("hipcc not available")
     out = tmp_path_factory.mktemp("isa") / "k.s"
-    subprocess.run([HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "-S", "--cuda-device-only",
-                    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-                    "-I", os.path.join(ROOT, "include"), SRC, "-o", str(out)],
-                   check=True, capture_output=True)
+    from paper_2608_25523_amd.build import FLAGS
+    flags = [f for f in FLAGS if f not in ("-shared", "-fPIC")]
+    subprocess.run([HIPCC, *flags, "-S", "--cuda-device-only", "-I", os.path.join(ROOT, "include"), SRC,
+                    "-o", str(out)], check=True, capture_output=True)
     return out.read_text()
 
 
@@ -46,3 +46,4 @@ def test_no_scratch_in_attention_kernels(isa):
     for kernel in kernels:
         body = isa.split(kernel + ":", 1)[1].split("s_endpgm", 1)[0]
         assert "scratch_" not in body, kernel
+
