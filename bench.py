@@ -2,8 +2,9 @@
 (TFLOP/s) at the Llama-3-8B attention-layer shape, on one MI355X.
 
 A step is one pass of the hot path over one batch: the KV append of the
-step's new tokens, then attention for every query row (grouped prefix
-phase, suffix phase and the in-kernel log-sum-exp merge).  Inputs are
+step's new tokens, then attention for every query row (the decode launch:
+agent prefixes shared by their decode rows and each request's own suffix,
+cut into pieces; then the log-sum-exp merge of the pieces).  Inputs are
 resident in HBM before timing starts.
 
 Primary line (``value``): decode-8B -- Hq 32 / Hkv 8 / d 128, 4 agent
@@ -239,9 +240,10 @@ def main():
         "data": "synthetic (seeded N(0,1) bf16; lengths per the workload recipe)",
         "config": {"workload": "decode-8B: Hq32/Hkv8/d128, 4 prefixes x 2048, 64 decode reqs (16/agent, "
                                "suffix U[64,512]), 65536-page pool, random placement",
-                   "unique_kv_bytes": u, "replicas": dec["replicas"], "items": st.num_items,
-                   "prefix_items": st.num_prefix_items, "suffix_items": st.num_suffix_items},
-        "roofline": {"bound": "hbm", "kernel": "attn_kernel (pfx_attention)",
+                   "unique_kv_bytes": u, "replicas": dec["replicas"], "prefix_items": st.num_prefix_items,
+                   "suffix_items": st.num_suffix_items, "decode_steps": st.num_decode_steps,
+                   "decode_pieces": st.num_decode_pieces},
+        "roofline": {"bound": "hbm", "kernel": "pfx_attention: decode_kernel + merge_rows_kernel",
                      "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic_from_profile("decode"),
                      "attn_us": round(dec["attn_ms"] * 1e3, 3)},
@@ -253,7 +255,7 @@ def main():
             "workload": "extend-8B: Hq32/Hkv8/d128, 3 prefixes x 4096, 32 reqs suffix U[256,2048]",
             "value": round(ext["flops"] / (ext["ms"] * 1e-3) / 1e12, 2), "unit": "TFLOP/s",
             "ms_per_step": round(ext["ms"], 4), "steps": ext["steps"],
-            "roofline": {"bound": "mfma", "kernel": "attn_kernel (pfx_attention)", "achieved": round(tf, 2),
+            "roofline": {"bound": "mfma", "kernel": "pfx_attention: extend_kernel", "achieved": round(tf, 2),
                          "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(tf / BF16_PEAK_TFLOPS, 4),
                          "traffic": traffic_from_profile("extend"), "flops": ext["flops"]},
         }

@@ -146,8 +146,9 @@ void pfx_alloc_destroy(pfx_alloc* alloc);
  *
  * pfx_plan_create validates the pool shape, the prefix table and the batch
  * (all host arrays; copied, so they may be freed afterwards), groups the
- * requests by agent, splits every prefix into key chunks whose KV is read
- * once for all of the agent's decode rows, and builds the work items.  It
+ * decode requests by agent (each prefix read once for all of an agent's
+ * decode rows and a KV head), cuts the decode items into pieces of at most
+ * piece_steps 32-key steps, and builds the extend blocks.  It
  * checks the budget of Sec. 3, Eq. (2) in pages:
  *     sum over distinct agents referenced of ceil(l_a / 16)
  *   + sum over requests of ceil(L_r / 16)   <=  num_pages,
@@ -189,7 +190,7 @@ typedef struct pfx_plan_stats {
 int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* prefixes, const pfx_batch* batch,
                     int32_t num_q_heads, int32_t mode, const pfx_plan_opts* opts, pfx_plan** out);
 
-/* Bytes of device workspace the plan needs (work list, counters, partials). */
+/* Bytes of device workspace the plan needs (work lists, partial states). */
 int pfx_plan_workspace_bytes(const pfx_plan* plan, size_t* bytes);
 
 /* Counts describing the plan (host only). */
@@ -234,16 +235,18 @@ int pfx_append_kv(const pfx_pool* pool, const pfx_plan* plan, const void* k_new,
  *     O = sum_j softmax_j(sm_scale * q . k_j) v_j,
  * accumulated in fp32 from bf16 inputs.  sm_scale <= 0 selects
  * 1/sqrt(head_dim).  Prefix KV is read once per agent group and KV head;
- * partial results over key ranges are combined with the log-sum-exp merge
- * (see pfx_merge_states).  Results are deterministic: the same plan shape
- * and inputs give bit-identical outputs, wherever the pages sit.
+ * the states of a decode row's pieces are combined with the log-sum-exp
+ * merge (as pfx_merge_states), in a second launch on the same stream.
+ * Results are deterministic: the same plan shape and inputs give
+ * bit-identical outputs, wherever the pages sit.  Calls that share a plan
+ * workspace must not overlap.
  * --------------------------------------------------------------------- */
 int pfx_attention(const pfx_pool* pool, const pfx_plan* plan, const void* q, void* o, float* lse,
                   float sm_scale, void* hip_stream);
 
 /* ---------------------------------------------------------------------
  * Log-sum-exp merge of attention results computed over disjoint key ranges
- * (exposed for testing; pfx_attention runs the same device code):
+ * (the same arithmetic pfx_attention applies to its decode pieces):
  *     lse = ln sum_k exp(lse_k),   O = sum_k exp(lse_k - lse) O_k.
  * o_parts: device fp32 [num_parts][rows][head_dim] (each O_k normalised
  * over its own keys); lse_parts: device fp32 [num_parts][rows];
