@@ -59,6 +59,10 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Placed inside a rarely taken branch (masking, rescaling): the compiler may
+// not turn the branch into always-executed selects.
+#define PFX_KEEP_BRANCH() asm volatile("" ::: "memory")
+
 // Max / sum over the four lanes l, l ^ 16, l ^ 32, l ^ 48 (the lanes holding
 // one query column), with the gfx950 row-swap instructions instead of LDS
 // permutes.  v_permlane16_swap a, b exchanges the odd 16-lane rows of a with
@@ -169,8 +173,10 @@ template <int D, int QB>
 struct WaveState {
   static constexpr int CH = D / 16;
   f32x4 acc[QB][CH];  // O^T: lane holds dims 16 blk + 4 grp + i of its column, [blk][i]
+                      // (extend's register path: dims CH (4 grp + i) + jj, [jj][i])
   float m[QB];        // running max (log2 units), same in the 4 lanes of a column
-  float l[QB];        // this lane's share of the running sum
+  float l[QB];        // this lane's share of the running sum (decode)
+  f32x4 lv[QB];       // extend: the running sum from the MFMA, element 0 of group 0
 };
 
 // NSUB consecutive 32-key steps against the wave's query blocks, with one
@@ -185,15 +191,22 @@ __device__ __forceinline__ void compute_steps(WaveState<D, QB>& ws, KVRegs<D>* c
                                               float scale_log2) {
   constexpr int KS = D / 32;
   constexpr int CH = D / 16;
+  const uint32_t one2 = (threadIdx.x & 15) == 0 ? 0x3F803F80u : 0u;  // bf16 1.0 pairs in row 0
+  const bf16x8 ones_row0 = __builtin_bit_cast(bf16x8, u32x4{one2, one2, one2, one2});
+  // The causal limit only bites on steps that reach past the smallest limit
+  // of the wave's columns (block 0, column 0 holds the lowest token; padding
+  // columns repeat it): elsewhere every key is visible to every column.
+  const int lim_lo = __builtin_amdgcn_readfirstlane(lim[0]);
   bool any_mask = false;
 #pragma unroll
   for (int u = 0; u < NSUB; ++u) {
     if (u >= nvalid) break;
     const bool tail = p[u].k0 + kStepKeys > p[u].kend;
-    any_mask |= tail || p[u].seg == 1;
+    any_mask |= tail || (p[u].seg == 1 && p[u].k0 + kStepKeys - 1 > lim_lo);
     if (tail) {
       // Keys past the end of the segment: zero their V (the slots may hold
       // anything) -- their probabilities are forced to 0 below.
+      PFX_KEEP_BRANCH();
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -222,6 +235,7 @@ __device__ __forceinline__ void compute_steps(WaveState<D, QB>& ws, KVRegs<D>* c
       }
     }
     if (any_mask) {
+      PFX_KEEP_BRANCH();
 #pragma unroll
       for (int u = 0; u < NSUB; ++u) {
         if (u >= nvalid) break;
@@ -246,9 +260,10 @@ __device__ __forceinline__ void compute_steps(WaveState<D, QB>& ws, KVRegs<D>* c
     mx *= scale_log2;  // scale > 0: max of the scaled scores
     const bool raise = mx > ws.m[b] + kRescaleSlack;
     if (__any(raise)) {
+      PFX_KEEP_BRANCH();
       const float mnew = raise ? mx : ws.m[b];
       const float alpha = fast_exp2(ws.m[b] - mnew);
-      ws.l[b] *= alpha;
+      ws.lv[b][0] *= alpha;  // rows other than 0 stay zero
 #pragma unroll
       for (int jj = 0; jj < CH; ++jj) ws.acc[b][jj] *= alpha;
       ws.m[b] = mnew;
@@ -259,10 +274,7 @@ __device__ __forceinline__ void compute_steps(WaveState<D, QB>& ws, KVRegs<D>* c
       if (u >= nvalid) break;
       float pr[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        pr[j] = fast_exp2(fmaf(sc[u][j], scale_log2, neg_m));
-        ws.l[b] += pr[j];
-      }
+      for (int j = 0; j < 8; ++j) pr[j] = fast_exp2(fmaf(sc[u][j], scale_log2, neg_m));
       u32x4 pw;
       pw[0] = pack_bf16(pr[0], pr[1]);
       pw[1] = pack_bf16(pr[2], pr[3]);
@@ -272,6 +284,9 @@ __device__ __forceinline__ void compute_steps(WaveState<D, QB>& ws, KVRegs<D>* c
 #pragma unroll
       for (int jj = 0; jj < CH; ++jj)
         ws.acc[b][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v_operand<D>(*rp[u], jj), pb, ws.acc[b][jj], 0, 0, 0);
+      // Row sums of P on the matrix unit: an A operand whose row 0 is ones
+      // (lane col 0 of each group) puts sum_k P[col][k] in row 0.
+      ws.lv[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones_row0, pb, ws.lv[b], 0, 0, 0);
     }
   }
 }
@@ -291,6 +306,7 @@ __device__ __forceinline__ void reset_state(WaveState<D, QB>& ws) {
   for (int b = 0; b < QB; ++b) {
     ws.m[b] = kNegBig;
     ws.l[b] = 0.f;
+    ws.lv[b] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int jj = 0; jj < D / 16; ++jj) ws.acc[b][jj] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
@@ -491,6 +507,7 @@ __device__ __forceinline__ void attend_step(WaveState<D, QB>& ws, const unsigned
     if (b >= nblk) break;
     float v[8] = {sc[b][0][0], sc[b][0][1], sc[b][0][2], sc[b][0][3], sc[b][1][0], sc[b][1][1], sc[b][1][2], sc[b][1][3]};
     if (tail || causal) {
+      PFX_KEEP_BRANCH();
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -503,6 +520,7 @@ __device__ __forceinline__ void attend_step(WaveState<D, QB>& ws, const unsigned
     mx = column_max(mx) * scale_log2;  // scale > 0: max of the scaled scores
     const bool raise = mx > ws.m[b] + kRescaleSlack;
     if (__any(raise)) {
+      PFX_KEEP_BRANCH();
       const float mnew = raise ? mx : ws.m[b];
       const float alpha = fast_exp2(ws.m[b] - mnew);
       ws.l[b] *= alpha;
@@ -523,6 +541,7 @@ __device__ __forceinline__ void attend_step(WaveState<D, QB>& ws, const unsigned
   uint64_t keep0 = ~uint64_t(0), keep1 = ~uint64_t(0);
   if (tail) {
     // Element e of a lane's V quarter is key 16 t + 4 grp + e.
+    PFX_KEEP_BRANCH();
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       if (k0 + 4 * grp + e >= kend) keep0 &= ~(uint64_t(0xFFFF) << (16 * e));
@@ -652,7 +671,6 @@ template <int D, int QBW>
 __device__ __forceinline__ void extend_block(const AttnArgs& a, const Item* itp, unsigned char* smem) {
   using TG = TileGeom<D>;
   constexpr int KS = D / 32;
-  constexpr int CH = D / 16;
   constexpr int NS = kStages;
   auto ring = reinterpret_cast<unsigned char (*)[TG::stage_bytes]>(smem);
   int* ptab = reinterpret_cast<int*>(smem + NS * TG::stage_bytes);
@@ -698,13 +716,7 @@ __device__ __forceinline__ void extend_block(const AttnArgs& a, const Item* itp,
     }
   }
   WaveState<D, QBW> ws;
-#pragma unroll
-  for (int b = 0; b < QBW; ++b) {
-    ws.m[b] = kNegBig;
-    ws.l[b] = 0.f;
-#pragma unroll
-    for (int jj = 0; jj < CH; ++jj) ws.acc[b][jj] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
+  reset_state(ws);
   const int s0_steps = (it.s0_kend - it.s0_kbeg + kStepKeys - 1) / kStepKeys;
   const int s1_steps = (it.s1_kend - it.s1_kbeg + kStepKeys - 1) / kStepKeys;
   const int nsteps = s0_steps + s1_steps;
@@ -713,22 +725,30 @@ __device__ __forceinline__ void extend_block(const AttnArgs& a, const Item* itp,
   for (int st = 0; st < NS - 1 && st < nsteps; ++st)
     issue_block_step<D>(ring[st], a, it, ptab, lead, p0n, st, s0_steps, h, wave, lane);
   __syncthreads();  // page table ready
-  for (int st = 0; st < nsteps; ++st) {
-    const int ahead = nsteps - 1 - st < NS - 2 ? nsteps - 1 - st : NS - 2;
-    wait_vmcnt(ahead * TG::loads_per_wave);
-    __syncthreads();
-    const int nxt = st + NS - 1;
-    if (nxt < nsteps) issue_block_step<D>(ring[nxt % NS], a, it, ptab, lead, p0n, nxt, s0_steps, h, wave, lane);
-    if (nb > 0) {
-      KVRegs<D> kv;
-      read_tile<D>(kv, ring[st % NS], col, grp);
-      compute_step<D, QBW>(ws, kv, qf, lim, step_pos(it, st, s0_steps), nb, grp, a.scale_log2);
+  // Unrolled by the ring depth: each copy of the body works on a fixed
+  // stage, so its LDS addresses are a lane offset plus an immediate.
+  for (int st0 = 0; st0 < nsteps; st0 += NS) {
+#pragma unroll
+    for (int r = 0; r < NS; ++r) {
+      const int st = st0 + r;
+      if (st >= nsteps) break;
+      const int ahead = nsteps - 1 - st < NS - 2 ? nsteps - 1 - st : NS - 2;
+      wait_vmcnt(ahead * TG::loads_per_wave);
+      __syncthreads();
+      const int nxt = st + NS - 1;
+      if (nxt < nsteps)
+        issue_block_step<D>(ring[(r + NS - 1) % NS], a, it, ptab, lead, p0n, nxt, s0_steps, h, wave, lane);
+      if (nb > 0) {
+        KVRegs<D> kv;
+        read_tile<D>(kv, ring[r], col, grp);
+        compute_step<D, QBW>(ws, kv, qf, lim, step_pos(it, st, s0_steps), nb, grp, a.scale_log2);
+      }
     }
   }
 #pragma unroll
   for (int b = 0; b < QBW; ++b) {
     const int c = (wave * QBW + b) * kTileCols + col;
-    write_rows_jj<D>(a, ws.acc[b], ws.m[b], ws.l[b], orow[b], b < nb && (c >> a.group_shift) < it.row_count, grp);
+    write_rows_jj<D>(a, ws.acc[b], ws.m[b], ws.lv[b][0], orow[b], b < nb && (c >> a.group_shift) < it.row_count, grp);
   }
 }
 
