@@ -256,11 +256,13 @@ __device__ __forceinline__ void compute_steps(WaveState<D, QB>& ws, KVRegs<D>* c
       mx = fmaxf(mx, fmaxf(fmaxf(fmaxf(sc[u][0], sc[u][1]), fmaxf(sc[u][2], sc[u][3])),
                            fmaxf(fmaxf(sc[u][4], sc[u][5]), fmaxf(sc[u][6], sc[u][7]))));
     }
-    mx = column_max(mx);
-    mx *= scale_log2;  // scale > 0: max of the scaled scores
-    const bool raise = mx > ws.m[b] + kRescaleSlack;
-    if (__any(raise)) {
+    // A column's running max only moves when its scaled max passes m + slack,
+    // which needs some lane of the column past it: the cross-lane reduction
+    // is paid only when a lane of the wave is (scale > 0).
+    if (__any(mx * scale_log2 > ws.m[b] + kRescaleSlack)) {
       PFX_KEEP_BRANCH();
+      mx = column_max(mx) * scale_log2;
+      const bool raise = mx > ws.m[b] + kRescaleSlack;
       const float mnew = raise ? mx : ws.m[b];
       const float alpha = fast_exp2(ws.m[b] - mnew);
       ws.lv[b][0] *= alpha;  // rows other than 0 stay zero
