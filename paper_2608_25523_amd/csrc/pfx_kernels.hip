@@ -175,8 +175,7 @@ struct WaveState {
   f32x4 acc[QB][CH];  // O^T: lane holds dims 16 blk + 4 grp + i of its column, [blk][i]
                       // (extend's register path: dims CH (4 grp + i) + jj, [jj][i])
   float m[QB];        // running max (log2 units), same in the 4 lanes of a column
-  float l[QB];        // this lane's share of the running sum (decode)
-  f32x4 lv[QB];       // extend: the running sum from the MFMA, element 0 of group 0
+  f32x4 lv[QB];       // running sum from the matrix unit: element 0 in the group-0 lanes, 0 elsewhere
 };
 
 // NSUB consecutive 32-key steps against the wave's query blocks, with one
@@ -307,7 +306,6 @@ __device__ __forceinline__ void reset_state(WaveState<D, QB>& ws) {
 #pragma unroll
   for (int b = 0; b < QB; ++b) {
     ws.m[b] = kNegBig;
-    ws.l[b] = 0.f;
     ws.lv[b] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int jj = 0; jj < D / 16; ++jj) ws.acc[b][jj] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -519,13 +517,14 @@ __device__ __forceinline__ void attend_step(WaveState<D, QB>& ws, const unsigned
         }
     }
     float mx = fmaxf(fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])), fmaxf(fmaxf(v[4], v[5]), fmaxf(v[6], v[7])));
-    mx = column_max(mx) * scale_log2;  // scale > 0: max of the scaled scores
-    const bool raise = mx > ws.m[b] + kRescaleSlack;
-    if (__any(raise)) {
+    // The cross-lane max is needed only when some lane passes m + slack.
+    if (__any(mx * scale_log2 > ws.m[b] + kRescaleSlack)) {
       PFX_KEEP_BRANCH();
+      mx = column_max(mx) * scale_log2;  // scale > 0: max of the scaled scores
+      const bool raise = mx > ws.m[b] + kRescaleSlack;
       const float mnew = raise ? mx : ws.m[b];
       const float alpha = fast_exp2(ws.m[b] - mnew);
-      ws.l[b] *= alpha;
+      ws.lv[b][0] *= alpha;  // rows other than 0 stay zero
 #pragma unroll
       for (int jj = 0; jj < CH; ++jj) ws.acc[b][jj] *= alpha;
       ws.m[b] = mnew;
@@ -533,10 +532,7 @@ __device__ __forceinline__ void attend_step(WaveState<D, QB>& ws, const unsigned
     const float neg_m = -ws.m[b];
     float pr[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      pr[j] = fast_exp2(fmaf(v[j], scale_log2, neg_m));
-      ws.l[b] += pr[j];
-    }
+    for (int j = 0; j < 8; ++j) pr[j] = fast_exp2(fmaf(v[j], scale_log2, neg_m));
     u32x4 pw = {pack_bf16(pr[0], pr[1]), pack_bf16(pr[2], pr[3]), pack_bf16(pr[4], pr[5]), pack_bf16(pr[6], pr[7])};
     pb[b] = __builtin_bit_cast(bf16x8, pw);
   }
@@ -560,6 +556,14 @@ __device__ __forceinline__ void attend_step(WaveState<D, QB>& ws, const unsigned
       if (b >= nblk) break;
       ws.acc[b][blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(op, pb[b], ws.acc[b][blk], 0, 0, 0);
     }
+  }
+  // Row sums of P on the matrix unit (row 0 of the A operand is ones).
+  const uint32_t one2 = col == 0 ? 0x3F803F80u : 0u;
+  const bf16x8 ones_row0 = __builtin_bit_cast(bf16x8, u32x4{one2, one2, one2, one2});
+#pragma unroll
+  for (int b = 0; b < QB; ++b) {
+    if (b >= nblk) break;
+    ws.lv[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones_row0, pb[b], ws.lv[b], 0, 0, 0);
   }
 }
 
@@ -954,7 +958,7 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
         if (k == cnst - 1) {
           // The piece's state goes out as it stands: accumulators in their
           // register order (group, block, element), (m, l) once per column.
-          const float l = column_sum(ws.l[0]);
+          const float l = ws.lv[0][0];  // the whole column sum in the group-0 lanes
           if (valid) {
             float* out = a.plan.o_part + size_t(orow) * D + grp * (4 * CH);
 #pragma unroll
