@@ -365,13 +365,22 @@ struct TileGeom {
   static constexpr int loads_per_wave = page_bytes / 1024;
 };
 
-// Chunk c of token row t sits at slot t * chunks + (c ^ row_key(t)): the
-// K operand reads (16 rows at one chunk) and the transposing V reads (four
-// consecutive rows at two adjacent chunks, per 16 lanes) then touch
-// distinct bank groups.
+// Chunk c of token row t sits at slot t * chunks + (c ^ row_key(t)).  LDS
+// on gfx950 has 64 banks of 4 bytes (a 256-byte period).  A 16-byte read is
+// served in four cycles of 16 lanes each: four blocks of four consecutive
+// lanes, the blocks of one half-wave split by the parity of the low three
+// bits of their index (lanes 0-3, 12-15, 20-27 together).  An 8-byte read,
+// plain or transposing, is served in two cycles of 32 consecutive lanes.
+// (Both measured with the bank-conflict counter on in-bounds probes.)  For
+// 256-byte rows the key below is an XOR-linear map (bits 0..3 of t to 2, 4,
+// 13, 8) chosen so that the three read patterns here see no conflict: the K
+// operand reads (lane (col, grp): row col, chunk 4 s + grp), the row reads
+// of V (row 4 grp + i, chunk col) and the transposing V reads (row
+// 4 grp + e, chunks 2 blk and 2 blk + 1).  For 128-byte rows no XOR key
+// clears all three; this one leaves the transposing reads free.
 template <int chunks>
 __device__ __forceinline__ int row_key(int t) {
-  if constexpr (chunks == 16) return ((t & 3) << 2) | ((t >> 2) & 3);
+  if constexpr (chunks == 16) return ((t & 3) << 1) ^ (t & 8) ^ (-((t >> 2) & 1) & 13);
   else return (((t >> 1) & 3) << 1) | ((t >> 3) & 1);
 }
 template <int chunks>
