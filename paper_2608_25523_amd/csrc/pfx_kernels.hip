@@ -9,21 +9,20 @@
 //                   taken straight from the lane's own scores, so the
 //                   online-softmax statistics of a column never leave the
 //                   four lanes that own it.
-// V is read from the pool with the keys as the contiguous direction of
-// neither operand; each lane loads 8 keys x (D/16) dims and transposes them
-// in registers with byte permutes.
+// V^T is read from the LDS stage with ds_read_b64_tr_b16, which hands each
+// lane 4 keys of one head dim out of a key-major tile.
 //
 // Three launches per call, in stream order:
 //   extend blocks: one workgroup per block of <= 128 query columns of one
 //     request and one KV head, streaming the prefix and the causal suffix
 //     through an LDS ring; rows written directly.
-//   decode: persistent workers.  The decode items (an agent's prefix against
-//     a block of its decode rows, a request's suffix against its own rows;
-//     one KV head each) are cut into 32-key steps, and every workgroup takes
-//     an equal contiguous run of the step list.  A worker's runs of steps
-//     flow through one LDS ring without a break at item boundaries; each
-//     piece of an item ends in final rows or a partial result.
-//   merge: rows seen by several pieces combine their partial results by
+//   decode: persistent workgroups.  The decode items (an agent's prefix
+//     against a block of its decode rows, a request's suffix against its own
+//     rows; one KV head each) are cut into pieces of at most 16 32-key
+//     steps, listed longest first and dealt to the workgroups in rounds; a
+//     workgroup's pieces flow through one LDS ring without a break at piece
+//     boundaries, and every piece leaves a partial state.
+//   merge: every decode row combines its pieces' partial states by
 //     log-sum-exp weights.
 // The launch boundaries order the phases: no atomics or device-wide fences.
 #include <hip/hip_runtime.h>
@@ -100,18 +99,6 @@ __device__ __forceinline__ float column_sum(float x) {
   return __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);
 }
 
-// V chunk held by one lane for one key: D/16 bf16 values.
-template <int D> struct VecCH;
-template <> struct VecCH<128> { typedef u32x4 T; static constexpr int dwords = 4; };
-template <> struct VecCH<64> { typedef u32x2 T; static constexpr int dwords = 2; };
-
-template <int D>
-struct KVRegs {
-  static constexpr int KS = D / 32;
-  u32x4 k[2][KS];                    // [tile][k-step]: key (lane & 15), dims 32s + 8*(lane>>4) .. +7
-  typename VecCH<D>::T v[2][4];      // [tile][i]: key 4*(lane>>4) + i, dims (D/16)*(lane&15) .. +D/16-1
-};
-
 struct AttnArgs {
   const uint16_t* kpool;
   const uint16_t* vpool;
@@ -148,158 +135,13 @@ __device__ __forceinline__ StepPos step_pos(const Item& it, int st, int s0_steps
   return p;
 }
 
-// bf16 element e (0..D/16-1) of a lane's V chunk, as the low 16 bits.
-template <int D>
-__device__ __forceinline__ uint32_t v_elem_pair(const typename VecCH<D>::T& a, const typename VecCH<D>::T& b,
-                                                int e) {
-  // Pack element e of key a (low half) with element e of key b (high half).
-  const uint32_t wa = a[e >> 1], wb = b[e >> 1];
-  return (e & 1) ? __builtin_amdgcn_perm(wb, wa, 0x07060302u) : __builtin_amdgcn_perm(wb, wa, 0x05040100u);
-}
-
-// V^T operand jj: dim CH*col + jj of the 8 keys this lane owns (tile 0 keys
-// 4*grp..+3, then tile 1 keys 4*grp..+3), built with byte permutes.
-template <int D>
-__device__ __forceinline__ bf16x8 v_operand(const KVRegs<D>& r, int jj) {
-  u32x4 w;
-  w[0] = v_elem_pair<D>(r.v[0][0], r.v[0][1], jj);
-  w[1] = v_elem_pair<D>(r.v[0][2], r.v[0][3], jj);
-  w[2] = v_elem_pair<D>(r.v[1][0], r.v[1][1], jj);
-  w[3] = v_elem_pair<D>(r.v[1][2], r.v[1][3], jj);
-  return __builtin_bit_cast(bf16x8, w);
-}
-
 template <int D, int QB>
 struct WaveState {
   static constexpr int CH = D / 16;
   f32x4 acc[QB][CH];  // O^T: lane holds dims 16 blk + 4 grp + i of its column, [blk][i]
-                      // (extend's register path: dims CH (4 grp + i) + jj, [jj][i])
   float m[QB];        // running max (log2 units), same in the 4 lanes of a column
   f32x4 lv[QB];       // running sum from the matrix unit: element 0 in the group-0 lanes, 0 elsewhere
 };
-
-// NSUB consecutive 32-key steps against the wave's query blocks, with one
-// online-softmax update for all of them: the NSUB score chains are
-// independent (instruction-level parallelism for a lone wave), and the
-// cross-lane max and the rescale check are paid once per NSUB * 32 keys.
-// Steps u >= nvalid are skipped.
-template <int D, int QB, int NSUB>
-__device__ __forceinline__ void compute_steps(WaveState<D, QB>& ws, KVRegs<D>* const (&rp)[NSUB],
-                                              const bf16x8 (&qf)[QB][D / 32], const int (&lim)[QB],
-                                              const StepPos (&p)[NSUB], int nvalid, int nblk, int grp,
-                                              float scale_log2) {
-  constexpr int KS = D / 32;
-  constexpr int CH = D / 16;
-  const uint32_t one2 = (threadIdx.x & 15) == 0 ? 0x3F803F80u : 0u;  // bf16 1.0 pairs in row 0
-  const bf16x8 ones_row0 = __builtin_bit_cast(bf16x8, u32x4{one2, one2, one2, one2});
-  // The causal limit only bites on steps that reach past the smallest limit
-  // of the wave's columns (block 0, column 0 holds the lowest token; padding
-  // columns repeat it): elsewhere every key is visible to every column.
-  const int lim_lo = __builtin_amdgcn_readfirstlane(lim[0]);
-  bool any_mask = false;
-#pragma unroll
-  for (int u = 0; u < NSUB; ++u) {
-    if (u >= nvalid) break;
-    const bool tail = p[u].k0 + kStepKeys > p[u].kend;
-    any_mask |= tail || (p[u].seg == 1 && p[u].k0 + kStepKeys - 1 > lim_lo);
-    if (tail) {
-      // Keys past the end of the segment: zero their V (the slots may hold
-      // anything) -- their probabilities are forced to 0 below.
-      PFX_KEEP_BRANCH();
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (p[u].k0 + 16 * t + 4 * grp + i >= p[u].kend) rp[u]->v[t][i] = typename VecCH<D>::T{};
-    }
-  }
-#pragma unroll
-  for (int b = 0; b < QB; ++b) {
-    if (b >= nblk) break;
-    // Raw scores s = q.k; lane holds keys 16t + 4*grp + i of each step.
-    float sc[NSUB][8];
-#pragma unroll
-    for (int u = 0; u < NSUB; ++u) {
-      if (u >= nvalid) break;
-      f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, rp[u]->k[0][s]), qf[b][s], s0, 0, 0, 0);
-        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, rp[u]->k[1][s]), qf[b][s], s1, 0, 0, 0);
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        sc[u][i] = s0[i];
-        sc[u][4 + i] = s1[i];
-      }
-    }
-    if (any_mask) {
-      PFX_KEEP_BRANCH();
-#pragma unroll
-      for (int u = 0; u < NSUB; ++u) {
-        if (u >= nvalid) break;
-        const int lim_b = p[u].seg == 1 ? lim[b] : 0x7fffffff;
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int key = p[u].k0 + 16 * t + 4 * grp + i;
-            if (key >= p[u].kend || key > lim_b) sc[u][4 * t + i] = -INFINITY;
-          }
-      }
-    }
-    float mx = -INFINITY;
-#pragma unroll
-    for (int u = 0; u < NSUB; ++u) {
-      if (u >= nvalid) break;
-      mx = fmaxf(mx, fmaxf(fmaxf(fmaxf(sc[u][0], sc[u][1]), fmaxf(sc[u][2], sc[u][3])),
-                           fmaxf(fmaxf(sc[u][4], sc[u][5]), fmaxf(sc[u][6], sc[u][7]))));
-    }
-    // A column's running max only moves when its scaled max passes m + slack,
-    // which needs some lane of the column past it: the cross-lane reduction
-    // is paid only when a lane of the wave is (scale > 0).
-    if (__any(mx * scale_log2 > ws.m[b] + kRescaleSlack)) {
-      PFX_KEEP_BRANCH();
-      mx = column_max(mx) * scale_log2;
-      const bool raise = mx > ws.m[b] + kRescaleSlack;
-      const float mnew = raise ? mx : ws.m[b];
-      const float alpha = fast_exp2(ws.m[b] - mnew);
-      ws.lv[b][0] *= alpha;  // rows other than 0 stay zero
-#pragma unroll
-      for (int jj = 0; jj < CH; ++jj) ws.acc[b][jj] *= alpha;
-      ws.m[b] = mnew;
-    }
-    const float neg_m = -ws.m[b];
-#pragma unroll
-    for (int u = 0; u < NSUB; ++u) {
-      if (u >= nvalid) break;
-      float pr[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) pr[j] = fast_exp2(fmaf(sc[u][j], scale_log2, neg_m));
-      u32x4 pw;
-      pw[0] = pack_bf16(pr[0], pr[1]);
-      pw[1] = pack_bf16(pr[2], pr[3]);
-      pw[2] = pack_bf16(pr[4], pr[5]);
-      pw[3] = pack_bf16(pr[6], pr[7]);
-      const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
-#pragma unroll
-      for (int jj = 0; jj < CH; ++jj)
-        ws.acc[b][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v_operand<D>(*rp[u], jj), pb, ws.acc[b][jj], 0, 0, 0);
-      // Row sums of P on the matrix unit: an A operand whose row 0 is ones
-      // (lane col 0 of each group) puts sum_k P[col][k] in row 0.
-      ws.lv[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones_row0, pb, ws.lv[b], 0, 0, 0);
-    }
-  }
-}
-
-template <int D, int QB>
-__device__ __forceinline__ void compute_step(WaveState<D, QB>& ws, KVRegs<D>& r, const bf16x8 (&qf)[QB][D / 32],
-                                             const int (&lim)[QB], const StepPos& p, int nblk, int grp,
-                                             float scale_log2) {
-  KVRegs<D>* const one[1] = {&r};
-  const StepPos pos[1] = {p};
-  compute_steps<D, QB, 1>(ws, one, qf, lim, pos, 1, nblk, grp, scale_log2);
-}
 
 template <int D, int QB>
 __device__ __forceinline__ void reset_state(WaveState<D, QB>& ws) {
@@ -576,54 +418,136 @@ __device__ __forceinline__ void attend_step(WaveState<D, QB>& ws, const unsigned
   }
 }
 
-// Read a stage into the register layout compute_step expects.
-template <int D>
-__device__ __forceinline__ void read_tile(KVRegs<D>& r, const unsigned char* stage, int col, int grp) {
+// One 32-key step of an extend block against the wave's QB blocks of 16
+// query columns (blocks past the wave's columns compute on zero queries and
+// are never written), straight from the stage in LDS:
+//   S^T = K Q^T: lane (col, grp) gets the scores of keys 16 t + 4 grp + i;
+//   online softmax in log2 units, the maximum raised lazily: the cross-lane
+//   column maximum is taken only when some lane passes m + slack;
+//   O^T += V^T P^T with P from the lane's own scores and V^T read by
+//   ds_read_b64_tr_b16 (accumulator [blk][i] = dim 16 blk + 4 grp + i), and
+//   the row sums of P on the matrix unit (an A operand whose row 0 is ones).
+// The rare paths (tail keys, masking on diagonal and tail steps, raising the
+// maximum) are one branch each for all blocks, and the exponentials of one
+// block interleave with the P V MFMAs of the other.
+template <int D, int QB>
+__device__ __forceinline__ void extend_step(WaveState<D, QB>& ws, const unsigned char* stage,
+                                            const bf16x8 (&qf)[QB][D / 32], const int (&lim)[QB], int lim_lo,
+                                            const StepPos& p, int lane, float scale_log2) {
   using TG = TileGeom<D>;
   constexpr int KS = D / 32;
+  constexpr int CH = D / 16;
+  const int col = lane & 15, grp = lane >> 4;
+  u32x4 kf[2][KS];
 #pragma unroll
   for (int t = 0; t < 2; ++t)
 #pragma unroll
     for (int s = 0; s < KS; ++s)
-      r.k[t][s] = *reinterpret_cast<const u32x4*>(stage + t * TG::page_bytes +
-                                                  16 * swizzled_slot<TG::chunks>(col, 4 * s + grp));
+      kf[t][s] = *reinterpret_cast<const u32x4*>(stage + t * TG::page_bytes +
+                                                 16 * swizzled_slot<TG::chunks>(col, 4 * s + grp));
+  bf16x8 vop[CH];
 #pragma unroll
-  for (int t = 0; t < 2; ++t)
+  for (int blk = 0; blk < CH; ++blk)
+    vop[blk] = v_operand_tr<D>(stage + 2 * TG::page_bytes, stage + 3 * TG::page_bytes, blk, lane, ~uint64_t(0),
+                               ~uint64_t(0));
+  const bool tail = p.k0 + kStepKeys > p.kend;
+  if (tail) {
+    // Keys past the end of the segment: zero their V (the slots may hold
+    // anything); their probabilities are forced to 0 below.  Element e of
+    // each half of an operand is key 16 t + 4 grp + e.
+    PFX_KEEP_BRANCH();
+    uint32_t keep[2][2] = {{~0u, ~0u}, {~0u, ~0u}};
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const unsigned char* vb = stage + (2 + t) * TG::page_bytes;
-      if constexpr (D == 128) {
-        r.v[t][i] = *reinterpret_cast<const u32x4*>(vb + 16 * swizzled_slot<TG::chunks>(4 * grp + i, col));
-      } else {
-        r.v[t][i] = *reinterpret_cast<const u32x2*>(vb + 16 * swizzled_slot<TG::chunks>(4 * grp + i, col >> 1) +
-                                                    8 * (col & 1));
-      }
-    }
-}
-
-// Final rows from the register path's layout: lane (col, grp) holds dims
-// CH (4 grp + i) + jj of its column, eight consecutive dims per i.
-template <int D>
-__device__ __forceinline__ void write_rows_jj(const AttnArgs& a, const f32x4 (&acc)[D / 16], float m, float l_lane,
-                                              int orow, bool valid, int grp) {
-  constexpr int CH = D / 16;
-  const float l = column_sum(l_lane);
-  if (!valid) return;
-  const float inv = l > 0.f ? 1.0f / l : 0.f;
-  const float lse_nat = l > 0.f ? (m + log2f(l)) * kLn2 : -INFINITY;
-  uint16_t* out = a.o + size_t(orow) * D + 4 * CH * grp;
+    for (int t = 0; t < 2; ++t)
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    if constexpr (CH == 8) {
-      u32x4 w = {pack_bf16(acc[0][i] * inv, acc[1][i] * inv), pack_bf16(acc[2][i] * inv, acc[3][i] * inv),
-                 pack_bf16(acc[4][i] * inv, acc[5][i] * inv), pack_bf16(acc[6][i] * inv, acc[7][i] * inv)};
-      *reinterpret_cast<u32x4*>(out + CH * i) = w;
-    } else {
-      u32x2 w = {pack_bf16(acc[0][i] * inv, acc[1][i] * inv), pack_bf16(acc[2][i] * inv, acc[3][i] * inv)};
-      *reinterpret_cast<u32x2*>(out + CH * i) = w;
+      for (int e = 0; e < 4; ++e)
+        if (p.k0 + 16 * t + 4 * grp + e >= p.kend) keep[t][e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
+#pragma unroll
+    for (int blk = 0; blk < CH; ++blk) {
+      u32x4 w = __builtin_bit_cast(u32x4, vop[blk]);
+      w[0] &= keep[0][0];
+      w[1] &= keep[0][1];
+      w[2] &= keep[1][0];
+      w[3] &= keep[1][1];
+      vop[blk] = __builtin_bit_cast(bf16x8, w);
     }
   }
-  if (a.lse && grp == 0) a.lse[orow] = lse_nat;
+  f32x4 sc[QB][2];
+#pragma unroll
+  for (int b = 0; b < QB; ++b) {
+    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf[0][s]), qf[b][s], s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf[1][s]), qf[b][s], s1, 0, 0, 0);
+    }
+    sc[b][0] = s0;
+    sc[b][1] = s1;
+  }
+  // The causal limit only bites on steps that reach past the smallest limit
+  // of the wave's columns (lim_lo); elsewhere every key is visible.
+  if (tail || (p.seg == 1 && p.k0 + kStepKeys - 1 > lim_lo)) {
+    PFX_KEEP_BRANCH();
+#pragma unroll
+    for (int b = 0; b < QB; ++b) {
+      const int lim_b = p.seg == 1 ? lim[b] : 0x7fffffff;
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int key = p.k0 + 16 * t + 4 * grp + i;
+          if (key >= p.kend || key > lim_b) sc[b][t][i] = -INFINITY;
+        }
+    }
+  }
+  float mx[QB];
+  bool pass = false;
+#pragma unroll
+  for (int b = 0; b < QB; ++b) {
+    mx[b] = fmaxf(fmaxf(fmaxf(sc[b][0][0], sc[b][0][1]), fmaxf(sc[b][0][2], sc[b][0][3])),
+                  fmaxf(fmaxf(sc[b][1][0], sc[b][1][1]), fmaxf(sc[b][1][2], sc[b][1][3])));
+    pass = pass || mx[b] * scale_log2 > ws.m[b] + kRescaleSlack;  // scale > 0
+  }
+  if (__any(pass)) {
+    PFX_KEEP_BRANCH();
+#pragma unroll
+    for (int b = 0; b < QB; ++b) {
+      const float cm = column_max(mx[b]) * scale_log2;
+      const float mnew = cm > ws.m[b] + kRescaleSlack ? cm : ws.m[b];
+      const float alpha = fast_exp2(ws.m[b] - mnew);  // 1 for columns that keep their maximum
+      ws.lv[b][0] *= alpha;                           // rows other than 0 stay zero
+#pragma unroll
+      for (int blk = 0; blk < CH; ++blk) ws.acc[b][blk] *= alpha;
+      ws.m[b] = mnew;
+    }
+  }
+  const uint32_t one2 = col == 0 ? 0x3F803F80u : 0u;  // bf16 1.0 pairs in row 0
+  const bf16x8 ones_row0 = __builtin_bit_cast(bf16x8, u32x4{one2, one2, one2, one2});
+#pragma unroll
+  for (int b = 0; b < QB; ++b) {
+    const float neg_m = -ws.m[b];
+    float pr[8];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pr[4 * t + i] = fast_exp2(fmaf(sc[b][t][i], scale_log2, neg_m));
+    const u32x4 pw = {pack_bf16(pr[0], pr[1]), pack_bf16(pr[2], pr[3]), pack_bf16(pr[4], pr[5]),
+                      pack_bf16(pr[6], pr[7])};
+    const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
+#pragma unroll
+    for (int blk = 0; blk < CH; ++blk)
+      ws.acc[b][blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop[blk], pb, ws.acc[b][blk], 0, 0, 0);
+    ws.lv[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones_row0, pb, ws.lv[b], 0, 0, 0);
+  }
+  // Block 0's probabilities first, then its P V MFMAs interleaved with the
+  // next block's exponentials.
+  __builtin_amdgcn_sched_group_barrier(0x002, 21, 1);
+#pragma unroll
+  for (int g = 0; g < (QB - 1) * (CH + 1); ++g) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+    __builtin_amdgcn_sched_group_barrier(0x002, 2, 1);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, CH + 1, 1);
 }
 
 // Normalise a wave's block and write it as final rows (bf16 o, lse): lane
@@ -730,6 +654,9 @@ __device__ __forceinline__ void extend_block(const AttnArgs& a, const Item* itp,
       for (int s = 0; s < KS; ++s) qf[b][s] = bf16x8{};
     }
   }
+  // Block 0, column 0 holds the wave's lowest token (padding columns repeat
+  // the item's first row).
+  const int lim_lo = __builtin_amdgcn_readfirstlane(lim[0]);
   WaveState<D, QBW> ws;
   reset_state(ws);
   const int s0_steps = (it.s0_kend - it.s0_kbeg + kStepKeys - 1) / kStepKeys;
@@ -753,17 +680,13 @@ __device__ __forceinline__ void extend_block(const AttnArgs& a, const Item* itp,
       const int nxt = st + NS - 1;
       if (nxt < nsteps)
         issue_block_step<D>(ring[(r + NS - 1) % NS], a, it, ptab, lead, p0n, nxt, s0_steps, h, wave, lane);
-      if (nb > 0) {
-        KVRegs<D> kv;
-        read_tile<D>(kv, ring[r], col, grp);
-        compute_step<D, QBW>(ws, kv, qf, lim, step_pos(it, st, s0_steps), nb, grp, a.scale_log2);
-      }
+      if (nb > 0) extend_step<D, QBW>(ws, ring[r], qf, lim, lim_lo, step_pos(it, st, s0_steps), lane, a.scale_log2);
     }
   }
 #pragma unroll
   for (int b = 0; b < QBW; ++b) {
     const int c = (wave * QBW + b) * kTileCols + col;
-    write_rows_jj<D>(a, ws.acc[b], ws.m[b], ws.lv[b][0], orow[b], b < nb && (c >> a.group_shift) < it.row_count, grp);
+    write_rows<D>(a, ws.acc[b], ws.m[b], ws.lv[b][0], orow[b], b < nb && (c >> a.group_shift) < it.row_count, grp);
   }
 }
 
