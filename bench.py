@@ -44,20 +44,35 @@ def log(msg):
 
 def timed_steps(fn_step, fn_attn, steps, warmup, torch):
     """Run warmup + timed steps; returns (ms per step, mean ms of the
-    attention call measured with events on the launch stream)."""
+    attention call measured with events on the launch stream).
+
+    Two passes: the steps with nothing between them (events only around the
+    whole pass) give the step time; the same number of attention calls back
+    to back, bracketed by one event pair, give the attention duration.
+    (Event records inside a ~35 us step add several us to what they
+    bracket.)"""
     for i in range(warmup):
         fn_step(i)
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    e0.record(stream)
     for i in range(steps):
-        fn_step(i, ev[i], stream)
+        fn_step(i)
+    e1.record(stream)
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) * 1e3 / steps
-    attn = sum(a.elapsed_time(b) for a, b in ev) / steps
-    return wall, attn
+    step_ms = max(wall, e0.elapsed_time(e1) / steps)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for i in range(steps):
+        fn_attn(i)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    attn = e0.elapsed_time(e1) / steps
+    return step_ms, attn
 
 
 def bench_decode(args, torch, B, RN, W):
@@ -75,16 +90,15 @@ def bench_decode(args, torch, B, RN, W):
         plans.append(B.plan_from_batch(ds.pool, rb, B.PFX_MODE_DECODE).upload())
     torch.cuda.synchronize()
 
-    def step(i, ev=None, stream=None):
+    def step(i):
         plan = plans[i % len(plans)]
         B.pfx_append_kv(ds.pool, plan, ds.k_new, ds.v_new)
-        if ev is not None:
-            ev[0].record(stream)
         B.pfx_attention(ds.pool, plan, ds.q, ds.o, ds.lse)
-        if ev is not None:
-            ev[1].record(stream)
 
-    ms, attn_ms = timed_steps(step, None, args.steps, args.warmup, torch)
+    def attn(i):
+        B.pfx_attention(ds.pool, plans[i % len(plans)], ds.q, ds.o, ds.lse)
+
+    ms, attn_ms = timed_steps(step, attn, args.steps, args.warmup, torch)
     B.pfx_sync_check()
     u = b.unique_kv_bytes()
     st = ds.plan.stats()
@@ -97,16 +111,15 @@ def bench_extend(args, torch, B, RN, W):
     ds = RN.DeviceStep(b, hv, poison=False)
     torch.cuda.synchronize()
 
-    def step(i, ev=None, stream=None):
+    def step(i):
         B.pfx_append_kv(ds.pool, ds.plan, ds.k_new, ds.v_new)
-        if ev is not None:
-            ev[0].record(stream)
         B.pfx_attention(ds.pool, ds.plan, ds.q, ds.o, ds.lse)
-        if ev is not None:
-            ev[1].record(stream)
+
+    def attn(i):
+        B.pfx_attention(ds.pool, ds.plan, ds.q, ds.o, ds.lse)
 
     steps = max(3, args.steps // 4)
-    ms, attn_ms = timed_steps(step, None, steps, max(1, args.warmup // 4), torch)
+    ms, attn_ms = timed_steps(step, attn, steps, max(1, args.warmup // 4), torch)
     B.pfx_sync_check()
     return dict(ms=ms, attn_ms=attn_ms, flops=b.attention_flops(), steps=steps)
 
