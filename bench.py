@@ -65,14 +65,23 @@ def timed_steps(fn_step, fn_attn, steps, warmup, torch):
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) * 1e3 / steps
     step_ms = max(wall, e0.elapsed_time(e1) / steps)
+    # The attention pass in groups of (up to) 10 back-to-back calls, one event
+    # pair per group: the mean over all calls, and the spread over groups.
+    group = 10
+    evs = []
     torch.cuda.synchronize()
-    e0.record(stream)
-    for i in range(steps):
-        fn_attn(i)
-    e1.record(stream)
+    for g0 in range(0, steps, group):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for i in range(g0, min(steps, g0 + group)):
+            fn_attn(i)
+        b.record(stream)
+        evs.append((a, b, min(steps, g0 + group) - g0))
     torch.cuda.synchronize()
-    attn = e0.elapsed_time(e1) / steps
-    return step_ms, attn
+    per = sorted(a.elapsed_time(b) / n for a, b, n in evs)
+    attn = sum(a.elapsed_time(b) for a, b, _ in evs) / steps
+    pct = lambda q: per[min(len(per) - 1, int(round(q * (len(per) - 1))))]
+    return step_ms, attn, {"p10": pct(0.1), "p50": pct(0.5), "p90": pct(0.9)}
 
 
 def bench_decode(args, torch, B, RN, W):
@@ -98,11 +107,45 @@ def bench_decode(args, torch, B, RN, W):
     def attn(i):
         B.pfx_attention(ds.pool, plans[i % len(plans)], ds.q, ds.o, ds.lse)
 
-    ms, attn_ms = timed_steps(step, attn, args.steps, args.warmup, torch)
+    ms, attn_ms, spread = timed_steps(step, attn, args.steps, args.warmup, torch)
     B.pfx_sync_check()
+    graph_ms = graph_replay_ms(plans, ds, args.steps, torch, B)
     u = b.unique_kv_bytes()
     st = ds.plan.stats()
-    return dict(batch=b, hv=hv, ms=ms, attn_ms=attn_ms, unique_bytes=u, replicas=len(plans), stats=st)
+    return dict(batch=b, hv=hv, ms=ms, attn_ms=attn_ms, spread=spread, graph_ms=graph_ms, unique_bytes=u,
+                replicas=len(plans), stats=st)
+
+
+def graph_replay_ms(plans, ds, steps, torch, B):
+    """One decode step per replica plan captured into a HIP graph (through
+    torch's graph API; the library's calls are plain kernel launches on the
+    given stream), replayed: ms per step.  The last replayed step's output
+    must equal the eager result of the same plan, else None."""
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        cs = torch.cuda.current_stream().cuda_stream
+        for p in plans:
+            B.pfx_append_kv(ds.pool, p, ds.k_new, ds.v_new, stream=cs)
+            B.pfx_attention(ds.pool, p, ds.q, ds.o, ds.lse, stream=cs)
+    torch.cuda.synchronize()
+    reps = max(2, steps // len(plans))
+    for _ in range(2):
+        g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / (reps * len(plans))
+    out_graph = ds.o.clone()
+    B.pfx_attention(ds.pool, plans[-1], ds.q, ds.o, ds.lse)
+    torch.cuda.synchronize()
+    same = bool(torch.equal(out_graph.view(torch.int16), ds.o.view(torch.int16)))
+    return ms if same else None
 
 
 def bench_extend(args, torch, B, RN, W):
@@ -119,7 +162,7 @@ def bench_extend(args, torch, B, RN, W):
         B.pfx_attention(ds.pool, ds.plan, ds.q, ds.o, ds.lse)
 
     steps = max(3, args.steps // 4)
-    ms, attn_ms = timed_steps(step, attn, steps, max(1, args.warmup // 4), torch)
+    ms, attn_ms, _ = timed_steps(step, attn, steps, max(1, args.warmup // 4), torch)
     B.pfx_sync_check()
     return dict(ms=ms, attn_ms=attn_ms, flops=b.attention_flops(), steps=steps)
 
@@ -259,7 +302,9 @@ def main():
         "roofline": {"bound": "hbm", "kernel": "pfx_attention: decode_kernel + merge_rows_kernel",
                      "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic_from_profile("decode"),
-                     "attn_us": round(dec["attn_ms"] * 1e3, 3)},
+                     "attn_us": round(dec["attn_ms"] * 1e3, 3),
+                     "attn_us_p10_p50_p90": [round(dec["spread"][k] * 1e3, 3) for k in ("p10", "p50", "p90")]},
+        "graph_ms_per_step": None if dec["graph_ms"] is None else round(dec["graph_ms"], 5),
         "cpu_baseline": cpu,
     }
     if ext is not None:

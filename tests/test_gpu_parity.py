@@ -128,6 +128,39 @@ def test_small_batches(case):
     run_and_check(b, hv, f"small{seed}", **opts)
 
 
+def test_graph_replay_matches_eager():
+    """A mixed step (append, then attention) captured into a HIP graph through
+    torch's graph API and replayed several times, with eager work and
+    synchronizations between the replays: every replay reproduces the eager
+    result bit for bit (the library's calls are plain kernel launches on the
+    given stream, with no memset nodes)."""
+    seed, hq, hkv, d, plen, reqs, opts = SMALL_CASES[1]
+    b = W.make_batch(seed, num_q_heads=hq, num_kv_heads=hkv, head_dim=d, num_pages=256, prefix_len=plen,
+                     agent=[r[0] for r in reqs], suffix_len=[r[1] for r in reqs], n_rows=[r[2] for r in reqs])
+    hv = W.host_values(b, seed + 50)
+    announce("graph replay: small2 mixed step, 3 replays")
+    ds = RN.DeviceStep(b, hv, **opts)
+    ds.step()
+    B.pfx_sync_check()
+    o_eager, l_eager = ds.outputs()
+    s = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        cs = torch.cuda.current_stream().cuda_stream
+        B.pfx_append_kv(ds.pool, ds.plan, ds.k_new, ds.v_new, stream=cs)
+        B.pfx_attention(ds.pool, ds.plan, ds.q, ds.o, ds.lse, stream=cs)
+    for rep in range(3):
+        ds.o.zero_()
+        ds.lse.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        B.pfx_sync_check()
+        o, l = ds.outputs()
+        assert np.array_equal(o, o_eager), f"replay {rep}: O differs from the eager result"
+        assert np.array_equal(l, l_eager), f"replay {rep}: LSE differs from the eager result"
+
+
 def test_many_partials_merge():
     """Thousands of workers for a small batch: prefix items cut into pieces of
     one or two steps, 40+ partial results per row, merged by the merge launch."""
