@@ -418,94 +418,79 @@ __device__ __forceinline__ void attend_step(WaveState<D, QB>& ws, const unsigned
   }
 }
 
-// One 32-key step of an extend block against the wave's QB blocks of 16
-// query columns (blocks past the wave's columns compute on zero queries and
-// are never written), straight from the stage in LDS:
+// Two consecutive 32-key steps of an extend block under one barrier,
+// against the wave's QB blocks of 16 query columns (blocks past the wave's
+// columns compute on zero queries and are never written):
 //   S^T = K Q^T: lane (col, grp) gets the scores of keys 16 t + 4 grp + i;
-//   online softmax in log2 units, the maximum raised lazily: the cross-lane
-//   column maximum is taken only when some lane passes m + slack;
+//   online softmax in log2 units, the maximum raised lazily: one maximum
+//   over the 64 keys, and the cross-lane column maximum taken only when some
+//   lane passes m + slack;
 //   O^T += V^T P^T with P from the lane's own scores and V^T read by
 //   ds_read_b64_tr_b16 (accumulator [blk][i] = dim 16 blk + 4 grp + i), and
 //   the row sums of P on the matrix unit (an A operand whose row 0 is ones).
-// The rare paths (tail keys, masking on diagonal and tail steps, raising the
-// maximum) are one branch each for all blocks, and the exponentials of one
-// block interleave with the P V MFMAs of the other.
+// The rare paths (masking on diagonal and tail steps, raising the maximum,
+// zeroing V past the end) are one branch each.  V^T of the second step is
+// read after the first step's products, so the two operand sets share
+// registers.
 template <int D, int QB>
-__device__ __forceinline__ void extend_step(WaveState<D, QB>& ws, const unsigned char* stage,
-                                            const bf16x8 (&qf)[QB][D / 32], const int (&lim)[QB], int lim_lo,
-                                            const StepPos& p, int lane, float scale_log2) {
+__device__ __forceinline__ void extend_pair(WaveState<D, QB>& ws, const unsigned char* st0,
+                                            const unsigned char* st1, const bf16x8 (&qf)[QB][D / 32],
+                                            const int (&lim)[QB], int lim_lo, const StepPos& p0, const StepPos& p1,
+                                            int lane, float scale_log2) {
   using TG = TileGeom<D>;
   constexpr int KS = D / 32;
   constexpr int CH = D / 16;
   const int col = lane & 15, grp = lane >> 4;
-  u32x4 kf[2][KS];
+  f32x4 sc[2][QB][2];
 #pragma unroll
-  for (int t = 0; t < 2; ++t)
+  for (int u = 0; u < 2; ++u) {
+    const unsigned char* stage = u ? st1 : st0;
 #pragma unroll
-    for (int s = 0; s < KS; ++s)
-      kf[t][s] = *reinterpret_cast<const u32x4*>(stage + t * TG::page_bytes +
-                                                 16 * swizzled_slot<TG::chunks>(col, 4 * s + grp));
-  bf16x8 vop[CH];
+    for (int t = 0; t < 2; ++t) {
+      u32x4 kf[KS];
 #pragma unroll
-  for (int blk = 0; blk < CH; ++blk)
-    vop[blk] = v_operand_tr<D>(stage + 2 * TG::page_bytes, stage + 3 * TG::page_bytes, blk, lane, ~uint64_t(0),
-                               ~uint64_t(0));
-  const bool tail = p.k0 + kStepKeys > p.kend;
-  if (tail) {
-    // Keys past the end of the segment: zero their V (the slots may hold
-    // anything); their probabilities are forced to 0 below.  Element e of
-    // each half of an operand is key 16 t + 4 grp + e.
-    PFX_KEEP_BRANCH();
-    uint32_t keep[2][2] = {{~0u, ~0u}, {~0u, ~0u}};
+      for (int s = 0; s < KS; ++s)
+        kf[s] = *reinterpret_cast<const u32x4*>(stage + t * TG::page_bytes +
+                                                16 * swizzled_slot<TG::chunks>(col, 4 * s + grp));
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+      for (int b = 0; b < QB; ++b) {
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        if (p.k0 + 16 * t + 4 * grp + e >= p.kend) keep[t][e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
-#pragma unroll
-    for (int blk = 0; blk < CH; ++blk) {
-      u32x4 w = __builtin_bit_cast(u32x4, vop[blk]);
-      w[0] &= keep[0][0];
-      w[1] &= keep[0][1];
-      w[2] &= keep[1][0];
-      w[3] &= keep[1][1];
-      vop[blk] = __builtin_bit_cast(bf16x8, w);
+        for (int s = 0; s < KS; ++s)
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf[s]), qf[b][s], acc, 0, 0, 0);
+        sc[u][b][t] = acc;
+      }
     }
   }
-  f32x4 sc[QB][2];
-#pragma unroll
-  for (int b = 0; b < QB; ++b) {
-    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf[0][s]), qf[b][s], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf[1][s]), qf[b][s], s1, 0, 0, 0);
-    }
-    sc[b][0] = s0;
-    sc[b][1] = s1;
-  }
-  // The causal limit only bites on steps that reach past the smallest limit
-  // of the wave's columns (lim_lo); elsewhere every key is visible.
-  if (tail || (p.seg == 1 && p.k0 + kStepKeys - 1 > lim_lo)) {
+  const bool tail0 = p0.k0 + kStepKeys > p0.kend, tail1 = p1.k0 + kStepKeys > p1.kend;
+  if (tail0 || tail1 || (p0.seg == 1 && p0.k0 + kStepKeys - 1 > lim_lo) ||
+      (p1.seg == 1 && p1.k0 + kStepKeys - 1 > lim_lo)) {
     PFX_KEEP_BRANCH();
 #pragma unroll
-    for (int b = 0; b < QB; ++b) {
-      const int lim_b = p.seg == 1 ? lim[b] : 0x7fffffff;
+    for (int u = 0; u < 2; ++u) {
+      const StepPos& p = u ? p1 : p0;
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
+      for (int b = 0; b < QB; ++b) {
+        const int lim_b = p.seg == 1 ? lim[b] : 0x7fffffff;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int key = p.k0 + 16 * t + 4 * grp + i;
-          if (key >= p.kend || key > lim_b) sc[b][t][i] = -INFINITY;
-        }
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int key = p.k0 + 16 * t + 4 * grp + i;
+            if (key >= p.kend || key > lim_b) sc[u][b][t][i] = -INFINITY;
+          }
+      }
     }
   }
   float mx[QB];
   bool pass = false;
 #pragma unroll
   for (int b = 0; b < QB; ++b) {
-    mx[b] = fmaxf(fmaxf(fmaxf(sc[b][0][0], sc[b][0][1]), fmaxf(sc[b][0][2], sc[b][0][3])),
-                  fmaxf(fmaxf(sc[b][1][0], sc[b][1][1]), fmaxf(sc[b][1][2], sc[b][1][3])));
+    float m0 = fmaxf(fmaxf(fmaxf(sc[0][b][0][0], sc[0][b][0][1]), fmaxf(sc[0][b][0][2], sc[0][b][0][3])),
+                     fmaxf(fmaxf(sc[0][b][1][0], sc[0][b][1][1]), fmaxf(sc[0][b][1][2], sc[0][b][1][3])));
+    float m1 = fmaxf(fmaxf(fmaxf(sc[1][b][0][0], sc[1][b][0][1]), fmaxf(sc[1][b][0][2], sc[1][b][0][3])),
+                     fmaxf(fmaxf(sc[1][b][1][0], sc[1][b][1][1]), fmaxf(sc[1][b][1][2], sc[1][b][1][3])));
+    mx[b] = fmaxf(m0, m1);
     pass = pass || mx[b] * scale_log2 > ws.m[b] + kRescaleSlack;  // scale > 0
   }
   if (__any(pass)) {
@@ -524,30 +509,52 @@ __device__ __forceinline__ void extend_step(WaveState<D, QB>& ws, const unsigned
   const uint32_t one2 = col == 0 ? 0x3F803F80u : 0u;  // bf16 1.0 pairs in row 0
   const bf16x8 ones_row0 = __builtin_bit_cast(bf16x8, u32x4{one2, one2, one2, one2});
 #pragma unroll
-  for (int b = 0; b < QB; ++b) {
-    const float neg_m = -ws.m[b];
-    float pr[8];
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) pr[4 * t + i] = fast_exp2(fmaf(sc[b][t][i], scale_log2, neg_m));
-    const u32x4 pw = {pack_bf16(pr[0], pr[1]), pack_bf16(pr[2], pr[3]), pack_bf16(pr[4], pr[5]),
-                      pack_bf16(pr[6], pr[7])};
-    const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
+  for (int u = 0; u < 2; ++u) {
+    const unsigned char* stage = u ? st1 : st0;
+    const StepPos& p = u ? p1 : p0;
+    if (u) asm volatile("" ::: "memory");  // the second step's V reads stay after the first step's products
+    bf16x8 vop[CH];
 #pragma unroll
     for (int blk = 0; blk < CH; ++blk)
-      ws.acc[b][blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop[blk], pb, ws.acc[b][blk], 0, 0, 0);
-    ws.lv[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones_row0, pb, ws.lv[b], 0, 0, 0);
-  }
-  // Block 0's probabilities first, then its P V MFMAs interleaved with the
-  // next block's exponentials.
-  __builtin_amdgcn_sched_group_barrier(0x002, 21, 1);
+      vop[blk] = v_operand_tr<D>(stage + 2 * TG::page_bytes, stage + 3 * TG::page_bytes, blk, lane, ~uint64_t(0),
+                                 ~uint64_t(0));
+    if (p.k0 + kStepKeys > p.kend) {
+      // Keys past the end of the segment: zero their V (the slots may hold
+      // anything).  Element e of each half of an operand is key 16 t + 4 grp + e.
+      PFX_KEEP_BRANCH();
+      uint32_t keep[2][2] = {{~0u, ~0u}, {~0u, ~0u}};
 #pragma unroll
-  for (int g = 0; g < (QB - 1) * (CH + 1); ++g) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
-    __builtin_amdgcn_sched_group_barrier(0x002, 2, 1);
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (p.k0 + 16 * t + 4 * grp + e >= p.kend) keep[t][e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
+#pragma unroll
+      for (int blk = 0; blk < CH; ++blk) {
+        u32x4 w = __builtin_bit_cast(u32x4, vop[blk]);
+        w[0] &= keep[0][0];
+        w[1] &= keep[0][1];
+        w[2] &= keep[1][0];
+        w[3] &= keep[1][1];
+        vop[blk] = __builtin_bit_cast(bf16x8, w);
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < QB; ++b) {
+      const float neg_m = -ws.m[b];
+      float pr[8];
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) pr[4 * t + i] = fast_exp2(fmaf(sc[u][b][t][i], scale_log2, neg_m));
+      const u32x4 pw = {pack_bf16(pr[0], pr[1]), pack_bf16(pr[2], pr[3]), pack_bf16(pr[4], pr[5]),
+                        pack_bf16(pr[6], pr[7])};
+      const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
+#pragma unroll
+      for (int blk = 0; blk < CH; ++blk)
+        ws.acc[b][blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop[blk], pb, ws.acc[b][blk], 0, 0, 0);
+      ws.lv[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones_row0, pb, ws.lv[b], 0, 0, 0);
+    }
   }
-  __builtin_amdgcn_sched_group_barrier(0x008, CH + 1, 1);
 }
 
 // Normalise a wave's block and write it as final rows (bf16 o, lse): lane
@@ -602,10 +609,10 @@ template <int D>
 constexpr int extend_smem_bytes() { return kStages * TileGeom<D>::stage_bytes + kMaxTilePages * 4; }
 
 // One extend block (QBW blocks of 16 columns per wave): its K/V streams once
-// through the LDS ring; at every step each wave waits for its own copies,
-// all waves meet (the step's stage complete everywhere, the previous stage
-// consumed), the freed stage is refilled kStages - 1 steps ahead, and every
-// wave multiplies the step against its own columns.
+// through the LDS ring, two steps at a time; at every pair each wave waits
+// for its own copies, all waves meet (the pair's stages complete everywhere,
+// the previous pair's stages consumed), those are refilled two steps ahead,
+// and every wave multiplies the pair against its own columns.
 template <int D, int QBW>
 __device__ __forceinline__ void extend_block(const AttnArgs& a, const Item* itp, unsigned char* smem) {
   using TG = TileGeom<D>;
@@ -664,23 +671,34 @@ __device__ __forceinline__ void extend_block(const AttnArgs& a, const Item* itp,
   const int nsteps = s0_steps + s1_steps;
   // The first steps' pages are among the leading ids: request them before
   // waiting for the page table.
-  for (int st = 0; st < NS - 1 && st < nsteps; ++st)
+  for (int st = 0; st < 2 && st < nsteps; ++st)
     issue_block_step<D>(ring[st], a, it, ptab, lead, p0n, st, s0_steps, h, wave, lane);
   __syncthreads();  // page table ready
-  // Unrolled by the ring depth: each copy of the body works on a fixed
-  // stage, so its LDS addresses are a lane offset plus an immediate.
-  for (int st0 = 0; st0 < nsteps; st0 += NS) {
+  // Two steps per barrier: at pair q (steps 2q, 2q + 1) wait for both
+  // stages, meet (so the stages of the previous pair are free), refill them
+  // with steps 2q + 2 and 2q + 3, and run the pair.  Unrolled by two pairs,
+  // so every copy of the body works on fixed stages and its LDS addresses
+  // are a lane offset plus an immediate.
+  static_assert(NS == 4, "pairs of steps in a ring of four stages");
+  for (int st0 = 0; st0 < nsteps; st0 += 4) {
 #pragma unroll
-    for (int r = 0; r < NS; ++r) {
-      const int st = st0 + r;
+    for (int k = 0; k < 2; ++k) {
+      const int st = st0 + 2 * k;
       if (st >= nsteps) break;
-      const int ahead = nsteps - 1 - st < NS - 2 ? nsteps - 1 - st : NS - 2;
-      wait_vmcnt(ahead * TG::loads_per_wave);
+      const bool two = st + 1 < nsteps;
+      wait_vmcnt(0);
       __syncthreads();
-      const int nxt = st + NS - 1;
-      if (nxt < nsteps)
-        issue_block_step<D>(ring[(r + NS - 1) % NS], a, it, ptab, lead, p0n, nxt, s0_steps, h, wave, lane);
-      if (nb > 0) extend_step<D, QBW>(ws, ring[r], qf, lim, lim_lo, step_pos(it, st, s0_steps), lane, a.scale_log2);
+      if (st + 2 < nsteps)
+        issue_block_step<D>(ring[(2 * k + 2) % NS], a, it, ptab, lead, p0n, st + 2, s0_steps, h, wave, lane);
+      if (st + 3 < nsteps)
+        issue_block_step<D>(ring[(2 * k + 3) % NS], a, it, ptab, lead, p0n, st + 3, s0_steps, h, wave, lane);
+      if (nb > 0) {
+        // An odd last step pairs with an empty one (no visible key: all its
+        // scores -inf, its V zeroed; its stage is not being refilled).
+        const StepPos q0 = step_pos(it, st, s0_steps);
+        const StepPos q1 = two ? step_pos(it, st + 1, s0_steps) : StepPos{q0.list_off, q0.kend, q0.kend, q0.seg};
+        extend_pair<D, QBW>(ws, ring[2 * k], ring[2 * k + 1], qf, lim, lim_lo, q0, q1, lane, a.scale_log2);
+      }
     }
   }
 #pragma unroll
