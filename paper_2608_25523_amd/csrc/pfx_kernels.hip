@@ -83,11 +83,11 @@ __device__ __forceinline__ void row_swap32(uint32_t& a, uint32_t& b) {
 __device__ __forceinline__ float column_max(float x) {
   uint32_t a = __builtin_bit_cast(uint32_t, x), b = a;
   row_swap16(a, b);
-  x = fmaxf(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b));
+  x = __builtin_elementwise_maximum(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b));
   a = __builtin_bit_cast(uint32_t, x);
   b = a;
   row_swap32(a, b);
-  return fmaxf(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b));
+  return __builtin_elementwise_maximum(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b));
 }
 __device__ __forceinline__ float column_sum(float x) {
   uint32_t a = __builtin_bit_cast(uint32_t, x), b = a;
@@ -367,7 +367,14 @@ __device__ __forceinline__ void attend_step(WaveState<D, QB>& ws, const unsigned
           if (key >= kend || (causal && key > lim[b])) v[4 * t + i] = -INFINITY;
         }
     }
-    float mx = fmaxf(fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])), fmaxf(fmaxf(v[4], v[5]), fmaxf(v[6], v[7])));
+    float x[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = v[i];
+#pragma unroll
+    for (int w = 4; w >= 1; w /= 2)
+#pragma unroll
+      for (int i = 0; i < w; ++i) x[i] = __builtin_elementwise_maximum(x[i], x[i + w]);
+    float mx = x[0];  // IEEE maximum: no NaN canonicalisation of the MFMA results
     // The cross-lane max is needed only when some lane passes m + slack.
     if (__any(mx * scale_log2 > ws.m[b] + kRescaleSlack)) {
       PFX_KEEP_BRANCH();
@@ -486,11 +493,20 @@ __device__ __forceinline__ void extend_pair(WaveState<D, QB>& ws, const unsigned
   bool pass = false;
 #pragma unroll
   for (int b = 0; b < QB; ++b) {
-    float m0 = fmaxf(fmaxf(fmaxf(sc[0][b][0][0], sc[0][b][0][1]), fmaxf(sc[0][b][0][2], sc[0][b][0][3])),
-                     fmaxf(fmaxf(sc[0][b][1][0], sc[0][b][1][1]), fmaxf(sc[0][b][1][2], sc[0][b][1][3])));
-    float m1 = fmaxf(fmaxf(fmaxf(sc[1][b][0][0], sc[1][b][0][1]), fmaxf(sc[1][b][0][2], sc[1][b][0][3])),
-                     fmaxf(fmaxf(sc[1][b][1][0], sc[1][b][1][1]), fmaxf(sc[1][b][1][2], sc[1][b][1][3])));
-    mx[b] = fmaxf(m0, m1);
+    // IEEE maximum (NaN-propagating, gfx950 v_maximum3_f32): fmaxf would put a
+    // NaN canonicalisation in front of every MFMA result it reads.
+    float x[16];
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) x[8 * u + 4 * t + i] = sc[u][b][t][i];
+#pragma unroll
+    for (int w = 8; w >= 1; w /= 2)
+#pragma unroll
+      for (int i = 0; i < w; ++i) x[i] = __builtin_elementwise_maximum(x[i], x[i + w]);
+    mx[b] = x[0];
     pass = pass || mx[b] * scale_log2 > ws.m[b] + kRescaleSlack;  // scale > 0
   }
   if (__any(pass)) {
