@@ -228,6 +228,21 @@ __device__ __forceinline__ int row_key(int t) {
 template <int chunks>
 __device__ __forceinline__ int swizzled_slot(int t, int c) { return t * chunks + (c ^ row_key<chunks>(t)); }
 
+// Byte offsets, within a (page, KV head) block, of the chunk that this lane
+// copies into slot 64 j + lane of the swizzled layout, less 1024 j (slot
+// 64 j + lane is row t = 64 j / chunks + lane / chunks, so the rows of copy j
+// start 1024 j bytes in).
+template <int D>
+__device__ __forceinline__ void block_lane_offsets(uint32_t (&off)[TileGeom<D>::loads_per_wave], int lane) {
+  using TG = TileGeom<D>;
+#pragma unroll
+  for (int j = 0; j < TG::loads_per_wave; ++j) {
+    const int t = (64 * j + lane) / TG::chunks;
+    const int c = (lane % TG::chunks) ^ row_key<TG::chunks>(t);
+    off[j] = uint32_t(2 * (t * D + 8 * c) - 1024 * j);
+  }
+}
+
 // Wait until at most n of this wave's vector-memory operations are pending.
 __device__ __forceinline__ void wait_vmcnt(int n) {
   // s_waitcnt encoding on gfx9: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] at [15:14].
@@ -285,6 +300,39 @@ __device__ __forceinline__ void copy16_to_lds(const void* src, uint32_t lds_addr
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds_addr) : "memory", "m0");
 }
 #pragma clang diagnostic pop
+
+// Copy one wave's share of a (page, KV head) block, L KiB, into LDS at
+// lds_addr: copy j reads base + off[j] + 1024 j and writes
+// lds_addr + 1024 j + 16 * lane.  The base is wave-uniform and goes in
+// SGPRs; the instruction offset 1024 j moves both the global and the LDS
+// address, so one M0 serves all L copies and the lane offsets are computed
+// once per block.
+template <int L>
+__device__ __forceinline__ void copy_block_to_lds(const void* base, const uint32_t (&off)[L], uint32_t lds_addr) {
+  static_assert(L == 2 || L == 4, "a block is 2 or 4 KiB");
+  const uint64_t b = reinterpret_cast<uintptr_t>(base);
+  // readfirstlane yields an int: take each half as unsigned before joining.
+  const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(uint32_t(b))));
+  const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(uint32_t(b >> 32))));
+  const uint64_t sb = (uint64_t(hi) << 32) | lo;
+  const uint32_t m = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(lds_addr)));
+  if constexpr (L == 4)
+    asm volatile(
+        "s_mov_b32 m0, %1\n\t"
+        "global_load_lds_dwordx4 %2, %0\n\t"
+        "global_load_lds_dwordx4 %3, %0 offset:1024\n\t"
+        "global_load_lds_dwordx4 %4, %0 offset:2048\n\t"
+        "global_load_lds_dwordx4 %5, %0 offset:3072" ::"s"(sb),
+        "s"(m), "v"(off[0]), "v"(off[1]), "v"(off[2]), "v"(off[3])
+        : "memory", "m0");
+  else
+    asm volatile(
+        "s_mov_b32 m0, %1\n\t"
+        "global_load_lds_dwordx4 %2, %0\n\t"
+        "global_load_lds_dwordx4 %3, %0 offset:1024" ::"s"(sb),
+        "s"(m), "v"(off[0]), "v"(off[1])
+        : "memory", "m0");
+}
 
 __device__ __forceinline__ uint32_t lds_address(const unsigned char* p) {
   return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_bytes)(p)));
@@ -599,7 +647,7 @@ __device__ __forceinline__ void write_rows(const AttnArgs& a, const f32x4 (&acc)
 template <int D>
 __device__ __forceinline__ void issue_block_step(unsigned char* stage, const AttnArgs& a, const Item& it,
                                                  const int* ptab, int lead, int p0n, int st, int s0_steps, int h,
-                                                 int wave, int lane) {
+                                                 int wave, const uint32_t (&voff)[TileGeom<D>::loads_per_wave]) {
   using TG = TileGeom<D>;
   const StepPos p = step_pos(it, st, s0_steps);
   const int t = wave & 1;
@@ -608,16 +656,9 @@ __device__ __forceinline__ void issue_block_step(unsigned char* stage, const Att
   int idx = (p.seg == 0 ? 0 : p0n) + ((p.k0 - seg_base) >> 4);
   if (t == 1 && p.k0 + 16 < p.kend) idx += 1;  // a missing second page re-reads the first (masked later)
   // The block's leading page ids sit one per lane in `lead`; later ones in the LDS table.
-  const int page = idx < kItemPages ? __builtin_amdgcn_readlane(lead, idx) : ptab[idx];
+  const int page = __builtin_amdgcn_readfirstlane(idx < kItemPages ? __builtin_amdgcn_readlane(lead, idx) : ptab[idx]);
   const uint16_t* base = (is_v ? a.vpool : a.kpool) + (size_t(page) * a.hkv + h) * (16 * D);
-  const uint32_t dst = lds_address(stage) + wave * TG::page_bytes;
-#pragma unroll
-  for (int j = 0; j < TG::loads_per_wave; ++j) {
-    const int q = 64 * j + lane;
-    const int tt = q / TG::chunks;
-    const int cc = (q % TG::chunks) ^ row_key<TG::chunks>(tt);
-    copy16_to_lds(base + tt * D + cc * 8, dst + 1024 * j);
-  }
+  copy_block_to_lds(base, voff, lds_address(stage) + wave * TG::page_bytes);
 }
 
 // LDS bytes of an extend block: the ring, then the page table.
@@ -685,10 +726,12 @@ __device__ __forceinline__ void extend_block(const AttnArgs& a, const Item* itp,
   const int s0_steps = (it.s0_kend - it.s0_kbeg + kStepKeys - 1) / kStepKeys;
   const int s1_steps = (it.s1_kend - it.s1_kbeg + kStepKeys - 1) / kStepKeys;
   const int nsteps = s0_steps + s1_steps;
+  uint32_t voff[TG::loads_per_wave];
+  block_lane_offsets<D>(voff, lane);
   // The first steps' pages are among the leading ids: request them before
   // waiting for the page table.
   for (int st = 0; st < 2 && st < nsteps; ++st)
-    issue_block_step<D>(ring[st], a, it, ptab, lead, p0n, st, s0_steps, h, wave, lane);
+    issue_block_step<D>(ring[st], a, it, ptab, lead, p0n, st, s0_steps, h, wave, voff);
   __syncthreads();  // page table ready
   // Two steps per barrier: at pair q (steps 2q, 2q + 1) wait for both
   // stages, meet (so the stages of the previous pair are free), refill them
@@ -705,9 +748,9 @@ __device__ __forceinline__ void extend_block(const AttnArgs& a, const Item* itp,
       wait_vmcnt(0);
       __syncthreads();
       if (st + 2 < nsteps)
-        issue_block_step<D>(ring[(2 * k + 2) % NS], a, it, ptab, lead, p0n, st + 2, s0_steps, h, wave, lane);
+        issue_block_step<D>(ring[(2 * k + 2) % NS], a, it, ptab, lead, p0n, st + 2, s0_steps, h, wave, voff);
       if (st + 3 < nsteps)
-        issue_block_step<D>(ring[(2 * k + 3) % NS], a, it, ptab, lead, p0n, st + 3, s0_steps, h, wave, lane);
+        issue_block_step<D>(ring[(2 * k + 3) % NS], a, it, ptab, lead, p0n, st + 3, s0_steps, h, wave, voff);
       if (nb > 0) {
         // An odd last step pairs with an empty one (no visible key: all its
         // scores -inf, its V zeroed; its stage is not being refilled).
@@ -763,20 +806,15 @@ __device__ __forceinline__ int piece_window(const Seg& sg, int wave, int lane) {
 // returns how many copies it issued (a wave with no columns copies no Q).
 template <int D>
 __device__ __forceinline__ int issue_piece_stage(unsigned char* stage, const AttnArgs& a, const Seg& sg, int win,
-                                                 int k, int ncols, int qh0, int wave, int lane) {
+                                                 int k, int ncols, int qh0, int wave, int lane,
+                                                 const uint32_t (&voff)[TileGeom<D>::loads_per_wave]) {
   using TG = TileGeom<D>;
   const uint32_t dst = lds_address(stage) + wave * TG::page_bytes;
   if (k >= 0) {
     // K/V: tile (wave & 1) of K (waves 0, 1) or V (waves 2, 3), swizzled.
     const int blk = __builtin_amdgcn_readlane(win, k);
     const uint16_t* base = ((wave >> 1) ? a.vpool : a.kpool) + size_t(blk) * (16 * D);
-#pragma unroll
-    for (int j = 0; j < TG::loads_per_wave; ++j) {
-      const int q = 64 * j + lane;
-      const int tt = q / TG::chunks;
-      const int cc = (q % TG::chunks) ^ row_key<TG::chunks>(tt);
-      copy16_to_lds(base + tt * D + cc * 8, dst + 1024 * j);
-    }
+    copy_block_to_lds(base, voff, dst);
     return TG::loads_per_wave;
   }
   // Q: chunk (p % chunks) of this wave's column p / chunks at 16 p; padding
@@ -821,6 +859,8 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
   }
   __syncthreads();
 
+  uint32_t voff[TG::loads_per_wave];
+  block_lane_offsets<D>(voff, lane);
   // Issue side: piece iord of the list, its next stage ik (-1: Q), and what
   // the issue needs of it.
   int iord = 0, ik = -1, inst = 0, incols = 0, iqh0 = 0, iwin = 0;
@@ -850,7 +890,7 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
     }
     if (in_piece) {
       const int q = iord % K;
-      n_ops = issue_piece_stage<D>(ring[r], a, slots[q], iwin, ik, incols, iqh0, wave, lane);
+      n_ops = issue_piece_stage<D>(ring[r], a, slots[q], iwin, ik, incols, iqh0, wave, lane, voff);
       if (ik < 0 && wave == 0) {
         // The descriptor two pieces ahead, into the slot of the piece two back.
         const int nxt = piece_of(b, iord + 2, S);
