@@ -299,7 +299,6 @@ typedef __attribute__((address_space(3))) unsigned char* lds_bytes;
 __device__ __forceinline__ void copy16_to_lds(const void* src, uint32_t lds_addr) {
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds_addr) : "memory", "m0");
 }
-#pragma clang diagnostic pop
 
 // Copy one wave's share of a (page, KV head) block, L KiB, into LDS at
 // lds_addr: copy j reads base + off[j] + 1024 j and writes
@@ -333,6 +332,7 @@ __device__ __forceinline__ void copy_block_to_lds(const void* base, const uint32
         "s"(m), "v"(off[0]), "v"(off[1])
         : "memory", "m0");
 }
+#pragma clang diagnostic pop
 
 __device__ __forceinline__ uint32_t lds_address(const unsigned char* p) {
   return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_bytes)(p)));
@@ -348,11 +348,9 @@ typedef __attribute__((address_space(3))) s16x4* lds_s16x4;
 // that instruction hands output lane i element e of what input lane
 // 4 e + i / 4 addressed, element i % 4; so lane 4 e + q addresses key
 // 4 grp + e, dims 16 blk + 4 q .. + 3, and lane i receives dim 16 blk + i
-// of the four keys.  Elements of keys at or past kend are zeroed (their
-// slots may hold anything, and 0 * NaN is NaN).
+// of the four keys.
 template <int D>
-__device__ __forceinline__ bf16x8 v_operand_tr(const unsigned char* v0, const unsigned char* v1, int blk, int lane,
-                                               uint64_t keep0, uint64_t keep1) {
+__device__ __forceinline__ bf16x8 v_operand_tr(const unsigned char* v0, const unsigned char* v1, int blk, int lane) {
   constexpr int chunks = D / 8;
   const int s = lane & 15;
   const int row = 4 * (lane >> 4) + (s >> 2);
@@ -360,10 +358,32 @@ __device__ __forceinline__ bf16x8 v_operand_tr(const unsigned char* v0, const un
   const int off = 16 * swizzled_slot<chunks>(row, 2 * blk + (q >> 1)) + 8 * (q & 1);
   const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(v0 + off));
   const s16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(v1 + off));
-  const uint64_t ua = __builtin_bit_cast(uint64_t, a) & keep0;
-  const uint64_t ub = __builtin_bit_cast(uint64_t, b) & keep1;
+  const uint64_t ua = __builtin_bit_cast(uint64_t, a);
+  const uint64_t ub = __builtin_bit_cast(uint64_t, b);
   u32x4 w = {uint32_t(ua), uint32_t(ua >> 32), uint32_t(ub), uint32_t(ub >> 32)};
   return __builtin_bit_cast(bf16x8, w);
+}
+
+// Zero, in a step's V^T operands, the keys at or past kend (their slots may
+// hold anything, and 0 * NaN is NaN).  Element e of each half of an operand
+// is key k0 + 16 t + 4 grp + e.
+template <int D>
+__device__ __forceinline__ void zero_v_tail(bf16x8 (&vop)[D / 16], int k0, int kend, int grp) {
+  uint32_t keep[2][2] = {{~0u, ~0u}, {~0u, ~0u}};
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (k0 + 16 * t + 4 * grp + e >= kend) keep[t][e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
+#pragma unroll
+  for (int blk = 0; blk < D / 16; ++blk) {
+    u32x4 w = __builtin_bit_cast(u32x4, vop[blk]);
+    w[0] &= keep[0][0];
+    w[1] &= keep[0][1];
+    w[2] &= keep[1][0];
+    w[3] &= keep[1][1];
+    vop[blk] = __builtin_bit_cast(bf16x8, w);
+  }
 }
 
 // One 32-key step (two 16-key pages staged in LDS: K tile 0, K tile 1,
@@ -442,25 +462,20 @@ __device__ __forceinline__ void attend_step(WaveState<D, QB>& ws, const unsigned
     u32x4 pw = {pack_bf16(pr[0], pr[1]), pack_bf16(pr[2], pr[3]), pack_bf16(pr[4], pr[5]), pack_bf16(pr[6], pr[7])};
     pb[b] = __builtin_bit_cast(bf16x8, pw);
   }
-  uint64_t keep0 = ~uint64_t(0), keep1 = ~uint64_t(0);
-  if (tail) {
-    // Element e of a lane's V quarter is key 16 t + 4 grp + e.
-    PFX_KEEP_BRANCH();
+  bf16x8 vop[CH];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      if (k0 + 4 * grp + e >= kend) keep0 &= ~(uint64_t(0xFFFF) << (16 * e));
-      if (k0 + 16 + 4 * grp + e >= kend) keep1 &= ~(uint64_t(0xFFFF) << (16 * e));
-    }
+  for (int blk = 0; blk < CH; ++blk)
+    vop[blk] = v_operand_tr<D>(stage + 2 * TG::page_bytes, stage + 3 * TG::page_bytes, blk, lane);
+  if (tail) {
+    PFX_KEEP_BRANCH();
+    zero_v_tail<D>(vop, k0, kend, grp);
   }
-  const unsigned char* v0 = stage + 2 * TG::page_bytes;
-  const unsigned char* v1 = stage + 3 * TG::page_bytes;
 #pragma unroll
   for (int blk = 0; blk < CH; ++blk) {
-    const bf16x8 op = v_operand_tr<D>(v0, v1, blk, lane, keep0, keep1);
 #pragma unroll
     for (int b = 0; b < QB; ++b) {
       if (b >= nblk) break;
-      ws.acc[b][blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(op, pb[b], ws.acc[b][blk], 0, 0, 0);
+      ws.acc[b][blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop[blk], pb[b], ws.acc[b][blk], 0, 0, 0);
     }
   }
   // Row sums of P on the matrix unit (row 0 of the A operand is ones).
@@ -580,27 +595,10 @@ __device__ __forceinline__ void extend_pair(WaveState<D, QB>& ws, const unsigned
     bf16x8 vop[CH];
 #pragma unroll
     for (int blk = 0; blk < CH; ++blk)
-      vop[blk] = v_operand_tr<D>(stage + 2 * TG::page_bytes, stage + 3 * TG::page_bytes, blk, lane, ~uint64_t(0),
-                                 ~uint64_t(0));
+      vop[blk] = v_operand_tr<D>(stage + 2 * TG::page_bytes, stage + 3 * TG::page_bytes, blk, lane);
     if (p.k0 + kStepKeys > p.kend) {
-      // Keys past the end of the segment: zero their V (the slots may hold
-      // anything).  Element e of each half of an operand is key 16 t + 4 grp + e.
       PFX_KEEP_BRANCH();
-      uint32_t keep[2][2] = {{~0u, ~0u}, {~0u, ~0u}};
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (p.k0 + 16 * t + 4 * grp + e >= p.kend) keep[t][e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
-#pragma unroll
-      for (int blk = 0; blk < CH; ++blk) {
-        u32x4 w = __builtin_bit_cast(u32x4, vop[blk]);
-        w[0] &= keep[0][0];
-        w[1] &= keep[0][1];
-        w[2] &= keep[1][0];
-        w[3] &= keep[1][1];
-        vop[blk] = __builtin_bit_cast(bf16x8, w);
-      }
+      zero_v_tail<D>(vop, p.k0, p.kend, grp);
     }
 #pragma unroll
     for (int b = 0; b < QB; ++b) {
@@ -919,59 +917,64 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
   int lim[1] = {0};
   int orow = 0, k0 = 0, kend = 0, causal = 0, cnst = 0;
   bool has_cols = false, valid = false;
-  for (int u = 0; !(ended && pending == 0); ++u) {
-    // Stage u: only the copies of the issue opportunities after it (the
-    // newest NS - 2 entries of ops) may still be pending.
-    int later = 0;
+  // Unrolled over the ring, so that every stage's LDS addresses are a lane
+  // offset plus an immediate.
+  while (!(ended && pending == 0)) {
 #pragma unroll
-    for (int i = 0; i < NS - 2; ++i) later += (ops >> (8 * i)) & 0xFFu;
-    wait_vmcnt(later);
-    __syncthreads();
-    issue_next((u + NS - 1) % NS);
+    for (int r = 0; r < NS; ++r) {
+      if (ended && pending == 0) break;
+      // Stage in ring slot r: only the copies of the issue opportunities after it (the
+      // newest NS - 2 entries of ops) may still be pending.
+      int later = 0;
+#pragma unroll
+      for (int i = 0; i < NS - 2; ++i) later += (ops >> (8 * i)) & 0xFFu;
+      wait_vmcnt(later);
+      __syncthreads();
+      issue_next((r + NS - 1) % NS);
 
-    const int r = u % NS;
-    const uint32_t code = (ent >> (8 * r)) & 0xFFu;
-    const unsigned char* stage = ring[r];
-    if (code & 0x80u) {
-      --pending;
-      const Seg& sg = slots[(code >> 5) & 3u];
-      const int k = int(code & 31u) - 1;
-      if (k < 0) {
-        // A piece starts: its columns, limits, output rows and Q.
-        const i32x4 h0 = *reinterpret_cast<const i32x4*>(&sg.h);       // kind, kv_head, ncols, nsteps
-        const i32x4 h1 = *reinterpret_cast<const i32x4*>(&sg.h.k0);    // k0, kend, causal_base, slot
-        const i32x4 h2 = *reinterpret_cast<const i32x4*>(&sg.h.item);  // item, piece, causal, -
-        const int ncols = __builtin_amdgcn_readfirstlane(h0[2]);
-        cnst = __builtin_amdgcn_readfirstlane(h0[3]);
-        k0 = __builtin_amdgcn_readfirstlane(h1[0]);
-        kend = __builtin_amdgcn_readfirstlane(h1[1]);
-        causal = __builtin_amdgcn_readfirstlane(h2[2]);
-        has_cols = 16 * wave < ncols;
-        const int c = 16 * wave + col;
-        valid = c < ncols;
-        const int j = valid ? c >> a.group_shift : 0;
-        const int tok = sg.tok[j];
-        lim[0] = causal ? tok + __builtin_amdgcn_readfirstlane(h1[2]) : 0x7fffffff;
-        orow = sg.out[j] + (c & (a.group - 1));
-        if (has_cols) {
-          const unsigned char* qb = stage + wave * TG::page_bytes;
+      const uint32_t code = (ent >> (8 * r)) & 0xFFu;
+      const unsigned char* stage = ring[r];
+      if (code & 0x80u) {
+        --pending;
+        const Seg& sg = slots[(code >> 5) & 3u];
+        const int k = int(code & 31u) - 1;
+        if (k < 0) {
+          // A piece starts: its columns, limits, output rows and Q.
+          const i32x4 h0 = *reinterpret_cast<const i32x4*>(&sg.h);       // kind, kv_head, ncols, nsteps
+          const i32x4 h1 = *reinterpret_cast<const i32x4*>(&sg.h.k0);    // k0, kend, causal_base, slot
+          const i32x4 h2 = *reinterpret_cast<const i32x4*>(&sg.h.item);  // item, piece, causal, -
+          const int ncols = __builtin_amdgcn_readfirstlane(h0[2]);
+          cnst = __builtin_amdgcn_readfirstlane(h0[3]);
+          k0 = __builtin_amdgcn_readfirstlane(h1[0]);
+          kend = __builtin_amdgcn_readfirstlane(h1[1]);
+          causal = __builtin_amdgcn_readfirstlane(h2[2]);
+          has_cols = 16 * wave < ncols;
+          const int c = 16 * wave + col;
+          valid = c < ncols;
+          const int j = valid ? c >> a.group_shift : 0;
+          const int tok = sg.tok[j];
+          lim[0] = causal ? tok + __builtin_amdgcn_readfirstlane(h1[2]) : 0x7fffffff;
+          orow = sg.out[j] + (c & (a.group - 1));
+          if (has_cols) {
+            const unsigned char* qb = stage + wave * TG::page_bytes;
 #pragma unroll
-          for (int s = 0; s < KS; ++s)
-            qf[0][s] = *reinterpret_cast<const bf16x8*>(qb + 16 * (col * TG::chunks + 4 * s + grp));
-        }
-      } else if (has_cols) {
-        attend_step<D, 1>(ws, stage, qf, lim, k0 + kStepKeys * k, kend, causal != 0, 1, lane, a.scale_log2);
-        if (k == cnst - 1) {
-          // The piece's state goes out as it stands: accumulators in their
-          // register order (group, block, element), (m, l) once per column.
-          const float l = ws.lv[0][0];  // the whole column sum in the group-0 lanes
-          if (valid) {
-            float* out = a.plan.o_part + size_t(orow) * D + grp * (4 * CH);
-#pragma unroll
-            for (int jj = 0; jj < CH; ++jj) *reinterpret_cast<f32x4*>(out + 4 * jj) = ws.acc[0][jj];
-            if (grp == 0) *reinterpret_cast<f32x2*>(a.plan.l_part + 2 * size_t(orow)) = f32x2{ws.m[0], l};
+            for (int s = 0; s < KS; ++s)
+              qf[0][s] = *reinterpret_cast<const bf16x8*>(qb + 16 * (col * TG::chunks + 4 * s + grp));
           }
-          reset_state(ws);
+        } else if (has_cols) {
+          attend_step<D, 1>(ws, stage, qf, lim, k0 + kStepKeys * k, kend, causal != 0, 1, lane, a.scale_log2);
+          if (k == cnst - 1) {
+            // The piece's state goes out as it stands: accumulators in their
+            // register order (group, block, element), (m, l) once per column.
+            const float l = ws.lv[0][0];  // the whole column sum in the group-0 lanes
+            if (valid) {
+              float* out = a.plan.o_part + size_t(orow) * D + grp * (4 * CH);
+#pragma unroll
+              for (int jj = 0; jj < CH; ++jj) *reinterpret_cast<f32x4*>(out + 4 * jj) = ws.acc[0][jj];
+              if (grp == 0) *reinterpret_cast<f32x2*>(a.plan.l_part + 2 * size_t(orow)) = f32x2{ws.m[0], l};
+            }
+            reset_state(ws);
+          }
         }
       }
     }
