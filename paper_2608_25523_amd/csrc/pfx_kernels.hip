@@ -135,6 +135,38 @@ __device__ __forceinline__ StepPos step_pos(const Item& it, int st, int s0_steps
   return p;
 }
 
+// The steps of an extend block where the common path changes, found once
+// per block so that an ordinary step needs no position arithmetic:
+//   tail0, tail1: the last step of segment 0 / 1 when the segment ends
+//     inside it (keys to mask, V to zero), else -1;
+//   half0, half1: such a step when its second page does not exist, else -1;
+//   diag: the first suffix step with a key past the wave's lowest limit
+//     (from there on every suffix step is masked);
+//   d1: page-table index of step st's first page is 2 st, plus d1 in
+//     segment 1.
+struct StepMarks {
+  int32_t s0_steps, nsteps, d1, tail0, tail1, half0, half1, diag;
+};
+
+__device__ __forceinline__ StepMarks step_marks(const Item& it, int p0n, int lim_lo) {
+  StepMarks mk;
+  const int s0_steps = (it.s0_kend - it.s0_kbeg + kStepKeys - 1) / kStepKeys;
+  const int s1_steps = (it.s1_kend - it.s1_kbeg + kStepKeys - 1) / kStepKeys;
+  mk.s0_steps = s0_steps;
+  mk.nsteps = s0_steps + s1_steps;
+  mk.d1 = p0n - 2 * s0_steps;
+  const int last0 = it.s0_kbeg + kStepKeys * (s0_steps - 1);  // first key of segment 0's last step
+  const int last1 = it.s1_kbeg + kStepKeys * (s1_steps - 1);
+  mk.tail0 = s0_steps > 0 && last0 + kStepKeys > it.s0_kend ? s0_steps - 1 : -1;
+  mk.half0 = s0_steps > 0 && last0 + 16 >= it.s0_kend ? s0_steps - 1 : -1;
+  mk.tail1 = s1_steps > 0 && last1 + kStepKeys > it.s1_kend ? mk.nsteps - 1 : -1;
+  mk.half1 = s1_steps > 0 && last1 + 16 >= it.s1_kend ? mk.nsteps - 1 : -1;
+  // Suffix step j is masked once its last key s1_kbeg + 32 j + 31 passes lim_lo.
+  const int x = lim_lo - it.s1_kbeg - (kStepKeys - 1);
+  mk.diag = s1_steps == 0 ? 0x7fffffff : s0_steps + (x < 0 ? 0 : x / kStepKeys + 1);
+  return mk;
+}
+
 template <int D, int QB>
 struct WaveState {
   static constexpr int CH = D / 16;
@@ -505,8 +537,8 @@ __device__ __forceinline__ void attend_step(WaveState<D, QB>& ws, const unsigned
 template <int D, int QB>
 __device__ __forceinline__ void extend_pair(WaveState<D, QB>& ws, const unsigned char* st0,
                                             const unsigned char* st1, const bf16x8 (&qf)[QB][D / 32],
-                                            const int (&lim)[QB], int lim_lo, const StepPos& p0, const StepPos& p1,
-                                            int lane, float scale_log2) {
+                                            const int (&lim)[QB], const Item& it, int st, bool two,
+                                            const StepMarks& mk, int lane, float scale_log2) {
   using TG = TileGeom<D>;
   constexpr int KS = D / 32;
   constexpr int CH = D / 16;
@@ -532,13 +564,14 @@ __device__ __forceinline__ void extend_pair(WaveState<D, QB>& ws, const unsigned
       }
     }
   }
-  const bool tail0 = p0.k0 + kStepKeys > p0.kend, tail1 = p1.k0 + kStepKeys > p1.kend;
-  if (tail0 || tail1 || (p0.seg == 1 && p0.k0 + kStepKeys - 1 > lim_lo) ||
-      (p1.seg == 1 && p1.k0 + kStepKeys - 1 > lim_lo)) {
+  // An odd last step pairs with an empty one (no visible key: all its scores
+  // -inf, its V zeroed).
+  if (!two || st + 1 >= mk.diag || st == mk.tail0 || st + 1 == mk.tail0 || st == mk.tail1 || st + 1 == mk.tail1) {
     PFX_KEEP_BRANCH();
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      const StepPos& p = u ? p1 : p0;
+      StepPos p = step_pos(it, st, mk.s0_steps);
+      if (u) p = two ? step_pos(it, st + 1, mk.s0_steps) : StepPos{p.list_off, p.kend, p.kend, p.seg};
 #pragma unroll
       for (int b = 0; b < QB; ++b) {
         const int lim_b = p.seg == 1 ? lim[b] : 0x7fffffff;
@@ -590,14 +623,14 @@ __device__ __forceinline__ void extend_pair(WaveState<D, QB>& ws, const unsigned
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
     const unsigned char* stage = u ? st1 : st0;
-    const StepPos& p = u ? p1 : p0;
     if (u) asm volatile("" ::: "memory");  // the second step's V reads stay after the first step's products
     bf16x8 vop[CH];
 #pragma unroll
     for (int blk = 0; blk < CH; ++blk)
       vop[blk] = v_operand_tr<D>(stage + 2 * TG::page_bytes, stage + 3 * TG::page_bytes, blk, lane);
-    if (p.k0 + kStepKeys > p.kend) {
+    if ((u == 1 && !two) || st + u == mk.tail0 || st + u == mk.tail1) {
       PFX_KEEP_BRANCH();
+      const StepPos p = u == 1 && !two ? StepPos{0, 0, 0, 0} : step_pos(it, st + u, mk.s0_steps);
       zero_v_tail<D>(vop, p.k0, p.kend, grp);
     }
 #pragma unroll
@@ -644,15 +677,13 @@ __device__ __forceinline__ void write_rows(const AttnArgs& a, const f32x4 (&acc)
 // tile (wave & 1) of K (waves 0, 1) or of V (waves 2, 3).
 template <int D>
 __device__ __forceinline__ void issue_block_step(unsigned char* stage, const AttnArgs& a, const Item& it,
-                                                 const int* ptab, int lead, int p0n, int st, int s0_steps, int h,
+                                                 const int* ptab, int lead, const StepMarks& mk, int st, int h,
                                                  int wave, const uint32_t (&voff)[TileGeom<D>::loads_per_wave]) {
   using TG = TileGeom<D>;
-  const StepPos p = step_pos(it, st, s0_steps);
   const int t = wave & 1;
   const bool is_v = wave >> 1;
-  const int seg_base = p.seg == 0 ? it.s0_kbeg : it.s1_kbeg;
-  int idx = (p.seg == 0 ? 0 : p0n) + ((p.k0 - seg_base) >> 4);
-  if (t == 1 && p.k0 + 16 < p.kend) idx += 1;  // a missing second page re-reads the first (masked later)
+  int idx = 2 * st + t + (st >= mk.s0_steps ? mk.d1 : 0);
+  if (t == 1 && (st == mk.half0 || st == mk.half1)) idx -= 1;  // a missing second page re-reads the first (masked later)
   // The block's leading page ids sit one per lane in `lead`; later ones in the LDS table.
   const int page = __builtin_amdgcn_readfirstlane(idx < kItemPages ? __builtin_amdgcn_readlane(lead, idx) : ptab[idx]);
   const uint16_t* base = (is_v ? a.vpool : a.kpool) + (size_t(page) * a.hkv + h) * (16 * D);
@@ -721,15 +752,14 @@ __device__ __forceinline__ void extend_block(const AttnArgs& a, const Item* itp,
   const int lim_lo = __builtin_amdgcn_readfirstlane(lim[0]);
   WaveState<D, QBW> ws;
   reset_state(ws);
-  const int s0_steps = (it.s0_kend - it.s0_kbeg + kStepKeys - 1) / kStepKeys;
-  const int s1_steps = (it.s1_kend - it.s1_kbeg + kStepKeys - 1) / kStepKeys;
-  const int nsteps = s0_steps + s1_steps;
+  const StepMarks mk = step_marks(it, p0n, lim_lo);
+  const int nsteps = mk.nsteps;
   uint32_t voff[TG::loads_per_wave];
   block_lane_offsets<D>(voff, lane);
   // The first steps' pages are among the leading ids: request them before
   // waiting for the page table.
   for (int st = 0; st < 2 && st < nsteps; ++st)
-    issue_block_step<D>(ring[st], a, it, ptab, lead, p0n, st, s0_steps, h, wave, voff);
+    issue_block_step<D>(ring[st], a, it, ptab, lead, mk, st, h, wave, voff);
   __syncthreads();  // page table ready
   // Two steps per barrier: at pair q (steps 2q, 2q + 1) wait for both
   // stages, meet (so the stages of the previous pair are free), refill them
@@ -746,16 +776,12 @@ __device__ __forceinline__ void extend_block(const AttnArgs& a, const Item* itp,
       wait_vmcnt(0);
       __syncthreads();
       if (st + 2 < nsteps)
-        issue_block_step<D>(ring[(2 * k + 2) % NS], a, it, ptab, lead, p0n, st + 2, s0_steps, h, wave, voff);
+        issue_block_step<D>(ring[(2 * k + 2) % NS], a, it, ptab, lead, mk, st + 2, h, wave, voff);
       if (st + 3 < nsteps)
-        issue_block_step<D>(ring[(2 * k + 3) % NS], a, it, ptab, lead, p0n, st + 3, s0_steps, h, wave, voff);
-      if (nb > 0) {
-        // An odd last step pairs with an empty one (no visible key: all its
-        // scores -inf, its V zeroed; its stage is not being refilled).
-        const StepPos q0 = step_pos(it, st, s0_steps);
-        const StepPos q1 = two ? step_pos(it, st + 1, s0_steps) : StepPos{q0.list_off, q0.kend, q0.kend, q0.seg};
-        extend_pair<D, QBW>(ws, ring[2 * k], ring[2 * k + 1], qf, lim, lim_lo, q0, q1, lane, a.scale_log2);
-      }
+        issue_block_step<D>(ring[(2 * k + 3) % NS], a, it, ptab, lead, mk, st + 3, h, wave, voff);
+      // An odd last step pairs with an empty one (its stage is not being
+      // refilled).
+      if (nb > 0) extend_pair<D, QBW>(ws, ring[2 * k], ring[2 * k + 1], qf, lim, it, st, two, mk, lane, a.scale_log2);
     }
   }
 #pragma unroll
