@@ -223,6 +223,37 @@ def copy_calibration(torch, B):
     return 2 * pages * 8 * 16 * 128 * 2
 
 
+def measured_copy_peak(torch, B, reps=10):
+    """A measured HBM ceiling beside the nominal one: pfx_page_copy of 16384
+    pages (32 KiB of K and 32 KiB of V each) device to device, in a seeded
+    random order on both sides, timed with events (each call also uploads
+    its two page-id lists); bytes read plus bytes written per second."""
+    import numpy as np
+
+    pages = 16384
+    shape = (pages, 8, 16, 128)
+    bufs = [torch.empty(shape, dtype=torch.bfloat16, device="cuda") for _ in range(4)]
+    rng = np.random.default_rng(4242)
+    src_ids = rng.permutation(pages).astype(np.int32)
+    dst_ids = rng.permutation(pages).astype(np.int32)
+    ws = torch.empty(B.pfx_page_copy_workspace_bytes(pages) + 256, dtype=torch.uint8, device="cuda")
+    src = B.make_pool(pages, 8, 128, bufs[0], bufs[1])
+    dst = B.make_pool(pages, 8, 128, bufs[2], bufs[3])
+    for _ in range(2):
+        B.pfx_page_copy(dst, src, dst_ids, src_ids, ws)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        B.pfx_page_copy(dst, src, dst_ids, src_ids, ws)
+    e1.record()
+    torch.cuda.synchronize()
+    moved = 2 * (2 * pages * 8 * 16 * 128 * 2)  # K and V, read and written
+    gbs = moved * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del bufs, ws
+    return gbs
+
+
 def traffic_from_profile(kind):
     """HBM bytes per launch from the committed counter summary, if it was
     taken with the kernel source as it is now; else None."""
@@ -264,6 +295,8 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     if args.calib_copy:
         log(f"calibration copy: {copy_calibration(torch, B)} bytes moved per launch")
+    copy_gbs = measured_copy_peak(torch, B)
+    log(f"measured device page copy: {copy_gbs:.0f} GB/s (read + write)")
     log("decode-8B: building inputs")
     dec = bench_decode(args, torch, B, RN, W)
     log(f"decode-8B: {dec['ms'] * 1e3:.1f} us/step, attention {dec['attn_ms'] * 1e3:.1f} us")
@@ -302,6 +335,8 @@ def main():
         "roofline": {"bound": "hbm", "kernel": "pfx_attention: decode_kernel + merge_rows_kernel",
                      "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic_from_profile("decode"),
+                     "measured_peak": round(copy_gbs, 1), "frac_measured": round(achieved / copy_gbs, 4),
+                     "measured_peak_kind": "pfx_page_copy device to device, random 32 KiB pages, read + write",
                      "attn_us": round(dec["attn_ms"] * 1e3, 3),
                      "attn_us_p10_p50_p90": [round(dec["spread"][k] * 1e3, 3) for k in ("p10", "p50", "p90")]},
         "graph_ms_per_step": None if dec["graph_ms"] is None else round(dec["graph_ms"], 5),
