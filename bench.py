@@ -18,7 +18,7 @@ working set exceeds the 256 MB last-level cache.
 U[256, 2048] prefilled against their agent's prefix; TFLOP/s over the
 causal-exact flop count.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-extend]
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-extend] [--more]
 """
 
 from __future__ import annotations
@@ -254,6 +254,101 @@ def measured_copy_peak(torch, B, reps=10):
     return gbs
 
 
+def events_ms(fn, n, torch, warm=3):
+    """Mean ms of n back-to-back calls of fn under one event pair."""
+    for _ in range(warm):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(n):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / n
+
+
+def bench_more(torch, B, RN, W):
+    """The other workloads, timed on request (--more): the tiny config-1
+    extend (launch-bound, reported only), config 4 (the pinned-host gather
+    of 4 evicted prefixes, then decode over all 16 agents in the 48 GiB
+    pool) and config 5 (80 layers' pools; the mixed launch, and its decode
+    and extend requests planned apart)."""
+    import dataclasses
+
+    import numpy as np
+
+    res = {}
+    b = W.config_batch(1)
+    ds = RN.DeviceStep(b, W.host_values_fast(b, 1001), poison=False)
+    res["config1_extend_attn_us"] = round(
+        events_ms(lambda: B.pfx_attention(ds.pool, ds.plan, ds.q, ds.o, ds.lse), 200, torch) * 1e3, 2)
+    del ds
+
+    b = W.config_batch(4)
+    evicted = [int(a) for a in b.meta["evicted"]]
+    ds = RN.DeviceStep(b, W.host_values_fast(b, 2004), host_resident=evicted, poison=False)
+    moved = 2 * len(ds.host_dst) * b.num_kv_heads * 16 * b.head_dim * 2
+    g_ms = events_ms(ds.gather_evicted, 5, torch, warm=1)
+    a_ms = events_ms(lambda: B.pfx_attention(ds.pool, ds.plan, ds.q, ds.o, ds.lse), 50, torch)
+    u = b.unique_kv_bytes()
+    res["config4"] = {"decode_attn_us": round(a_ms * 1e3, 2), "unique_kv_bytes": u,
+                      "decode_GBs": round(u / (a_ms * 1e-3) / 1e9, 1),
+                      "decode_frac": round(u / (a_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                      "gather_bytes": moved, "gather_ms": round(g_ms, 4),
+                      "gather_GBs_pcie_inclusive": round(moved / (g_ms * 1e-3) / 1e9, 1)}
+    del ds
+    torch.cuda.empty_cache()
+
+    b = W.config_batch(5)
+    layers = int(b.meta["layers"])
+    hkv, d, hq = b.num_kv_heads, b.head_dim, b.num_q_heads
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(50_000)
+    shape = (b.num_pages, hkv, 16, d)
+    base_k = torch.randn(shape, dtype=torch.bfloat16, device="cuda", generator=gen)
+    base_v = torch.randn(shape, dtype=torch.bfloat16, device="cuda", generator=gen)
+    pools = [B.make_pool(b.num_pages, hkv, d, torch.roll(base_k, 977 * l + 1, 0), torch.roll(base_v, 1489 * l + 3, 0))
+             for l in range(layers)]
+    del base_k, base_v
+    dec_only = dataclasses.replace(b, n_rows=np.where(b.n_rows == 1, b.n_rows, 0).astype(np.int32))
+    ext_only = dataclasses.replace(b, n_rows=np.where(b.n_rows > 1, b.n_rows, 0).astype(np.int32))
+    out5 = {"layers": layers}
+    for name, bb in (("mixed", b), ("decode", dec_only), ("extend", ext_only)):
+        t = bb.num_tokens
+        q = torch.randn((t, hq, d), dtype=torch.bfloat16, device="cuda", generator=gen)
+        o = torch.empty_like(q)
+        lse = torch.empty((t, hq), dtype=torch.float32, device="cuda")
+        plan = B.plan_from_batch(pools[0], bb, B.PFX_MODE_MIXED).upload()
+        B.pfx_attention(pools[0], plan, q, o, lse)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for l in range(layers):
+            B.pfx_attention(pools[l], plan, q, o, lse)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        rec = {"ms_80_layers": round(ms, 3)}
+        if name in ("mixed", "decode"):
+            u = dec_only.unique_kv_bytes() * layers
+            rec["decode_GBs"] = round(u / (ms * 1e-3) / 1e9, 1) if name == "decode" else None
+        if name in ("mixed", "extend"):
+            f = ext_only.attention_flops() * layers
+            rec["extend_TFs"] = round(f / (ms * 1e-3) / 1e12, 1) if name == "extend" else None
+        if name == "mixed":
+            bound = max(dec_only.unique_kv_bytes() / (HBM_PEAK_GBS * 1e9),
+                        (ext_only.attention_flops() + dec_only.attention_flops()) / (BF16_PEAK_TFLOPS * 1e12))
+            rec["peak_bound_ms_80_layers"] = round(bound * layers * 1e3, 3)
+            rec = {k: v for k, v in rec.items() if v is not None}
+        out5[name] = {k: v for k, v in rec.items() if v is not None}
+        del q, o, lse, plan
+    res["config5"] = out5
+    del pools
+    torch.cuda.empty_cache()
+    return res
+
+
 def traffic_from_profile(kind):
     """HBM bytes per launch from the committed counter summary, if it was
     taken with the kernel source as it is now; else None."""
@@ -279,6 +374,7 @@ def main():
     ap.add_argument("--replicas", type=int, default=10)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-extend", action="store_true")
+    ap.add_argument("--more", action="store_true", help="also time configs 1, 4 and 5 (adds about a minute)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run a 1 GiB device copy (counter calibration for rocprofv3 --pmc runs)")
     args = ap.parse_args()
@@ -305,6 +401,10 @@ def main():
         log("extend-8B: building inputs")
         ext = bench_extend(args, torch, B, RN, W)
         log(f"extend-8B: {ext['ms']:.3f} ms/step, attention {ext['attn_ms']:.3f} ms")
+    more = None
+    if args.more:
+        log("configs 1, 4, 5")
+        more = bench_more(torch, B, RN, W)
     cpu = None
     if not args.no_cpu:
         log("cpu baseline (oracle)")
@@ -352,6 +452,8 @@ def main():
                          "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(tf / BF16_PEAK_TFLOPS, 4),
                          "traffic": traffic_from_profile("extend"), "flops": ext["flops"]},
         }
+    if more is not None:
+        out["more_configs"] = more
     print(json.dumps(out), flush=True)
 
 

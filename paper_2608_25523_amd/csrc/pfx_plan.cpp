@@ -6,6 +6,8 @@
 #include <cstdio>
 #include <cstring>
 #include <new>
+#include <unordered_map>
+#include <vector>
 
 #include "pfx_internal.h"
 
@@ -442,6 +444,51 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   auto piece_cost = [](const Seg& sg) { return (sg.h.kind == kPrefixItem ? 11 : 10) * sg.h.nsteps + 10; };
   std::stable_sort(p->segs.begin(), p->segs.end(),
                    [&](const Seg& x, const Seg& y) { return piece_cost(x) > piece_cost(y); });
+
+  // The column blocks of one prefix chunk (one KV head, the same steps of an
+  // agent's prefix, different decode rows) read the same K/V.  Pieces are
+  // dealt to workgroup p mod S in even rounds and S - 1 - p mod S in odd
+  // ones, and the dispatcher hands workgroups to the 8 XCDs in turn, so
+  // positions eight apart in one round run on one XCD.  Within each run of
+  // equal-cost prefix pieces, chunks are taken eight at a time and block j
+  // of the c-th is placed at 8 j + c: a chunk's blocks then run side by side
+  // behind one L2 and read it from HBM about once.  Only the order changes
+  // (every piece keeps its partial slot), so results do not.
+  {
+    std::vector<Seg> order;
+    order.reserve(p->segs.size());
+    size_t i = 0;
+    while (i < p->segs.size()) {
+      const int32_t cost = piece_cost(p->segs[i]);
+      const bool prefix = p->segs[i].h.kind == kPrefixItem;
+      size_t j = i;
+      while (j < p->segs.size() && piece_cost(p->segs[j]) == cost && (p->segs[j].h.kind == kPrefixItem) == prefix)
+        ++j;
+      if (!prefix) {
+        order.insert(order.end(), p->segs.begin() + i, p->segs.begin() + j);
+        i = j;
+        continue;
+      }
+      // A chunk is named by the page block of its first step.
+      std::vector<std::vector<size_t>> chunks;
+      std::unordered_map<int32_t, size_t> chunk_of;
+      for (size_t k = i; k < j; ++k) {
+        auto ins = chunk_of.emplace(p->segs[k].steps[0], chunks.size());
+        if (ins.second) chunks.emplace_back();
+        chunks[ins.first->second].push_back(k);
+      }
+      for (size_t g = 0; g < chunks.size(); g += 8) {
+        const size_t g1 = std::min(chunks.size(), g + 8);
+        size_t blocks = 0;
+        for (size_t c = g; c < g1; ++c) blocks = std::max(blocks, chunks[c].size());
+        for (size_t bj = 0; bj < blocks; ++bj)
+          for (size_t c = g; c < g1; ++c)
+            if (bj < chunks[c].size()) order.push_back(p->segs[chunks[c][bj]]);
+      }
+      i = j;
+    }
+    p->segs.swap(order);
+  }
 
   // ---- extend blocks (Sec. 3): up to 128 query columns of one request,
   // over the whole prefix (no mask) then the suffix (causal), written

@@ -336,6 +336,28 @@ def test_config_plans_build_and_group_prefixes():
             assert s.num_extend_items == sum((int(n) + 31) // 32 for n in b.n_rows) * 8
 
 
+def test_prefix_chunk_blocks_are_dealt_to_one_xcd():
+    """The column blocks of one prefix chunk (same KV head and steps, other
+    decode rows) sit eight pieces apart within one dealing round, so with 512
+    persistent workgroups they run on workgroups of one XCD residue (b mod 8)
+    and share its L2.  Config 4's chunks all do; config 5's do except where a
+    group of chunks straddles a round."""
+    S = 512
+    for cfg, least in ((4, 1.0), (5, 0.85)):
+        segs = plan_for(W.config_batch(cfg)).export(3)
+        pos = {}
+        for p, sg in enumerate(segs):
+            if sg[0] == 0:                    # prefix piece; sg[144]: page block of its first step
+                pos.setdefault(int(sg[144]), []).append(p)
+        multi = [ps for ps in pos.values() if len(ps) > 1]
+        assert multi
+        def wg(p):
+            n, x = divmod(p, S)
+            return x if n % 2 == 0 else S - 1 - x
+        ok = sum(len({p // S for p in ps}) == 1 and len({wg(p) % 8 for p in ps}) == 1 for ps in multi)
+        assert ok >= least * len(multi), (cfg, ok, len(multi))
+
+
 def test_upload_rejects_small_workspace_without_gpu_work():
     b = small_batch()
     p = plan_for(b)
