@@ -272,8 +272,8 @@ def bench_more(torch, B, RN, W):
     """The other workloads, timed on request (--more): the tiny config-1
     extend (launch-bound, reported only), config 4 (the pinned-host gather
     of 4 evicted prefixes, then decode over all 16 agents in the 48 GiB
-    pool) and config 5 (80 layers' pools; the mixed launch, and its decode
-    and extend requests planned apart)."""
+    pool), config 5 (80 layers' pools; the mixed launch, and its decode
+    and extend requests planned apart) and prefix movement."""
     import dataclasses
 
     import numpy as np
@@ -346,7 +346,77 @@ def bench_more(torch, B, RN, W):
     res["config5"] = out5
     del pools
     torch.cuda.empty_cache()
+    res["movement"] = bench_movement(torch, B, RN, W)
     return res
+
+
+def bench_movement(torch, B, RN, W):
+    """Prefix movement (Eq. (8)): B_swap per direction fitted from timed
+    evictions and loads of 512, 2048 and 8192-token prefixes (mu = tau bytes
+    per token); a serialized transition (two prefixes out, one in) against
+    the model; and a 64 MB load on a second stream beside the decode-8B
+    attention calls on the first."""
+    import numpy as np
+
+    from paper_2608_25523_amd import movement as MV
+
+    b = W.config_batch(2)
+    ds = RN.DeviceStep(b, W.host_values_fast(b, 7), poison=False)
+    hkv, d = b.num_kv_heads, b.head_dim
+    tau = hkv * d * 2 * 2
+    used = set(int(p) for p in b.used_pages())
+    spare = np.array([p for p in range(b.num_pages) if p not in used], np.int32)
+    rng = np.random.default_rng(77)
+    spare = rng.permutation(spare)
+    store = MV.HostStore(4096, hkv, d)
+    mover = MV.Mover(ds.pool, store, 4096)
+    cal = MV.calibrate_swap(mover, [spare[:n] for n in (32, 128, 512)], tau)
+    out = {"mu_bytes_per_token": tau, "b_swap_out_GBs": round(cal["b_out"] / 1e9, 2),
+           "b_swap_in_GBs": round(cal["b_in"] / 1e9, 2),
+           "overhead_out_us": round(cal["overhead_out_s"] * 1e6, 1), "overhead_in_us": round(cal["overhead_in_s"] * 1e6, 1)}
+    # A transition: prefixes of 2048 and 512 tokens out, one of 8192 in, serialized.
+    outs = [spare[512:640], spare[640:672]]
+    ins = spare[1024:1536]
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    at = 0
+    for pg in outs:
+        mover.evict(pg, np.arange(at, at + len(pg), dtype=np.int32))
+        at += len(pg)
+    mover.load(ins, np.arange(len(ins), dtype=np.int32))
+    e1.record()
+    torch.cuda.synchronize()
+    t_meas = e0.elapsed_time(e1) * 1e-3
+    tok_out, tok_in = 16 * sum(len(p) for p in outs), 16 * len(ins)
+    t_model = tau * tok_out / cal["b_out"] + tau * tok_in / cal["b_in"]
+    out["transition"] = {"tokens_out": tok_out, "tokens_in": tok_in, "measured_ms": round(t_meas * 1e3, 3),
+                         "eq8_ms": round(t_model * 1e3, 3)}
+    # Overlap: a 2048-page load on a second stream beside 30 attention calls.
+    attn = lambda: B.pfx_attention(ds.pool, ds.plan, ds.q, ds.o, ds.lse)
+    load_pages, load_slots = spare[2048:4096], np.arange(2048, dtype=np.int32)
+    a_alone = events_ms(attn, 30, torch)
+    l_alone = events_ms(lambda: mover.load(load_pages, load_slots), 3, torch, warm=1)
+    main, side = torch.cuda.current_stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    m0, m1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    side.wait_stream(main)
+    s0.record(side)
+    mover.load(load_pages, load_slots, stream=side.cuda_stream)
+    s1.record(side)
+    m0.record(main)
+    for _ in range(30):
+        attn()
+    m1.record(main)
+    torch.cuda.synchronize()
+    out["overlap"] = {"load_MB": round(len(load_pages) * 16 * tau / 1e6, 1), "load_alone_ms": round(l_alone, 3),
+                      "load_beside_attention_ms": round(s0.elapsed_time(s1), 3),
+                      "attention_alone_us": round(a_alone * 1e3, 2),
+                      "attention_beside_load_us": round(m0.elapsed_time(m1) / 30 * 1e3, 2)}
+    del ds, store, mover
+    torch.cuda.empty_cache()
+    return out
 
 
 def traffic_from_profile(kind):

@@ -267,7 +267,9 @@ int pfx_merge_states(const float* o_parts, const float* lse_parts, int32_t num_p
  * evicts (GPU -> host).  src_pages and dst_pages are host arrays, checked
  * against the two page counts (PFX_ERANGE) and for repeated destinations
  * (PFX_EINVAL) before anything runs; they are staged in the caller's device
- * workspace (at least pfx_page_copy_workspace_bytes(n) bytes).
+ * workspace (at least pfx_page_copy_workspace_bytes(n) bytes).  A page
+ * array that is neither device memory nor pinned host memory is rejected
+ * (PFX_EINVAL) before anything runs.
  * --------------------------------------------------------------------- */
 size_t pfx_page_copy_workspace_bytes(int32_t n);
 int pfx_page_copy(const pfx_pool* dst, const pfx_pool* src, const int32_t* dst_pages,

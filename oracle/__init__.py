@@ -21,3 +21,4 @@ from .attention import (  # noqa: F401
     page_copy,
     pages_needed,
 )
+from . import movement  # noqa: F401,E402

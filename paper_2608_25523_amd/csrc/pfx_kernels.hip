@@ -1275,6 +1275,15 @@ extern "C" int pfx_page_copy(const pfx_pool* dst, const pfx_pool* src, const int
     pairs[2 * i] = dst_pages[i];
     pairs[2 * i + 1] = src_pages[i];
   }
+  // Every page array must be device memory or pinned host memory (the
+  // kernel would fault on pageable host memory).
+  for (const void* ptr : {dst->k_pages, dst->v_pages, src->k_pages, src->v_pages}) {
+    hipPointerAttribute_t at;
+    if (hipPointerGetAttributes(&at, ptr) != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(PFX_EINVAL, "pfx_page_copy: a page pointer is neither device nor pinned host memory");
+    }
+  }
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = hipMemcpyAsync(ws, pairs.data(), pairs.size() * 4, hipMemcpyHostToDevice, s);
   if (e != hipSuccess) return hip_fail(e, "pfx_page_copy: hipMemcpyAsync");

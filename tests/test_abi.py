@@ -392,3 +392,6 @@ def test_device_calls_validate_before_launch():
     assert B.LIB.pfx_page_copy(C.byref(dst), C.byref(src), ids, srcs, 2, ws, 16, None) == B.PFX_ENOMEM
     bad = B.pfx_pool(6, 16, 2, 128, 8, 8)
     assert B.LIB.pfx_page_copy(C.byref(bad), C.byref(src), ids, srcs, 2, ws, 4096, None) == B.PFX_EINVAL
+    # valid ids and workspace, page pointers HIP does not know: refused before any launch
+    assert B.LIB.pfx_page_copy(C.byref(dst), C.byref(src), ids, srcs, 2, ws, 4096, None) == B.PFX_EINVAL
+    assert "neither device nor pinned host" in B.pfx_last_error()
