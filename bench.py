@@ -347,6 +347,14 @@ def bench_more(torch, B, RN, W):
     del pools
     torch.cuda.empty_cache()
     res["movement"] = bench_movement(torch, B, RN, W)
+    from paper_2608_25523_amd import service as SV
+    pre = SV.profile_prefill([256, 512, 1024, 2048, 4096, 8192], prefix_len=4096)
+    dec = SV.profile_decode([1, 4, 16, 64], prefix_len=2048, suffix_len=288)
+    res["service_tables"] = {
+        "shape": "one layer, Hq32/Hkv8/d128; prefill over a 4096-token prefix; decode: B requests of one "
+                 "agent, 2048-token prefix, 288-token suffixes",
+        "t_prefill_us": {str(k): round(v * 1e6, 1) for k, v in pre.items()},
+        "t_decode_step_us": {str(k): round(v * 1e6, 2) for k, v in dec.items()}}
     return res
 
 

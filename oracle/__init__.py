@@ -22,3 +22,4 @@ from .attention import (  # noqa: F401
     pages_needed,
 )
 from . import movement  # noqa: F401,E402
+from . import service  # noqa: F401,E402
