@@ -273,7 +273,8 @@ def bench_more(torch, B, RN, W):
     extend (launch-bound, reported only), config 4 (the pinned-host gather
     of 4 evicted prefixes, then decode over all 16 agents in the 48 GiB
     pool), config 5 (80 layers' pools; the mixed launch, and its decode
-    and extend requests planned apart) and prefix movement."""
+    and extend requests planned apart), prefix movement, the rebuild of a
+    preempted request and the service-time tables."""
     import dataclasses
 
     import numpy as np
@@ -347,6 +348,7 @@ def bench_more(torch, B, RN, W):
     del pools
     torch.cuda.empty_cache()
     res["movement"] = bench_movement(torch, B, RN, W)
+    res["rebuild"] = bench_rebuild(torch, B, RN, W)
     from paper_2608_25523_amd import service as SV
     pre = SV.profile_prefill([256, 512, 1024, 2048, 4096, 8192], prefix_len=4096)
     dec = SV.profile_decode([1, 4, 16, 64], prefix_len=2048, suffix_len=288)
@@ -356,6 +358,43 @@ def bench_more(torch, B, RN, W):
         "t_prefill_us": {str(k): round(v * 1e6, 1) for k, v in pre.items()},
         "t_decode_step_us": {str(k): round(v * 1e6, 2) for k, v in dec.items()}}
     return res
+
+
+def bench_rebuild(torch, B, RN, W, y=256, prompt=200, prefix=2048):
+    """Rebuilding a preempted request's y generated tokens (Eq. (9)): by
+    replaying y decode steps (append + attention each, plans built
+    beforehand), and by one extend call over the y tokens (append +
+    attention)."""
+    import numpy as np
+
+    full = W.make_batch(4050, num_q_heads=32, num_kv_heads=8, head_dim=128, num_pages=512, prefix_len=[prefix],
+                        agent=[0], suffix_len=[prompt + y], n_rows=[prompt + y])
+    hv = W.host_values_fast(full, 4051)
+    ds = RN.DeviceStep(full, hv, poison=False)
+    kn, vn = RN.to_device_bits(hv.k_new), RN.to_device_bits(hv.v_new)
+    q1 = torch.randn((1, 32, 128), dtype=torch.bfloat16, device="cuda")
+    qy = torch.randn((y, 32, 128), dtype=torch.bfloat16, device="cuda")
+    o1, l1 = torch.empty_like(q1), torch.empty((1, 32), dtype=torch.float32, device="cuda")
+    oy, ly = torch.empty_like(qy), torch.empty((y, 32), dtype=torch.float32, device="cuda")
+    plans = [B.plan_from_batch(ds.pool, W.with_lengths(full, [prompt + k + 1], [1]), B.PFX_MODE_DECODE).upload()
+             for k in range(y)]
+    plan_y = B.plan_from_batch(ds.pool, W.with_lengths(full, [prompt + y], [y]), B.PFX_MODE_EXTEND).upload()
+
+    def by_decode():
+        for k in range(y):
+            B.pfx_append_kv(ds.pool, plans[k], kn[prompt + k:prompt + k + 1], vn[prompt + k:prompt + k + 1])
+            B.pfx_attention(ds.pool, plans[k], q1, o1, l1)
+
+    def by_extend():
+        B.pfx_append_kv(ds.pool, plan_y, kn[prompt:], vn[prompt:])
+        B.pfx_attention(ds.pool, plan_y, qy, oy, ly)
+
+    dec_ms = events_ms(by_decode, 3, torch, warm=1)
+    ext_ms = events_ms(by_extend, 10, torch)
+    del ds, plans, plan_y
+    return {"tokens": y, "prompt": prompt, "prefix": prefix, "by_decode_ms": round(dec_ms, 3),
+            "t_decode_step_us": round(dec_ms / y * 1e3, 2), "by_extend_ms": round(ext_ms, 3),
+            "decode_over_extend": round(dec_ms / ext_ms, 1)}
 
 
 def bench_movement(torch, B, RN, W):

@@ -226,6 +226,17 @@ def config_batch(cfg: int, seed: int | None = None) -> Batch:
     raise ValueError(f"unknown config {cfg}")
 
 
+def with_lengths(batch: Batch, suffix_len, n_rows) -> Batch:
+    """The same pool, prefixes and request pages with other suffix lengths
+    and query rows: each request keeps the first pages its length needs
+    (its page list may have been sized for a longer suffix)."""
+    suffix_len = np.asarray(suffix_len, dtype=np.int32)
+    pages = [np.asarray(p[:_pages(int(l))], dtype=np.int32) for p, l in zip(batch.suffix_pages, suffix_len)]
+    return Batch(batch.num_q_heads, batch.num_kv_heads, batch.head_dim, batch.num_pages, batch.prefix_len,
+                 batch.prefix_pages, batch.agent, suffix_len, np.asarray(n_rows, dtype=np.int32), pages,
+                 dict(batch.meta))
+
+
 def tiny_decode_step(extend: Batch, step: int, extra_pages: list) -> Batch:
     """Config 1, decode step ``step`` (0..15) after the extend step: every
     request has one new token at suffix position 32 + step.  ``extra_pages``
