@@ -110,10 +110,35 @@ def bench_decode(args, torch, B, RN, W):
     ms, attn_ms, spread = timed_steps(step, attn, args.steps, args.warmup, torch)
     B.pfx_sync_check()
     graph_ms = graph_replay_ms(plans, ds, args.steps, torch, B)
+    side = side_costs(b, ds, plans, args.steps, torch, B)
     u = b.unique_kv_bytes()
     st = ds.plan.stats()
     return dict(batch=b, hv=hv, ms=ms, attn_ms=attn_ms, spread=spread, graph_ms=graph_ms, unique_bytes=u,
-                replicas=len(plans), stats=st)
+                replicas=len(plans), stats=st, side=side)
+
+
+def side_costs(b, ds, plans, steps, torch, B):
+    """The step's other parts, timed apart from attention: the KV append
+    (events around back-to-back calls), and the plan -- built on the host
+    from the batch's page tables (CPU wall time of the call, binding included) and copied
+    into an already allocated workspace (events)."""
+    n = max(steps, 20)
+    append_ms = events_ms(lambda: B.pfx_append_kv(ds.pool, plans[0], ds.k_new, ds.v_new), n, torch)
+    pind, pids, plen = b.prefix_csr()
+    sind, sids = b.suffix_csr()
+    qind = b.q_indptr()
+    build = lambda: B.pfx_plan_create(ds.pool, pind, pids, plen, b.agent, sind, sids, b.suffix_len, qind,
+                                      b.num_q_heads, B.PFX_MODE_DECODE)
+    build()
+    t0 = time.perf_counter()
+    for _ in range(n):
+        p = build()
+    build_ms = (time.perf_counter() - t0) * 1e3 / n
+    ws = torch.empty(p.workspace_bytes() + 256, dtype=torch.uint8, device="cuda")
+    upload_ms = events_ms(lambda: p.upload(workspace=ws), n, torch)
+    B.pfx_sync_check()
+    return {"append_us": round(append_ms * 1e3, 3), "plan_build_host_us": round(build_ms * 1e3, 2),
+            "plan_upload_us": round(upload_ms * 1e3, 3), "plan_workspace_bytes": int(p.workspace_bytes())}
 
 
 def graph_replay_ms(plans, ds, steps, torch, B):
@@ -557,6 +582,7 @@ def main():
                      "attn_us": round(dec["attn_ms"] * 1e3, 3),
                      "attn_us_p10_p50_p90": [round(dec["spread"][k] * 1e3, 3) for k in ("p10", "p50", "p90")]},
         "graph_ms_per_step": None if dec["graph_ms"] is None else round(dec["graph_ms"], 5),
+        "step_parts": dec["side"],
         "cpu_baseline": cpu,
     }
     if ext is not None:

@@ -127,10 +127,10 @@ struct pfx_plan {
   int32_t num_pages = 0, hkv = 0, d = 0, hq = 0, group = 0, mode = 0;
   int32_t decode_workers = 0;  // decode workgroups requested (0: two per compute unit)
   int32_t num_reqs = 0, num_tokens = 0;
-  std::vector<pfx::Item> items;  // extend blocks
+  int32_t num_items = 0;       // extend blocks (their records live in the blob at off_items)
   std::vector<int32_t> row_tok, page_list, tok_req, tok_slot;
   std::vector<pfx::ReqInfo> req;
-  std::vector<pfx::Seg> segs;  // decode pieces
+  int32_t num_segs = 0;        // decode pieces (their records live in the blob at off_segs)
   int64_t num_decode_steps = 0;
   std::vector<int32_t> merge_tok;
   std::vector<pfx::MergeHead> merge_head;
@@ -141,6 +141,8 @@ struct pfx_plan {
   size_t off_items = 0, off_row_tok = 0, off_page_list = 0, off_tok_slot = 0, off_segs = 0,
          off_merge_tok = 0, off_merge_head = 0, off_opart = 0, off_lpart = 0, total_bytes = 0, blob_bytes = 0;
   std::vector<unsigned char> blob;  // host image of [0, blob_bytes)
+  const pfx::Item* host_items() const { return reinterpret_cast<const pfx::Item*>(blob.data() + off_items); }
+  const pfx::Seg* host_segs() const { return reinterpret_cast<const pfx::Seg*>(blob.data() + off_segs); }
   void* dev_ws = nullptr;
   size_t dev_ws_bytes = 0;
 };

@@ -1140,9 +1140,9 @@ static int check_pool_matches(const pfx_pool* pool, const pfx_plan* p, const cha
 
 template <int D>
 static void launch_all(AttnArgs a, const pfx_plan* p, hipStream_t s) {
-  if (!p->items.empty()) hipLaunchKernelGGL((extend_kernel<D>), dim3(p->items.size()), dim3(256), 0, s, a);
-  if (!p->segs.empty()) {
-    const int S = std::min<int>(a.num_workers, static_cast<int>(p->segs.size()));
+  if (p->num_items > 0) hipLaunchKernelGGL((extend_kernel<D>), dim3(p->num_items), dim3(256), 0, s, a);
+  if (p->num_segs > 0) {
+    const int S = std::min<int>(a.num_workers, p->num_segs);
     hipLaunchKernelGGL((decode_kernel<D>), dim3(S), dim3(256), 0, s, a);
   }
   const int n_tok = static_cast<int>(p->merge_tok.size());
@@ -1196,7 +1196,7 @@ extern "C" int pfx_attention(const pfx_pool* pool, const pfx_plan* p, const void
                              float sm_scale, void* stream) {
   int rc = check_pool_matches(pool, p, "pfx_attention");
   if (rc) return rc;
-  if (p->items.empty() && p->segs.empty()) return PFX_OK;
+  if (p->num_items == 0 && p->num_segs == 0) return PFX_OK;
   if (!q || !o) return fail(PFX_EINVAL, "pfx_attention: q or o is NULL");
   if (!(sm_scale > 0.f)) sm_scale = 1.0f / sqrtf(float(p->d));
   AttnArgs a;
@@ -1211,7 +1211,7 @@ extern "C" int pfx_attention(const pfx_pool* pool, const pfx_plan* p, const void
   a.group = p->group;
   a.group_shift = __builtin_ctz(static_cast<unsigned>(p->group));
   a.scale_log2 = sm_scale * kLog2e;
-  a.num_pieces = static_cast<int32_t>(p->segs.size());
+  a.num_pieces = p->num_segs;
   a.num_workers = p->decode_workers;
   if (a.num_workers <= 0) {
     int dev = 0, ncu = 0;

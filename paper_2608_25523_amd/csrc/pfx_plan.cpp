@@ -27,6 +27,12 @@ int fail(int code, const char* fmt, ...) {
 
 void clear_error() { g_err.clear(); }
 
+// One host image kept per thread for the next plan (see pfx_plan_destroy).
+static std::vector<unsigned char>& spare_blob() {
+  thread_local std::vector<unsigned char> spare;
+  return spare;
+}
+
 static size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 static int64_t pages_for(int64_t tokens) { return (tokens + PFX_PAGE_SIZE - 1) / PFX_PAGE_SIZE; }
@@ -245,12 +251,13 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
                 (long long)need, pool->num_pages);
 
   // ---- page ids: in range and owned exactly once ----
-  std::vector<uint8_t> owner(pool->num_pages, 0);
+  std::vector<uint64_t> owner((size_t(pool->num_pages) + 63) / 64, 0);  // one bit per page
   auto claim = [&](int32_t id, const char* what, int32_t who) -> int {
     if (id < 0 || id >= pool->num_pages)
       return fail(PFX_ERANGE, "pfx_plan_create: %s %d uses page %d outside [0, %d)", what, who, id, pool->num_pages);
-    if (owner[id]) return fail(PFX_EINVAL, "pfx_plan_create: page %d is used twice (%s %d)", id, what, who);
-    owner[id] = 1;
+    const uint64_t bit = uint64_t(1) << (id & 63);
+    if (owner[id >> 6] & bit) return fail(PFX_EINVAL, "pfx_plan_create: page %d is used twice (%s %d)", id, what, who);
+    owner[id >> 6] |= bit;
     return PFX_OK;
   };
   for (int32_t a = 0; a < A; ++a) {
@@ -359,43 +366,36 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   // ---- decode pieces: each item's 32-key steps (two 16-key pages of one
   // KV head) cut into runs of at most kPieceSteps, as even as possible ----
   auto page_blk = [&](const DItem& x, int32_t pg) { return p->page_list[x.page_off + pg] * hkv + x.h; };
-  std::vector<int32_t> npieces(dit.size(), 0);
+  // A piece is described by its item, its index and its step range here; the
+  // full records are written once, in launch order, further down.
+  struct Piece {
+    int32_t item, piece, s0, s1;
+  };
+  std::vector<Piece> pcs;
+  {
+    size_t total = 0;
+    for (const DItem& x : dit) {
+      const int32_t ns = (x.keys + kStepKeys - 1) / kStepKeys;
+      total += size_t((ns + piece_steps - 1) / piece_steps);
+    }
+    pcs.reserve(total);
+  }
   for (size_t xi = 0; xi < dit.size(); ++xi) {
-    const DItem& x = dit[xi];
-    const int32_t ns = (x.keys + kStepKeys - 1) / kStepKeys;
-    const int32_t npages = static_cast<int32_t>(pages_for(x.keys));
+    const int32_t ns = (dit[xi].keys + kStepKeys - 1) / kStepKeys;
     const int32_t np = (ns + piece_steps - 1) / piece_steps;
     p->num_decode_steps += ns;
-    for (int32_t k = 0; k < np; ++k) {
-      const int32_t s0 = int32_t(int64_t(k) * ns / np), s1 = int32_t(int64_t(k + 1) * ns / np);
-      Seg sg{};
-      sg.h.kind = x.kind;
-      sg.h.kv_head = x.h;
-      sg.h.ncols = x.rows * G;
-      sg.h.nsteps = s1 - s0;
-      sg.h.k0 = s0 * kStepKeys;
-      sg.h.kend = x.keys;
-      sg.h.causal_base = x.causal_base;
-      sg.h.causal = x.kind == kSuffixItem && x.rows > 1;
-      sg.h.item = static_cast<int32_t>(xi);
-      sg.h.piece = k;
-      for (int32_t i = s0; i < s1; ++i) {
-        const int32_t pg0 = 2 * i, pg1 = 2 * i + 1 < npages ? 2 * i + 1 : 2 * i;  // a missing page repeats (masked)
-        sg.steps[2 * (i - s0)] = page_blk(x, pg0);
-        sg.steps[2 * (i - s0) + 1] = page_blk(x, pg1);
-      }
-      p->segs.push_back(sg);
-    }
-    npieces[xi] = np;
+    for (int32_t k = 0; k < np; ++k)
+      pcs.push_back(Piece{static_cast<int32_t>(xi), k, int32_t(int64_t(k) * ns / np), int32_t(int64_t(k + 1) * ns / np)});
+    dit[xi].npieces = np;
   }
-  for (size_t x = 0; x < dit.size(); ++x) dit[x].npieces = npieces[x];
 
   // ---- partial slots: a decode row of KV head h is seen by the pieces of
   // its prefix item (slots 0 ..) and then of its suffix item; every piece
   // leaves its unnormalised state in a slot and the merge (Sec. 4.2,
   // Eq. (8)) combines them into the row (a lone piece is just normalised) ----
-  std::vector<int32_t> tok_base(size_t(total_tokens) * hkv, -1), np_prefix(size_t(R) * hkv, 0),
-      np_total(size_t(R) * hkv, 0);
+  // A decode request's rows are consecutive in the merge list, from
+  // req_mrow[r]; merge_head[row * Hkv + h] holds their first slot and count.
+  std::vector<int32_t> np_prefix(size_t(R) * hkv, 0), np_total(size_t(R) * hkv, 0), req_mrow(R, -1);
   int64_t part_units = 0;
   for (int32_t r = 0; r < R; ++r) {
     if (!is_decode_class(r)) continue;
@@ -407,13 +407,13 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
       any |= np_total[rh] >= 1;
     }
     if (!any) continue;
+    req_mrow[r] = static_cast<int32_t>(p->merge_tok.size());
     for (int32_t t = 0; t < p->req[r].n; ++t) {
       const int32_t tok = p->req[r].q_start + t;
       p->merge_tok.push_back(tok);
       for (int32_t h = 0; h < hkv; ++h) {
         const int32_t np = np_total[size_t(r) * hkv + h];
         if (np >= 1) {
-          tok_base[size_t(tok) * hkv + h] = static_cast<int32_t>(part_units);
           p->merge_head.push_back(MergeHead{static_cast<int32_t>(part_units), np});
           part_units += np;
         } else {
@@ -425,25 +425,18 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   if (part_units * G > (int64_t(1) << 31) / std::max(1, p->d))
     return delete p, fail(PFX_ERANGE, "pfx_plan_create: too many partial rows");
   p->num_part_rows = part_units * G;
-  for (Seg& sg : p->segs) {
-    const DItem& it = dit[sg.h.item];
-    for (int32_t j = 0; j < it.rows; ++j) {
-      const int32_t tok = drow_tok[it.row_first + j];
-      const int32_t r = p->tok_req[tok];
-      const size_t rh = size_t(r) * hkv + it.h;
-      sg.tok[j] = tok;
-      const int32_t slot = (it.kind == kPrefixItem ? 0 : np_prefix[rh]) + sg.h.piece;
-      sg.h.slot = slot;  // the same for every row of the piece
-      sg.out[j] = (tok_base[size_t(tok) * hkv + it.h] + slot) * G;
-    }
-  }
 
   // Longest first: a prefix step multiplies 64 query columns, a suffix step
   // at most 16, so prefix steps weigh a little more; every piece also has a
   // stage for its query rows.
-  auto piece_cost = [](const Seg& sg) { return (sg.h.kind == kPrefixItem ? 11 : 10) * sg.h.nsteps + 10; };
-  std::stable_sort(p->segs.begin(), p->segs.end(),
-                   [&](const Seg& x, const Seg& y) { return piece_cost(x) > piece_cost(y); });
+  const size_t nsegs = pcs.size();
+  auto is_prefix = [&](int32_t k) { return dit[pcs[k].item].kind == kPrefixItem; };
+  std::vector<int32_t> pcost(nsegs), rank(nsegs);
+  for (size_t k = 0; k < nsegs; ++k) {
+    pcost[k] = (is_prefix(int32_t(k)) ? 11 : 10) * (pcs[k].s1 - pcs[k].s0) + 10;
+    rank[k] = static_cast<int32_t>(k);
+  }
+  std::stable_sort(rank.begin(), rank.end(), [&](int32_t x, int32_t y) { return pcost[x] > pcost[y]; });
 
   // The column blocks of one prefix chunk (one KV head, the same steps of an
   // agent's prefix, different decode rows) read the same K/V.  Pieces are
@@ -454,28 +447,28 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   // of the c-th is placed at 8 j + c: a chunk's blocks then run side by side
   // behind one L2 and read it from HBM about once.  Only the order changes
   // (every piece keeps its partial slot), so results do not.
+  std::vector<int32_t> order;
+  order.reserve(nsegs);
   {
-    std::vector<Seg> order;
-    order.reserve(p->segs.size());
     size_t i = 0;
-    while (i < p->segs.size()) {
-      const int32_t cost = piece_cost(p->segs[i]);
-      const bool prefix = p->segs[i].h.kind == kPrefixItem;
+    while (i < nsegs) {
+      const int32_t cost = pcost[rank[i]];
+      const bool prefix = is_prefix(rank[i]);
       size_t j = i;
-      while (j < p->segs.size() && piece_cost(p->segs[j]) == cost && (p->segs[j].h.kind == kPrefixItem) == prefix)
-        ++j;
+      while (j < nsegs && pcost[rank[j]] == cost && is_prefix(rank[j]) == prefix) ++j;
       if (!prefix) {
-        order.insert(order.end(), p->segs.begin() + i, p->segs.begin() + j);
+        order.insert(order.end(), rank.begin() + i, rank.begin() + j);
         i = j;
         continue;
       }
       // A chunk is named by the page block of its first step.
-      std::vector<std::vector<size_t>> chunks;
+      std::vector<std::vector<int32_t>> chunks;
       std::unordered_map<int32_t, size_t> chunk_of;
       for (size_t k = i; k < j; ++k) {
-        auto ins = chunk_of.emplace(p->segs[k].steps[0], chunks.size());
+        const Piece& pc = pcs[rank[k]];
+        auto ins = chunk_of.emplace(page_blk(dit[pc.item], 2 * pc.s0), chunks.size());
         if (ins.second) chunks.emplace_back();
-        chunks[ins.first->second].push_back(k);
+        chunks[ins.first->second].push_back(rank[k]);
       }
       for (size_t g = 0; g < chunks.size(); g += 8) {
         const size_t g1 = std::min(chunks.size(), g + 8);
@@ -483,17 +476,24 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
         for (size_t c = g; c < g1; ++c) blocks = std::max(blocks, chunks[c].size());
         for (size_t bj = 0; bj < blocks; ++bj)
           for (size_t c = g; c < g1; ++c)
-            if (bj < chunks[c].size()) order.push_back(p->segs[chunks[c][bj]]);
+            if (bj < chunks[c].size()) order.push_back(chunks[c][bj]);
       }
       i = j;
     }
-    p->segs.swap(order);
   }
+
+  if (nsegs > size_t(INT32_MAX)) return delete p, fail(PFX_ERANGE, "pfx_plan_create: too many decode pieces");
 
   // ---- extend blocks (Sec. 3): up to 128 query columns of one request,
   // over the whole prefix (no mask) then the suffix (causal), written
   // directly ----
-  std::vector<Item> items;
+  // A block of rows of one request, before it is expanded over the KV heads.
+  struct XBlock {
+    int32_t r, i0, i1, rbeg;
+    int64_t cost;  // keys it streams: the whole prefix and the suffix up to its last row
+  };
+  std::vector<XBlock> xbs;
+  p->row_tok.reserve(total_tokens);
   for (int32_t r = 0; r < R; ++r) {
     const ReqInfo ri = p->req[r];
     if (ri.n == 0 || is_decode_class(r)) continue;
@@ -505,48 +505,25 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
       const int32_t i1 = std::min(ri.n, i0 + per);
       const int32_t rbeg = static_cast<int32_t>(p->row_tok.size());
       for (int32_t i = i0; i < i1; ++i) p->row_tok.push_back(ri.q_start + i);
-      for (int32_t h = 0; h < hkv; ++h) {
-        Item it{};
-        it.kv_head = h;
-        it.row_begin = rbeg;
-        it.row_count = i1 - i0;
-        it.nblk = blocks_for(i1 - i0);
-        it.s0_page_off = P > 0 ? prefix_off[a] : 0;
-        it.s0_kbeg = 0;
-        it.s0_kend = P;
-        it.s1_page_off = suffix_off[r];
-        it.s1_kbeg = 0;
-        it.s1_kend = L - ri.n + i1;
-        it.causal_base = L - ri.n - ri.q_start;
-        it.out_slot = -1;
-        it.kind = kExtendItem;
-        it.req = r;
-        items.push_back(it);
-        ++p->n_extend_items;
-      }
+      xbs.push_back(XBlock{r, i0, i1, rbeg, int64_t(P) + (L - ri.n + i1)});
     }
   }
-  // Longest key ranges first keeps the tail of the launch short.
-  auto cost = [](const Item& it) { return int64_t(it.s0_kend - it.s0_kbeg) + (it.s1_kend - it.s1_kbeg); };
-  std::stable_sort(items.begin(), items.end(), [&](const Item& x, const Item& y) { return cost(x) > cost(y); });
-  // Each block's leading page ids and first token.
-  for (Item& it : items) {
-    int32_t k = 0;
-    for (int32_t pg = it.s0_kbeg >> 4; it.s0_kend > it.s0_kbeg && pg < (it.s0_kend + 15) >> 4 && k < kItemPages; ++pg)
-      it.first_pages[k++] = p->page_list[it.s0_page_off + pg];
-    for (int32_t pg = it.s1_kbeg >> 4; it.s1_kend > it.s1_kbeg && pg < (it.s1_kend + 15) >> 4 && k < kItemPages; ++pg)
-      it.first_pages[k++] = p->page_list[it.s1_page_off + pg];
-    it.tok0 = p->row_tok[it.row_begin];
-  }
-  p->items = std::move(items);
+  // Longest key ranges first keeps the tail of the launch short (the KV
+  // heads of one block stay together, in order).
+  std::vector<int32_t> xrank(xbs.size());
+  for (size_t k = 0; k < xbs.size(); ++k) xrank[k] = static_cast<int32_t>(k);
+  std::stable_sort(xrank.begin(), xrank.end(), [&](int32_t x, int32_t y) { return xbs[x].cost > xbs[y].cost; });
+  const size_t nitems = xbs.size() * size_t(hkv);
+  if (nitems > size_t(INT32_MAX)) return delete p, fail(PFX_ERANGE, "pfx_plan_create: too many extend blocks");
+  p->n_extend_items = static_cast<int32_t>(nitems);
 
   // ---- workspace layout ----
   size_t off = 0;
-  p->off_items = off;      off = align256(off + p->items.size() * sizeof(Item));
+  p->off_items = off;      off = align256(off + nitems * sizeof(Item));
   p->off_row_tok = off;    off = align256(off + p->row_tok.size() * 4);
   p->off_page_list = off;  off = align256(off + p->page_list.size() * 4);
   p->off_tok_slot = off;   off = align256(off + p->tok_slot.size() * 4);
-  p->off_segs = off;       off = align256(off + p->segs.size() * sizeof(Seg));
+  p->off_segs = off;       off = align256(off + nsegs * sizeof(Seg));
   p->off_merge_tok = off;  off = align256(off + p->merge_tok.size() * 4);
   p->off_merge_head = off; off = align256(off + p->merge_head.size() * sizeof(MergeHead));
   p->blob_bytes = off;
@@ -554,17 +531,92 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   p->off_lpart = off;      off = align256(off + size_t(p->num_part_rows) * 8);
   p->total_bytes = std::max<size_t>(off, 256);
 
+  p->num_items = static_cast<int32_t>(nitems);
+  p->num_segs = static_cast<int32_t>(nsegs);
+
+  // The host image: the last destroyed plan's buffer is reused when it is
+  // large enough (a serving loop builds a plan every step, and fresh pages
+  // of a few hundred KiB cost more to fault in than to fill).
+  p->blob.swap(spare_blob());
   p->blob.assign(p->blob_bytes, 0);
   auto put = [&](size_t at, const void* src, size_t bytes) {
     if (bytes) std::memcpy(p->blob.data() + at, src, bytes);
   };
-  put(p->off_items, p->items.data(), p->items.size() * sizeof(Item));
   put(p->off_row_tok, p->row_tok.data(), p->row_tok.size() * 4);
   put(p->off_page_list, p->page_list.data(), p->page_list.size() * 4);
   put(p->off_tok_slot, p->tok_slot.data(), p->tok_slot.size() * 4);
-  put(p->off_segs, p->segs.data(), p->segs.size() * sizeof(Seg));
   put(p->off_merge_tok, p->merge_tok.data(), p->merge_tok.size() * 4);
   put(p->off_merge_head, p->merge_head.data(), p->merge_head.size() * sizeof(MergeHead));
+
+  // The extend block records, in launch order: each block's leading page
+  // ids and first token are filled in here.
+  Item* items = reinterpret_cast<Item*>(p->blob.data() + p->off_items);
+  size_t nit = 0;
+  for (int32_t xi : xrank) {
+    const XBlock& xb = xbs[xi];
+    const ReqInfo ri = p->req[xb.r];
+    const int32_t a = b->agent[xb.r];
+    const int32_t P = a >= 0 ? pt->prefix_len[a] : 0;
+    const int32_t L = b->suffix_len[xb.r];
+    Item it{};  // the same for every KV head but the head itself
+    it.row_begin = xb.rbeg;
+    it.row_count = xb.i1 - xb.i0;
+    it.nblk = blocks_for(xb.i1 - xb.i0);
+    it.s0_page_off = P > 0 ? prefix_off[a] : 0;
+    it.s0_kbeg = 0;
+    it.s0_kend = P;
+    it.s1_page_off = suffix_off[xb.r];
+    it.s1_kbeg = 0;
+    it.s1_kend = L - ri.n + xb.i1;
+    it.causal_base = L - ri.n - ri.q_start;
+    it.out_slot = -1;
+    it.kind = kExtendItem;
+    it.req = xb.r;
+    int32_t k = 0;
+    for (int32_t pg = it.s0_kbeg >> 4; it.s0_kend > it.s0_kbeg && pg < (it.s0_kend + 15) >> 4 && k < kItemPages; ++pg)
+      it.first_pages[k++] = p->page_list[it.s0_page_off + pg];
+    for (int32_t pg = it.s1_kbeg >> 4; it.s1_kend > it.s1_kbeg && pg < (it.s1_kend + 15) >> 4 && k < kItemPages; ++pg)
+      it.first_pages[k++] = p->page_list[it.s1_page_off + pg];
+    it.tok0 = p->row_tok[it.row_begin];
+    for (int32_t h = 0; h < hkv; ++h) {
+      it.kv_head = h;
+      new (items + nit++) Item(it);
+    }
+  }
+
+  // The piece records, in launch order.
+  Seg* segs = reinterpret_cast<Seg*>(p->blob.data() + p->off_segs);
+  for (size_t k = 0; k < nsegs; ++k) {
+    const Piece& pc = pcs[order[k]];
+    const DItem& x = dit[pc.item];
+    const int32_t npages = static_cast<int32_t>(pages_for(x.keys));
+    Seg& sg = *new (segs + k) Seg{};
+    sg.h.kind = x.kind;
+    sg.h.kv_head = x.h;
+    sg.h.ncols = x.rows * G;
+    sg.h.nsteps = pc.s1 - pc.s0;
+    sg.h.k0 = pc.s0 * kStepKeys;
+    sg.h.kend = x.keys;
+    sg.h.causal_base = x.causal_base;
+    sg.h.causal = x.kind == kSuffixItem && x.rows > 1;
+    sg.h.item = pc.item;
+    sg.h.piece = pc.piece;
+    for (int32_t i = pc.s0; i < pc.s1; ++i) {
+      const int32_t pg0 = 2 * i, pg1 = 2 * i + 1 < npages ? 2 * i + 1 : 2 * i;  // a missing page repeats (masked)
+      sg.steps[2 * (i - pc.s0)] = page_blk(x, pg0);
+      sg.steps[2 * (i - pc.s0) + 1] = page_blk(x, pg1);
+    }
+    for (int32_t j = 0; j < x.rows; ++j) {
+      const int32_t tok = drow_tok[x.row_first + j];
+      const int32_t r = p->tok_req[tok];
+      const size_t rh = size_t(r) * hkv + x.h;
+      sg.tok[j] = tok;
+      const int32_t slot = (x.kind == kPrefixItem ? 0 : np_prefix[rh]) + pc.piece;
+      sg.h.slot = slot;  // the same for every row of the piece
+      const size_t mrow = size_t(req_mrow[r]) + (tok - p->req[r].q_start);
+      sg.out[j] = (p->merge_head[mrow * hkv + x.h].base + slot) * G;
+    }
+  }
 
   *out = p;
   return PFX_OK;
@@ -587,7 +639,7 @@ extern "C" int pfx_plan_get_stats(const pfx_plan* p, pfx_plan_stats* s) {
   s->num_partial_rows = static_cast<int32_t>(p->num_part_rows);
   s->pages_needed = p->pages_needed;
   s->num_decode_steps = static_cast<int32_t>(p->num_decode_steps);
-  s->num_decode_pieces = static_cast<int32_t>(p->segs.size());
+  s->num_decode_pieces = p->num_segs;
   s->reserved[0] = s->reserved[1] = 0;
   s->workspace_bytes = static_cast<int64_t>(p->total_bytes);
   return PFX_OK;
@@ -598,10 +650,10 @@ extern "C" int pfx_plan_export(const pfx_plan* p, int32_t which, int32_t* out, i
   const int32_t* src = nullptr;
   int64_t n = 0;
   switch (which) {
-    case 0: src = reinterpret_cast<const int32_t*>(p->items.data()); n = int64_t(p->items.size()) * 32; break;
+    case 0: src = reinterpret_cast<const int32_t*>(p->host_items()); n = int64_t(p->num_items) * 32; break;
     case 1: src = p->row_tok.data(); n = int64_t(p->row_tok.size()); break;
     case 2: src = p->page_list.data(); n = int64_t(p->page_list.size()); break;
-    case 3: src = reinterpret_cast<const int32_t*>(p->segs.data()); n = int64_t(p->segs.size()) * 176; break;
+    case 3: src = reinterpret_cast<const int32_t*>(p->host_segs()); n = int64_t(p->num_segs) * 176; break;
     case 6: src = p->merge_tok.data(); n = int64_t(p->merge_tok.size()); break;
     case 7: src = reinterpret_cast<const int32_t*>(p->merge_head.data()); n = int64_t(p->merge_head.size()) * 2; break;
     default: return fail(PFX_EINVAL, "pfx_plan_export: which = %d", which);
@@ -613,4 +665,9 @@ extern "C" int pfx_plan_export(const pfx_plan* p, int32_t which, int32_t* out, i
   return PFX_OK;
 }
 
-extern "C" void pfx_plan_destroy(pfx_plan* p) { delete p; }
+extern "C" void pfx_plan_destroy(pfx_plan* p) {
+  if (!p) return;
+  std::vector<unsigned char>& spare = pfx::spare_blob();
+  if (p->blob.capacity() > spare.capacity()) spare.swap(p->blob);
+  delete p;
+}

@@ -395,3 +395,36 @@ def test_device_calls_validate_before_launch():
     # valid ids and workspace, page pointers HIP does not know: refused before any launch
     assert B.LIB.pfx_page_copy(C.byref(dst), C.byref(src), ids, srcs, 2, ws, 4096, None) == B.PFX_EINVAL
     assert "neither device nor pinned host" in B.pfx_last_error()
+
+
+def plan_tables(p):
+    return [p.export(w).copy() for w in (0, 1, 2, 3, 6, 7)] + [p.workspace_bytes()]
+
+
+def same_tables(x, y):
+    return all(np.array_equal(a, b) for a, b in zip(x, y))
+
+
+def test_plan_host_image_reuse_never_touches_a_live_plan():
+    # A destroyed plan's host image is handed to the next plan built on the
+    # thread.  A live plan keeps its own: its tables stay as built while
+    # other plans of other sizes come and go, and a plan rebuilt from the
+    # same inputs is identical.
+    import gc
+    big, small = W.config_batch(2), small_batch()
+    pool_big = B.make_pool(big.num_pages, big.num_kv_heads, big.head_dim)
+    a = B.plan_from_batch(pool_big, big, B.PFX_MODE_MIXED)
+    want = plan_tables(a)
+    for k in range(4):
+        b = plan_for(small) if k % 2 else B.plan_from_batch(pool_big, big, B.PFX_MODE_DECODE, piece_steps=5 + k)
+        del b
+        gc.collect()
+        c = plan_for(small, mode=B.PFX_MODE_EXTEND)
+        assert same_tables(plan_tables(a), want)
+        del c
+        gc.collect()
+    again = B.plan_from_batch(pool_big, big, B.PFX_MODE_MIXED)
+    assert same_tables(plan_tables(again), want)
+    del a
+    gc.collect()
+    assert same_tables(plan_tables(again), want)
