@@ -889,10 +889,11 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
   // the issue needs of it.
   int iord = 0, ik = -1, inst = 0, incols = 0, iqh0 = 0, iwin = 0;
   bool in_piece = false, ended = false;
-  // Per ring stage, what was issued into it: bit 7 valid, bits 5-6 slot,
-  // bits 0-4 step + 1 (0: Q).  ops: copies this wave issued per issue
-  // opportunity, 8 bits each, newest lowest.
-  uint32_t ent = 0, ops = 0;
+  // Per ring stage (16 bits each), what was issued into it: bit 8 valid,
+  // bits 6-7 slot, bits 0-5 step + 1 (0: Q).  ops: copies this wave issued
+  // per issue opportunity, 8 bits each, newest lowest.
+  uint64_t ent = 0;
+  uint32_t ops = 0;
   int pending = 0;
 
   auto issue_next = [&](int r) {
@@ -925,14 +926,14 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
           ++n_ops;
         }
       }
-      code = 0x80u | (uint32_t(q) << 5) | uint32_t(ik + 1);
+      code = 0x100u | (uint32_t(q) << 6) | uint32_t(ik + 1);
       ++pending;
       if (++ik == inst) {
         ++iord;
         in_piece = false;
       }
     }
-    ent = (ent & ~(0xFFu << (8 * r))) | (code << (8 * r));
+    ent = (ent & ~(uint64_t(0xFFFFu) << (16 * r))) | (uint64_t(code) << (16 * r));
     ops = (ops << 8) | uint32_t(n_ops);
   };
   for (int u = 0; u < NS - 1; ++u) issue_next(u);
@@ -958,12 +959,12 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
       __syncthreads();
       issue_next((r + NS - 1) % NS);
 
-      const uint32_t code = (ent >> (8 * r)) & 0xFFu;
+      const uint32_t code = uint32_t(ent >> (16 * r)) & 0xFFFFu;
       const unsigned char* stage = ring[r];
-      if (code & 0x80u) {
+      if (code & 0x100u) {
         --pending;
-        const Seg& sg = slots[(code >> 5) & 3u];
-        const int k = int(code & 31u) - 1;
+        const Seg& sg = slots[(code >> 6) & 3u];
+        const int k = int(code & 63u) - 1;
         if (k < 0) {
           // A piece starts: its columns, limits, output rows and Q.
           const i32x4 h0 = *reinterpret_cast<const i32x4*>(&sg.h);       // kind, kv_head, ncols, nsteps
