@@ -183,7 +183,7 @@ typedef struct pfx_plan_stats {
   int32_t num_partial_rows;    /* partial result rows (one query head each) kept in the workspace */
   int32_t pages_needed;        /* left-hand side of the Eq. (2) check, in pages */
   int32_t num_decode_steps;    /* 32-key steps of all decode items */
-  int32_t num_decode_pieces;   /* runs of at most 16 steps of one decode item */
+  int32_t num_decode_pieces;   /* runs of at most piece_steps steps of one decode item */
   int32_t reserved[2];
   int64_t workspace_bytes;
 } pfx_plan_stats;

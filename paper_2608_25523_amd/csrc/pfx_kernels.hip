@@ -18,7 +18,7 @@
 //     through an LDS ring; rows written directly.
 //   decode: persistent workgroups.  The decode items (an agent's prefix
 //     against a block of its decode rows, a request's suffix against its own
-//     rows; one KV head each) are cut into pieces of at most 16 32-key
+//     rows; one KV head each) are cut into pieces of at most 32 32-key
 //     steps, listed longest first and dealt to the workgroups in rounds; a
 //     workgroup's pieces flow through one LDS ring without a break at piece
 //     boundaries, and every piece leaves a partial state.
