@@ -165,8 +165,8 @@ typedef struct pfx_plan_opts {
    * compute unit of the device; never more than there are decode pieces).
    * The work division does not depend on it, only its timing. */
   int32_t decode_workers;
-  /* Longest decode piece, in 32-key steps (0 = automatic: 16, or 32 when
-   * the decode items hold at least 32768 steps; at most 32).  Shorter pieces
+  /* Longest decode piece, in 32-key steps (0 = automatic: 16, 32 when the
+   * decode items hold at least 32768 steps, 64 from 65536; at most 64).  Shorter pieces
    * balance the workgroups better but give each decode row more partial
    * results to merge. */
   int32_t piece_steps;
@@ -199,7 +199,7 @@ int pfx_plan_get_stats(const pfx_plan* plan, pfx_plan_stats* out);
 
 /* Copy one of the plan's host arrays out, for inspection and tests:
  * which = 0: extend blocks, 32 int32 each; 1: their row-token list;
- * 2: page list; 3: decode pieces, 208 int32 each (header, row tokens,
+ * 2: page list; 3: decode pieces, 272 int32 each (header, row tokens,
  * output rows, page blocks of the steps); 6: tokens whose rows are merged;
  * 7: their (base, count) of partial slots per KV head.
  * Writes min(cap, size) values and sets *count to the full size. */

@@ -74,7 +74,7 @@ class pfx_plan_stats(C.Structure):
 
 
 # Shapes of the arrays pfx_plan_export returns (int32 columns per record).
-EXPORT_WIDTH = {0: 32, 1: 1, 2: 1, 3: 208, 6: 1, 7: 2}
+EXPORT_WIDTH = {0: 32, 1: 1, 2: 1, 3: 272, 6: 1, 7: 2}
 
 
 def _load(path: str = LIB_PATH):

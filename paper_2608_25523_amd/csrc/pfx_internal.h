@@ -63,7 +63,7 @@ static_assert(sizeof(Item) == 128, "Item is 32 int32");
 // longest first and dealt to the persistent workgroups in rounds (forward,
 // then backward), so the longest run first and the shortest fill the tail.
 constexpr int kSegRows = kDecodeTileCols;  // rows of a piece (columns / G)
-constexpr int kPieceSteps = 32;            // steps of a piece, at most
+constexpr int kPieceSteps = 64;            // steps of a piece, at most
 constexpr int kPieceSlots = 4;             // pieces a workgroup holds in LDS
 
 struct alignas(16) SegHead {
@@ -89,7 +89,7 @@ struct alignas(16) Seg {
                                   // o/lse row (final) or o_part/l_part row (partial)
   int32_t steps[2 * kPieceSteps]; // per step: (page * Hkv + head) of its two 16-key pages
 };
-static_assert(sizeof(Seg) == 832, "Seg is 208 int32");
+static_assert(sizeof(Seg) == 1088, "Seg is 272 int32");
 
 // Partial results of one (decode token, KV head): nparts slots of G rows at
 // o_part/l_part rows (base + slot) * G + g.  A partial row holds a piece's

@@ -18,7 +18,7 @@
 //     through an LDS ring; rows written directly.
 //   decode: persistent workgroups.  The decode items (an agent's prefix
 //     against a block of its decode rows, a request's suffix against its own
-//     rows; one KV head each) are cut into pieces of at most 32 32-key
+//     rows; one KV head each) are cut into pieces of at most 64 32-key
 //     steps, listed longest first and dealt to the workgroups in rounds; a
 //     workgroup's pieces flow through one LDS ring without a break at piece
 //     boundaries, and every piece leaves a partial state.
@@ -864,7 +864,7 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
   constexpr int NS = kStages;
   constexpr int K = kPieceSlots;
   constexpr int kVecs = int(sizeof(Seg)) / 16;
-  static_assert(kVecs <= 64, "a descriptor is one copy instruction");
+  static_assert(kVecs > 64 && kVecs <= 128, "a descriptor is two copy instructions");
   __shared__ __attribute__((aligned(1024))) unsigned char smem[decode_smem_bytes<D>()];
   auto ring = reinterpret_cast<unsigned char (*)[TG::stage_bytes]>(smem);
   Seg* slots = reinterpret_cast<Seg*>(smem + NS * TG::stage_bytes);
@@ -889,8 +889,8 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
   // the issue needs of it.
   int iord = 0, ik = -1, inst = 0, incols = 0, iqh0 = 0, iwin = 0;
   bool in_piece = false, ended = false;
-  // Per ring stage (16 bits each), what was issued into it: bit 8 valid,
-  // bits 6-7 slot, bits 0-5 step + 1 (0: Q).  ops: copies this wave issued
+  // Per ring stage (16 bits each), what was issued into it: bit 9 valid,
+  // bits 7-8 slot, bits 0-6 step + 1 (0: Q).  ops: copies this wave issued
   // per issue opportunity, 8 bits each, newest lowest.
   uint64_t ent = 0;
   uint32_t ops = 0;
@@ -920,13 +920,15 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
         // The descriptor two pieces ahead, into the slot of the piece two back.
         const int nxt = piece_of(b, iord + 2, S);
         if (nxt < np) {
-          if (lane < kVecs)
-            copy16_to_lds(reinterpret_cast<const unsigned char*>(&a.plan.segs[nxt]) + 16 * lane,
-                          lds_address(reinterpret_cast<const unsigned char*>(&slots[(iord + 2) % K])));
-          ++n_ops;
+          // Two copies: 16-byte chunks lane and 64 + lane (lanes 0 .. kVecs - 65).
+          const unsigned char* src = reinterpret_cast<const unsigned char*>(&a.plan.segs[nxt]);
+          const uint32_t dst = lds_address(reinterpret_cast<const unsigned char*>(&slots[(iord + 2) % K]));
+          copy16_to_lds(src + 16 * lane, dst);
+          if (lane < kVecs - 64) copy16_to_lds(src + 16 * (64 + lane), dst + 1024);
+          n_ops += 2;
         }
       }
-      code = 0x100u | (uint32_t(q) << 6) | uint32_t(ik + 1);
+      code = 0x200u | (uint32_t(q) << 7) | uint32_t(ik + 1);
       ++pending;
       if (++ik == inst) {
         ++iord;
@@ -961,10 +963,10 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
 
       const uint32_t code = uint32_t(ent >> (16 * r)) & 0xFFFFu;
       const unsigned char* stage = ring[r];
-      if (code & 0x100u) {
+      if (code & 0x200u) {
         --pending;
-        const Seg& sg = slots[(code >> 6) & 3u];
-        const int k = int(code & 63u) - 1;
+        const Seg& sg = slots[(code >> 7) & 3u];
+        const int k = int(code & 127u) - 1;
         if (k < 0) {
           // A piece starts: its columns, limits, output rows and Q.
           const i32x4 h0 = *reinterpret_cast<const i32x4*>(&sg.h);       // kind, kv_head, ncols, nsteps

@@ -37,12 +37,12 @@ static size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 static int64_t pages_for(int64_t tokens) { return (tokens + PFX_PAGE_SIZE - 1) / PFX_PAGE_SIZE; }
 
-// Longest decode piece by default, in steps: 16, or 32 once the decode
-// items hold at least kLongPiecesFrom steps (64 for each workgroup of a
-// 512-workgroup launch).  Every piece costs a Q stage, a partial state and
-// its share of the merge; shorter pieces balance a small launch better.
+// Longest decode piece by default, in steps: 16; 32 once the decode items
+// hold at least kLongPiecesFrom steps (64 for each workgroup of a
+// 512-workgroup launch); 64 from twice that.  Every piece costs a Q stage,
+// a partial state and its share of the merge; shorter pieces balance a
+// small launch better.
 constexpr int32_t kDefaultPieceSteps = 16;
-constexpr int32_t kLongPieceSteps = 32;
 constexpr int64_t kLongPiecesFrom = 64 * 512;
 
 DevPlan dev_plan(const pfx_plan* p) {
@@ -380,7 +380,7 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   if (piece_steps == 0) {
     int64_t steps = 0;
     for (const DItem& x : dit) steps += (x.keys + kStepKeys - 1) / kStepKeys;
-    piece_steps = steps >= kLongPiecesFrom ? kLongPieceSteps : kDefaultPieceSteps;
+    piece_steps = steps >= 2 * kLongPiecesFrom ? 64 : steps >= kLongPiecesFrom ? 32 : kDefaultPieceSteps;
   }
   {
     size_t total = 0;
@@ -663,7 +663,7 @@ extern "C" int pfx_plan_export(const pfx_plan* p, int32_t which, int32_t* out, i
     case 0: src = reinterpret_cast<const int32_t*>(p->host_items()); n = int64_t(p->num_items) * 32; break;
     case 1: src = p->row_tok.data(); n = int64_t(p->row_tok.size()); break;
     case 2: src = p->page_list.data(); n = int64_t(p->page_list.size()); break;
-    case 3: src = reinterpret_cast<const int32_t*>(p->host_segs()); n = int64_t(p->num_segs) * 208; break;
+    case 3: src = reinterpret_cast<const int32_t*>(p->host_segs()); n = int64_t(p->num_segs) * 272; break;
     case 6: src = p->merge_tok.data(); n = int64_t(p->merge_tok.size()); break;
     case 7: src = reinterpret_cast<const int32_t*>(p->merge_head.data()); n = int64_t(p->merge_head.size()) * 2; break;
     default: return fail(PFX_EINVAL, "pfx_plan_export: which = %d", which);

@@ -194,7 +194,7 @@ def enumerate_coverage(plan, batch):
                         hit(tok, qh, plen + k)
                 outs.setdefault((tok, qh), []).append(("final", tok * hq + qh))
 
-    # Decode: items cut into pieces of at most 32 steps, longest first.
+    # Decode: items cut into pieces of at most 64 steps, longest first.
     segs = plan.export(3)
     mtok, mhead = plan.export(6), plan.export(7).reshape(-1, hkv, 2)
     midx = {int(t): i for i, t in enumerate(mtok)}
@@ -202,7 +202,7 @@ def enumerate_coverage(plan, batch):
     costs = []
     for sg in segs:
         kind, h, ncols, nst, k0, kend, cbase, slot, item, piece, causal = (int(x) for x in sg[:11])
-        assert kind in (0, 1) and 1 <= ncols <= 64 and ncols % G == 0 and k0 % 32 == 0 and 1 <= nst <= 32
+        assert kind in (0, 1) and 1 <= ncols <= 64 and ncols % G == 0 and k0 % 32 == 0 and 1 <= nst <= 64
         costs.append((11 if kind == 0 else 10) * nst + 10)
         pieces.setdefault(item, []).append((piece, k0, nst, kend))
         tok0 = int(sg[16])
