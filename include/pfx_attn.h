@@ -161,9 +161,11 @@ void pfx_alloc_destroy(pfx_alloc* alloc);
 typedef struct pfx_plan pfx_plan;
 
 typedef struct pfx_plan_opts {
-  /* Persistent workgroups of the decode launch (0 = automatic: two per
-   * compute unit of the device; never more than there are decode pieces).
-   * The work division does not depend on it, only its timing. */
+  /* Workgroups of the decode launch (0 = automatic: one per decode piece,
+   * handed out by the dispatcher; a smaller count makes them persistent,
+   * each running several pieces through its LDS ring; never more than there
+   * are pieces).  The work division does not depend on it, only its
+   * timing. */
   int32_t decode_workers;
   /* Longest decode piece, in 32-key steps (0 = automatic: 16, 32 when the
    * decode items hold at least 32768 steps, 64 from 65536; at most 64).  Shorter pieces

@@ -16,7 +16,7 @@
 //   extend blocks: one workgroup per block of <= 128 query columns of one
 //     request and one KV head, streaming the prefix and the causal suffix
 //     through an LDS ring; rows written directly.
-//   decode: persistent workgroups.  The decode items (an agent's prefix
+//   decode: one workgroup per piece, or persistent ones.  The decode items (an agent's prefix
 //     against a block of its decode rows, a request's suffix against its own
 //     rows; one KV head each) are cut into pieces of at most 64 32-key
 //     steps, listed longest first and dealt to the workgroups in rounds; a
@@ -801,13 +801,13 @@ __global__ __launch_bounds__(256, 2) void extend_kernel(AttnArgs a) {
 // ---------------------------------------------------------------------------
 // Decode.
 //
-// Persistent workgroups, each running a fixed list of pieces (round r of the
-// longest-first list gives workgroup b piece r S + b on even rounds and
-// r S + S - 1 - b on odd ones) through one LDS ring: every piece contributes
-// a Q stage (its query rows, each wave's 16 columns in its quarter of the
-// stage) and then its K/V steps, and stage u is refilled with stage
-// u + kStages - 1 whatever piece that belongs to, so a piece boundary does
-// not drain the ring.  A piece's descriptor (header, rows, page blocks)
+// S workgroups (by default one per piece), each running a fixed list of
+// pieces through one LDS ring.  Round r of the longest-first list gives
+// workgroup b piece r S + b on even rounds and r S + S - 1 - b on odd ones.
+// Every piece contributes a Q stage (its query rows, each wave's 16
+// columns in its quarter of the stage) and then its K/V steps, and stage u
+// is refilled with stage u + kStages - 1 whatever piece that belongs to, so
+// a piece boundary does not drain the ring.  A piece's descriptor (header, rows, page blocks)
 // comes into one of kPieceSlots LDS slots by a direct copy that wave 0
 // issues with the Q stage two pieces earlier; it is complete once that stage
 // has been waited for, long before the issue reaches the piece.
@@ -1215,14 +1215,9 @@ extern "C" int pfx_attention(const pfx_pool* pool, const pfx_plan* p, const void
   a.group_shift = __builtin_ctz(static_cast<unsigned>(p->group));
   a.scale_log2 = sm_scale * kLog2e;
   a.num_pieces = p->num_segs;
-  a.num_workers = p->decode_workers;
-  if (a.num_workers <= 0) {
-    int dev = 0, ncu = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || ncu <= 0)
-      return fail(PFX_EHIP, "pfx_attention: cannot read the compute-unit count");
-    a.num_workers = 2 * ncu;
-  }
+  // By default one workgroup per piece: the dispatcher hands them out as
+  // compute units free up (two fit on one), in list order, longest first.
+  a.num_workers = p->decode_workers > 0 ? p->decode_workers : p->num_segs;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (p->d == 128) launch_all<128>(a, p, s); else launch_all<64>(a, p, s);
   return check_launch("pfx_attention");
