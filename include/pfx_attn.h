@@ -167,8 +167,8 @@ typedef struct pfx_plan_opts {
    * are pieces).  The work division does not depend on it, only its
    * timing. */
   int32_t decode_workers;
-  /* Longest decode piece, in 32-key steps (0 = automatic: 16, 32 when the
-   * decode items hold at least 32768 steps, 64 from 65536; at most 64).  Shorter pieces
+  /* Longest decode piece, in 32-key steps (0 = automatic: 16, or 64 when
+   * the decode items hold at least 32768 steps; at most 64).  Shorter pieces
    * balance the workgroups better but give each decode row more partial
    * results to merge. */
   int32_t piece_steps;

@@ -37,13 +37,13 @@ static size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 static int64_t pages_for(int64_t tokens) { return (tokens + PFX_PAGE_SIZE - 1) / PFX_PAGE_SIZE; }
 
-// Longest decode piece by default, in steps: 16; 32 once the decode items
-// hold at least kLongPiecesFrom steps (64 for each workgroup of a
-// 512-workgroup launch); 64 from twice that.  Every piece costs a Q stage,
+// Longest decode piece by default, in steps: 16, or 64 once the decode
+// items hold at least kLongPiecesFrom steps.  Every piece costs a Q stage,
 // a partial state and its share of the merge; shorter pieces balance a
 // small launch better.
 constexpr int32_t kDefaultPieceSteps = 16;
-constexpr int64_t kLongPiecesFrom = 64 * 512;
+constexpr int32_t kLongPieceSteps = 64;
+constexpr int64_t kLongPiecesFrom = 32768;
 
 DevPlan dev_plan(const pfx_plan* p) {
   unsigned char* base = static_cast<unsigned char*>(p->dev_ws);
@@ -380,7 +380,7 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   if (piece_steps == 0) {
     int64_t steps = 0;
     for (const DItem& x : dit) steps += (x.keys + kStepKeys - 1) / kStepKeys;
-    piece_steps = steps >= 2 * kLongPiecesFrom ? 64 : steps >= kLongPiecesFrom ? 32 : kDefaultPieceSteps;
+    piece_steps = steps >= kLongPiecesFrom ? kLongPieceSteps : kDefaultPieceSteps;
   }
   {
     size_t total = 0;

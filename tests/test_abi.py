@@ -431,15 +431,15 @@ def test_plan_host_image_reuse_never_touches_a_live_plan():
 
 
 def test_default_piece_length_follows_the_launch_size():
-    # 16 steps below 32768 decode steps, 32 below 65536, 64 from there; an
-    # explicit piece_steps wins.
-    for cfg, want in ((2, 16), (4, 32), (5, 64)):
+    # 16 steps below 32768 decode steps, 64 from there; an explicit
+    # piece_steps wins.
+    for cfg, want in ((2, 16), (4, 64), (5, 64)):
         b = W.config_batch(cfg)
         p = plan_for(b)
         segs = p.export(3)
         steps = p.stats().num_decode_steps
-        assert int(segs[:, 3].max()) == want, (cfg, steps)
-        assert (steps >= 65536) == (want == 64) and (steps >= 32768) == (want >= 32)
+        assert want // 2 < int(segs[:, 3].max()) <= want, (cfg, steps)   # items are cut evenly
+        assert (steps >= 32768) == (want == 64)
     p = plan_for(W.config_batch(5), piece_steps=16)
     assert int(p.export(3)[:, 3].max()) == 16
     with pytest.raises(B.PfxError):
