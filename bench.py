@@ -18,7 +18,7 @@ working set exceeds the 256 MB last-level cache.
 U[256, 2048] prefilled against their agent's prefix; TFLOP/s over the
 causal-exact flop count.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-extend] [--more]
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-extend] [--no-configs] [--more]
 """
 
 from __future__ import annotations
@@ -42,7 +42,7 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def timed_steps(fn_step, fn_attn, steps, warmup, torch):
+def timed_steps(fn_step, fn_attn, steps, warmup, torch, group=10):
     """Run warmup + timed steps; returns (ms per step, mean ms of the
     attention call measured with events on the launch stream).
 
@@ -67,21 +67,36 @@ def timed_steps(fn_step, fn_attn, steps, warmup, torch):
     step_ms = max(wall, e0.elapsed_time(e1) / steps)
     # The attention pass in groups of (up to) 10 back-to-back calls, one event
     # pair per group: the mean over all calls, and the spread over groups.
-    group = 10
-    evs = []
+    attn, spread = attention_ms(fn_attn, max(steps, MIN_ATTN_CALLS), torch, group=group)
+    return step_ms, attn, spread
+
+
+# Attention is timed over at least this many calls, whatever --steps is.
+MIN_ATTN_CALLS = 100
+
+
+def attention_ms(fn_attn, calls, torch, group=10):
+    """Mean ms of ``calls`` attention calls (rounded up to whole groups),
+    launched back to back on the current stream in groups of ``group`` under
+    one event pair each; p10 / p50 / p90 over the groups."""
+    stream = torch.cuda.current_stream()
+    for i in range(3):
+        fn_attn(i)
     torch.cuda.synchronize()
-    for g0 in range(0, steps, group):
+    calls = (calls + group - 1) // group * group
+    evs = []
+    for g0 in range(0, calls, group):
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record(stream)
-        for i in range(g0, min(steps, g0 + group)):
+        for i in range(g0, g0 + group):
             fn_attn(i)
         b.record(stream)
-        evs.append((a, b, min(steps, g0 + group) - g0))
+        evs.append((a, b))
     torch.cuda.synchronize()
-    per = sorted(a.elapsed_time(b) / n for a, b, n in evs)
-    attn = sum(a.elapsed_time(b) for a, b, _ in evs) / steps
+    per = sorted(a.elapsed_time(b) / group for a, b in evs)
+    mean = sum(a.elapsed_time(b) for a, b in evs) / calls
     pct = lambda q: per[min(len(per) - 1, int(round(q * (len(per) - 1))))]
-    return step_ms, attn, {"p10": pct(0.1), "p50": pct(0.5), "p90": pct(0.9)}
+    return mean, {"p10": pct(0.1), "p50": pct(0.5), "p90": pct(0.9), "calls": calls}
 
 
 def bench_decode(args, torch, B, RN, W):
@@ -174,6 +189,8 @@ def graph_replay_ms(plans, ds, steps, torch, B):
 
 
 def bench_extend(args, torch, B, RN, W):
+    """Extend-8B (config 3): steps of append + attention, then attention and
+    append each timed back to back on their own."""
     b = W.config_batch(3)
     hv = W.host_values_fast(b, 2003)
     ds = RN.DeviceStep(b, hv, poison=False)
@@ -186,10 +203,12 @@ def bench_extend(args, torch, B, RN, W):
     def attn(i):
         B.pfx_attention(ds.pool, ds.plan, ds.q, ds.o, ds.lse)
 
-    steps = max(3, args.steps // 4)
-    ms, attn_ms, _ = timed_steps(step, attn, steps, max(1, args.warmup // 4), torch)
+    steps = max(20, args.steps)
+    ms, attn_ms, spread = timed_steps(step, attn, steps, max(2, args.warmup), torch, group=5)
+    append_ms = events_ms(lambda: B.pfx_append_kv(ds.pool, ds.plan, ds.k_new, ds.v_new), 20, torch)
     B.pfx_sync_check()
-    return dict(ms=ms, attn_ms=attn_ms, flops=b.attention_flops(), steps=steps)
+    return dict(batch=b, hv=hv, ms=ms, attn_ms=attn_ms, spread=spread, append_ms=append_ms,
+                flops=b.attention_flops(), steps=steps)
 
 
 def cpu_baseline(res, W, seconds=12.0):
@@ -225,6 +244,43 @@ def cpu_baseline(res, W, seconds=12.0):
     return {"value": round(nbytes / dt / 1e9, 4), "unit": "GB/s", "cores": cores, "kind": "oracle",
             "sample": f"{done} decode requests (all 32 heads each; the 64-request decode-8B step cycled) in "
                       f"{dt:.1f} s, fp64 numpy oracle, BLAS threads {threads}"}
+
+
+def cpu_baseline_extend(res, W, seconds=12.0, rows_per_call=64):
+    """The fp64 oracle on a bounded sample of the extend-8B step: blocks of
+    ``rows_per_call`` consecutive query rows (all 32 heads) of one request at
+    a time, requests in turn, each block at a seeded random offset, until
+    ``seconds`` of CPU work; throughput in causal-exact TFLOP/s of the rows
+    computed."""
+    import numpy as np
+
+    import oracle
+
+    b, hv = res["batch"], res["hv"]
+    cores = len(os.sched_getaffinity(0))
+    index = {int(p): i for i, p in enumerate(hv.pages)}
+    pp = [np.array([index[int(p)] for p in pl]) for pl in b.prefix_pages]
+    sp = [np.array([index[int(p)] for p in pl]) for pl in b.suffix_pages]
+    kp, vp = oracle.append_kv(hv.k_pages, hv.v_pages, sp, b.suffix_len, b.n_rows, hv.k_new, hv.v_new)
+    rng = np.random.default_rng(3003)
+    t0 = time.perf_counter()
+    done, flops, nrows = 0, 0, 0
+    while time.perf_counter() - t0 < seconds:
+        r = done % len(b.agent)
+        n, L, P = int(b.n_rows[r]), int(b.suffix_len[r]), int(b.prefix_len[int(b.agent[r])])
+        i0 = int(rng.integers(0, max(1, n - rows_per_call + 1)))
+        rows = list(range(i0, min(n, i0 + rows_per_call)))
+        oracle.prefix_shared_attention(kp, vp, pp, b.prefix_len, b.agent, sp, b.suffix_len, b.n_rows, hv.q,
+                                       b.num_q_heads, rows={r: rows})
+        flops += sum(4 * b.head_dim * b.num_q_heads * (P + L - n + i + 1) for i in rows)
+        nrows += len(rows)
+        done += 1
+    dt = time.perf_counter() - t0
+    threads = os.environ.get("OMP_NUM_THREADS", "unset")
+    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+            "sample": f"{nrows} extend rows (all 32 heads each) in {done} blocks of up to {rows_per_call} "
+                      f"consecutive rows of one request, requests of the extend-8B step in turn, in {dt:.1f} s; "
+                      f"fp64 numpy oracle, BLAS threads {threads}"}
 
 
 def copy_calibration(torch, B):
@@ -293,13 +349,13 @@ def events_ms(fn, n, torch, warm=3):
     return e0.elapsed_time(e1) / n
 
 
-def bench_more(torch, B, RN, W):
-    """The other workloads, timed on request (--more): the tiny config-1
-    extend (launch-bound, reported only), config 4 (the pinned-host gather
-    of 4 evicted prefixes, then decode over all 16 agents in the 48 GiB
-    pool), config 5 (80 layers' pools; the mixed launch, and its decode
-    and extend requests planned apart), prefix movement, the rebuild of a
-    preempted request and the service-time tables."""
+def bench_configs(torch, B, RN, W):
+    """The other three workloads, in the default run: the tiny config-1
+    extend and decode (launch-bound, reported only), config 4 (the
+    pinned-host gather of 4 evicted prefixes, then decode over all 16 agents
+    in the 48 GiB pool) and config 5 (80 layers' pools; its decode requests,
+    its extend requests and the mixed batch, each planned once and called
+    per layer)."""
     import dataclasses
 
     import numpy as np
@@ -307,20 +363,31 @@ def bench_more(torch, B, RN, W):
     res = {}
     b = W.config_batch(1)
     ds = RN.DeviceStep(b, W.host_values_fast(b, 1001), poison=False)
-    res["config1_extend_attn_us"] = round(
-        events_ms(lambda: B.pfx_attention(ds.pool, ds.plan, ds.q, ds.o, ds.lse), 200, torch) * 1e3, 2)
-    del ds
+    ext_ms, ext_sp = attention_ms(lambda i: B.pfx_attention(ds.pool, ds.plan, ds.q, ds.o, ds.lse), 200, torch)
+    sb = W.tiny_decode_step(b, 0, sorted(set(range(b.num_pages)) - set(int(p) for p in b.used_pages()))[:4])
+    plan1 = B.plan_from_batch(ds.pool, sb, B.PFX_MODE_DECODE).upload()
+    q1 = torch.zeros((4, 8, 64), dtype=torch.bfloat16, device="cuda")
+    o1 = torch.empty_like(q1)
+    l1 = torch.empty((4, 8), dtype=torch.float32, device="cuda")
+    dec_ms, dec_sp = attention_ms(lambda i: B.pfx_attention(ds.pool, plan1, q1, o1, l1), 200, torch)
+    res["config1"] = {"workload": "tiny: Hq8/Hkv2/d64, one 128-token prefix, 4 reqs x 32-token suffix",
+                      "extend_attn_us": round(ext_ms * 1e3, 2), "decode_step_attn_us": round(dec_ms * 1e3, 2),
+                      "note": "launch-bound; reported, not targeted"}
+    del ds, plan1
 
     b = W.config_batch(4)
     evicted = [int(a) for a in b.meta["evicted"]]
     ds = RN.DeviceStep(b, W.host_values_fast(b, 2004), host_resident=evicted, poison=False)
     moved = 2 * len(ds.host_dst) * b.num_kv_heads * 16 * b.head_dim * 2
     g_ms = events_ms(ds.gather_evicted, 5, torch, warm=1)
-    a_ms = events_ms(lambda: B.pfx_attention(ds.pool, ds.plan, ds.q, ds.o, ds.lse), 50, torch)
+    a_ms, a_sp = attention_ms(lambda i: B.pfx_attention(ds.pool, ds.plan, ds.q, ds.o, ds.lse), MIN_ATTN_CALLS, torch)
     u = b.unique_kv_bytes()
-    res["config4"] = {"decode_attn_us": round(a_ms * 1e3, 2), "unique_kv_bytes": u,
-                      "decode_GBs": round(u / (a_ms * 1e-3) / 1e9, 1),
-                      "decode_frac": round(u / (a_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+    gbs = u / (a_ms * 1e-3) / 1e9
+    res["config4"] = {"workload": "hetero-8B: 16 prefixes log-U[512,8192], 256 decode reqs Zipf(1.1), suffix "
+                                  "U[32,1024], 48 GiB pool; 4 evicted prefixes gathered from pinned host first",
+                      "decode_attn_us": round(a_ms * 1e3, 2),
+                      "attn_us_p10_p50_p90": [round(a_sp[k] * 1e3, 2) for k in ("p10", "p50", "p90")],
+                      "unique_kv_bytes": u, "decode_GBs": round(gbs, 1), "decode_frac": round(gbs / HBM_PEAK_GBS, 4),
                       "gather_bytes": moved, "gather_ms": round(g_ms, 4),
                       "gather_GBs_pcie_inclusive": round(moved / (g_ms * 1e-3) / 1e9, 1)}
     del ds
@@ -334,13 +401,19 @@ def bench_more(torch, B, RN, W):
     shape = (b.num_pages, hkv, 16, d)
     base_k = torch.randn(shape, dtype=torch.bfloat16, device="cuda", generator=gen)
     base_v = torch.randn(shape, dtype=torch.bfloat16, device="cuda", generator=gen)
-    pools = [B.make_pool(b.num_pages, hkv, d, torch.roll(base_k, 977 * l + 1, 0), torch.roll(base_v, 1489 * l + 3, 0))
-             for l in range(layers)]
+    # Each layer's pool tensors stay referenced for as long as the
+    # descriptors (which hold raw pointers) are used.
+    keep = [(torch.roll(base_k, 977 * l + 1, 0), torch.roll(base_v, 1489 * l + 3, 0)) for l in range(layers)]
+    pools = [B.make_pool(b.num_pages, hkv, d, kt, vt) for kt, vt in keep]
     del base_k, base_v
     dec_only = dataclasses.replace(b, n_rows=np.where(b.n_rows == 1, b.n_rows, 0).astype(np.int32))
     ext_only = dataclasses.replace(b, n_rows=np.where(b.n_rows > 1, b.n_rows, 0).astype(np.int32))
-    out5 = {"layers": layers}
-    for name, bb in (("mixed", b), ("decode", dec_only), ("extend", ext_only)):
+    u5 = dec_only.unique_kv_bytes()
+    f5 = ext_only.attention_flops()
+    out5 = {"workload": "mixed-70B: Hq64/Hkv8/d128, 8 prefixes x 8192; per layer 32 extend reqs (suffix "
+                        "U[512,4096]) + 448 decode reqs (suffix U[64,2048]); 80 layers' pools, 2.6 GB each",
+            "layers": layers, "decode_unique_kv_bytes_per_layer": u5, "extend_flops_per_layer": f5}
+    for name, bb in (("decode", dec_only), ("extend", ext_only), ("mixed", b)):
         t = bb.num_tokens
         q = torch.randn((t, hq, d), dtype=torch.bfloat16, device="cuda", generator=gen)
         o = torch.empty_like(q)
@@ -356,22 +429,28 @@ def bench_more(torch, B, RN, W):
         torch.cuda.synchronize()
         ms = e0.elapsed_time(e1)
         rec = {"ms_80_layers": round(ms, 3)}
-        if name in ("mixed", "decode"):
-            u = dec_only.unique_kv_bytes() * layers
-            rec["decode_GBs"] = round(u / (ms * 1e-3) / 1e9, 1) if name == "decode" else None
-        if name in ("mixed", "extend"):
-            f = ext_only.attention_flops() * layers
-            rec["extend_TFs"] = round(f / (ms * 1e-3) / 1e12, 1) if name == "extend" else None
-        if name == "mixed":
-            bound = max(dec_only.unique_kv_bytes() / (HBM_PEAK_GBS * 1e9),
-                        (ext_only.attention_flops() + dec_only.attention_flops()) / (BF16_PEAK_TFLOPS * 1e12))
-            rec["peak_bound_ms_80_layers"] = round(bound * layers * 1e3, 3)
-            rec = {k: v for k, v in rec.items() if v is not None}
-        out5[name] = {k: v for k, v in rec.items() if v is not None}
+        if name == "decode":
+            g = u5 * layers / (ms * 1e-3) / 1e9
+            rec.update(GBs=round(g, 1), frac=round(g / HBM_PEAK_GBS, 4))
+        elif name == "extend":
+            tf = f5 * layers / (ms * 1e-3) / 1e12
+            rec.update(TFLOPs=round(tf, 1), frac=round(tf / BF16_PEAK_TFLOPS, 4))
+        else:
+            bound = max(u5 / (HBM_PEAK_GBS * 1e9),
+                        (f5 + dec_only.attention_flops()) / (BF16_PEAK_TFLOPS * 1e12)) * layers * 1e3
+            rec.update(peak_bound_ms_80_layers=round(bound, 3), frac_of_bound=round(bound / ms, 4))
+        out5[name] = rec
         del q, o, lse, plan
     res["config5"] = out5
-    del pools
+    del pools, keep
     torch.cuda.empty_cache()
+    return res
+
+
+def bench_extras(torch, B, RN, W):
+    """Timed on request (--more): prefix movement, the rebuild of a
+    preempted request and the service-time tables."""
+    res = {}
     res["movement"] = bench_movement(torch, B, RN, W)
     res["rebuild"] = bench_rebuild(torch, B, RN, W)
     from paper_2608_25523_amd import service as SV
@@ -516,7 +595,9 @@ def main():
     ap.add_argument("--replicas", type=int, default=10)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-extend", action="store_true")
-    ap.add_argument("--more", action="store_true", help="also time configs 1, 4 and 5 (adds about a minute)")
+    ap.add_argument("--no-configs", action="store_true", help="skip configs 1, 4 and 5 (about a minute)")
+    ap.add_argument("--more", action="store_true",
+                    help="also time prefix movement, the rebuild of a preempted request and the service tables")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run a 1 GiB device copy (counter calibration for rocprofv3 --pmc runs)")
     args = ap.parse_args()
@@ -542,15 +623,26 @@ def main():
     if not args.no_extend:
         log("extend-8B: building inputs")
         ext = bench_extend(args, torch, B, RN, W)
-        log(f"extend-8B: {ext['ms']:.3f} ms/step, attention {ext['attn_ms']:.3f} ms")
-    more = None
-    if args.more:
+        log(f"extend-8B: {ext['ms']:.3f} ms/step, attention {ext['attn_ms']:.3f} ms, "
+            f"append {ext['append_ms']:.3f} ms")
+    configs = None
+    if not args.no_configs:
         log("configs 1, 4, 5")
-        more = bench_more(torch, B, RN, W)
-    cpu = None
+        configs = bench_configs(torch, B, RN, W)
+        log(f"config4 decode {configs['config4']['decode_attn_us']} us; config5 "
+            f"decode {configs['config5']['decode']['ms_80_layers']} ms, extend "
+            f"{configs['config5']['extend']['ms_80_layers']} ms (80 layers)")
+    extras = None
+    if args.more:
+        log("movement, rebuild, service tables")
+        extras = bench_extras(torch, B, RN, W)
+    cpu = cpu_ext = None
     if not args.no_cpu:
-        log("cpu baseline (oracle)")
+        log("cpu baseline (oracle): decode-8B")
         cpu = cpu_baseline(dec, W)
+        if ext is not None:
+            log("cpu baseline (oracle): extend-8B")
+            cpu_ext = cpu_baseline_extend(ext, W)
 
     u = dec["unique_bytes"]
     value = u / (dec["ms"] * 1e-3) / 1e9
@@ -579,7 +671,7 @@ def main():
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic_from_profile("decode"),
                      "measured_peak": round(copy_gbs, 1), "frac_measured": round(achieved / copy_gbs, 4),
                      "measured_peak_kind": "pfx_page_copy device to device, random 32 KiB pages, read + write",
-                     "attn_us": round(dec["attn_ms"] * 1e3, 3),
+                     "attn_us": round(dec["attn_ms"] * 1e3, 3), "attn_calls": dec["spread"]["calls"],
                      "attn_us_p10_p50_p90": [round(dec["spread"][k] * 1e3, 3) for k in ("p10", "p50", "p90")]},
         "graph_ms_per_step": None if dec["graph_ms"] is None else round(dec["graph_ms"], 5),
         "step_parts": dec["side"],
@@ -590,13 +682,18 @@ def main():
         out["extend"] = {
             "workload": "extend-8B: Hq32/Hkv8/d128, 3 prefixes x 4096, 32 reqs suffix U[256,2048]",
             "value": round(ext["flops"] / (ext["ms"] * 1e-3) / 1e12, 2), "unit": "TFLOP/s",
-            "ms_per_step": round(ext["ms"], 4), "steps": ext["steps"],
+            "ms_per_step": round(ext["ms"], 4), "steps": ext["steps"], "append_ms": round(ext["append_ms"], 4),
             "roofline": {"bound": "mfma", "kernel": "pfx_attention: extend_kernel", "achieved": round(tf, 2),
                          "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(tf / BF16_PEAK_TFLOPS, 4),
-                         "traffic": traffic_from_profile("extend"), "flops": ext["flops"]},
+                         "traffic": traffic_from_profile("extend"), "flops": ext["flops"],
+                         "attn_ms": round(ext["attn_ms"], 4), "attn_calls": ext["spread"]["calls"],
+                         "attn_ms_p10_p50_p90": [round(ext["spread"][k], 4) for k in ("p10", "p50", "p90")]},
+            "cpu_baseline": cpu_ext,
         }
-    if more is not None:
-        out["more_configs"] = more
+    if configs is not None:
+        out.update(configs)
+    if extras is not None:
+        out["extras"] = extras
     print(json.dumps(out), flush=True)
 
 

@@ -20,8 +20,6 @@ constexpr int kTileWaves = 4;
 // block (32 per wave).
 constexpr int kDecodeTileCols = kTileWaves * 16;
 constexpr int kExtendTileCols = kTileWaves * 32;
-// Page ids one extend block may reference (its LDS page table).
-constexpr int kMaxTilePages = 1024;
 // Keys processed per inner step (two 16-token pages).
 constexpr int kStepKeys = 32;
 
@@ -151,5 +149,8 @@ namespace pfx {
 // Thread-local error text, set by every failing entry point.
 int fail(int code, const char* fmt, ...);
 void clear_error();
-pfx::DevPlan dev_plan(const pfx_plan* p);
+// Device pointers of the plan's tables and partial states in a copy of its
+// workspace image at `base` (the uploaded workspace by default).
+pfx::DevPlan dev_plan(const pfx_plan* p, void* base);
+inline pfx::DevPlan dev_plan(const pfx_plan* p) { return dev_plan(p, p->dev_ws); }
 }  // namespace pfx

@@ -673,26 +673,58 @@ __device__ __forceinline__ void write_rows(const AttnArgs& a, const f32x4 (&acc)
   if (a.lse && grp == 0) a.lse[orow] = lse_nat;
 }
 
-// Issue this wave's share of an extend block's step st into a stage buffer:
-// tile (wave & 1) of K (waves 0, 1) or of V (waves 2, 3).
-template <int D>
-__device__ __forceinline__ void issue_block_step(unsigned char* stage, const AttnArgs& a, const Item& it,
-                                                 const int* ptab, int lead, const StepMarks& mk, int st, int h,
-                                                 int wave, const uint32_t (&voff)[TileGeom<D>::loads_per_wave]) {
-  using TG = TileGeom<D>;
+// The page ids of an extend block -- its page table, segment 0's pages then
+// segment 1's -- reach each wave as it needs them: a window of 64
+// consecutive entries, one per lane (`cur`, entries w0 .. w0 + 63), and the
+// window after it (`next`), requested when the wave moves into `cur`, about
+// 32 steps before it is needed.  So a block may stream any number of pages.
+struct PageWindow {
+  const int32_t* list;  // the plan's page list
+  int32_t s0_at, s1_at; // where the table's entries of segment 0 and of segment 1 start in it
+  int32_t p0n, ntab;    // entries of segment 0; of the whole table
+  int32_t w0;           // first entry held in cur
+  int32_t cur, next;
+};
+
+__device__ __forceinline__ int window_entry(const PageWindow& w, int e) {
+  if (e >= w.ntab) return 0;
+  return e < w.p0n ? w.list[w.s0_at + e] : w.list[w.s1_at + e - w.p0n];
+}
+
+// Page-table entry of this wave's tile (wave & 1) of step st.
+__device__ __forceinline__ int step_entry(const StepMarks& mk, int st, int wave) {
   const int t = wave & 1;
-  const bool is_v = wave >> 1;
   int idx = 2 * st + t + (st >= mk.s0_steps ? mk.d1 : 0);
   if (t == 1 && (st == mk.half0 || st == mk.half1)) idx -= 1;  // a missing second page re-reads the first (masked later)
-  // The block's leading page ids sit one per lane in `lead`; later ones in the LDS table.
-  const int page = __builtin_amdgcn_readfirstlane(idx < kItemPages ? __builtin_amdgcn_readlane(lead, idx) : ptab[idx]);
-  const uint16_t* base = (is_v ? a.vpool : a.kpool) + (size_t(page) * a.hkv + h) * (16 * D);
+  return idx;
+}
+
+// Issue this wave's share of an extend block's step st into a stage buffer:
+// tile (wave & 1) of K (waves 0, 1) or of V (waves 2, 3), from page `page`.
+template <int D>
+__device__ __forceinline__ void issue_block_copy(unsigned char* stage, const AttnArgs& a, int page, int h, int wave,
+                                                 const uint32_t (&voff)[TileGeom<D>::loads_per_wave]) {
+  using TG = TileGeom<D>;
+  const uint16_t* base = ((wave >> 1) ? a.vpool : a.kpool) + (size_t(page) * a.hkv + h) * (16 * D);
   copy_block_to_lds(base, voff, lds_address(stage) + wave * TG::page_bytes);
 }
 
-// LDS bytes of an extend block: the ring, then the page table.
+// Step st's page through the window.  Entries grow by at most 3 from one of
+// this wave's steps to the next, so a step either finds its entry in cur or
+// moves one window on (its successor, requested 64 entries earlier, has
+// arrived: every pair waits for all of the wave's memory operations).
+__device__ __forceinline__ int window_page(PageWindow& pw, int idx, int lane) {
+  if (idx >= pw.w0 + 64) {
+    pw.w0 += 64;
+    pw.cur = pw.next;
+    pw.next = window_entry(pw, pw.w0 + 64 + lane);
+  }
+  return __builtin_amdgcn_readfirstlane(__builtin_amdgcn_readlane(pw.cur, idx - pw.w0));
+}
+
+// LDS bytes of an extend block: the ring.
 template <int D>
-constexpr int extend_smem_bytes() { return kStages * TileGeom<D>::stage_bytes + kMaxTilePages * 4; }
+constexpr int extend_smem_bytes() { return kStages * TileGeom<D>::stage_bytes; }
 
 // One extend block (QBW blocks of 16 columns per wave): its K/V streams once
 // through the LDS ring, two steps at a time; at every pair each wave waits
@@ -705,7 +737,6 @@ __device__ __forceinline__ void extend_block(const AttnArgs& a, const Item* itp,
   constexpr int KS = D / 32;
   constexpr int NS = kStages;
   auto ring = reinterpret_cast<unsigned char (*)[TG::stage_bytes]>(smem);
-  int* ptab = reinterpret_cast<int*>(smem + NS * TG::stage_bytes);
   const int lead = itp->first_pages[threadIdx.x & (kItemPages - 1)];  // issued before the block's scalar load
   const Item it = *itp;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -714,13 +745,21 @@ __device__ __forceinline__ void extend_block(const AttnArgs& a, const Item* itp,
   const int h = it.kv_head;
   const int G = a.group;
 
-  // Page ids of both segments, staged once per block.
+  // The block's page table: segment 0's pages, then segment 1's, read
+  // through a window of 64 entries per wave (the first two windows now).
   const int p0b = it.s0_kbeg >> 4;
   const int p0n = it.s0_kend > it.s0_kbeg ? ((it.s0_kend + 15) >> 4) - p0b : 0;
   const int p1b = it.s1_kbeg >> 4;
   const int p1n = it.s1_kend > it.s1_kbeg ? ((it.s1_kend + 15) >> 4) - p1b : 0;
-  for (int i = threadIdx.x; i < p0n + p1n; i += 256)
-    ptab[i] = i < p0n ? a.plan.page_list[it.s0_page_off + p0b + i] : a.plan.page_list[it.s1_page_off + p1b + i - p0n];
+  PageWindow pw;
+  pw.list = a.plan.page_list;
+  pw.s0_at = it.s0_page_off + p0b;
+  pw.s1_at = it.s1_page_off + p1b;
+  pw.p0n = p0n;
+  pw.ntab = p0n + p1n;
+  pw.w0 = 0;
+  pw.cur = window_entry(pw, lane);
+  pw.next = window_entry(pw, 64 + lane);
 
   // This wave's query columns: blocks wave*QBW .. wave*QBW + QBW - 1.
   const int ncols = it.row_count * G;
@@ -756,11 +795,12 @@ __device__ __forceinline__ void extend_block(const AttnArgs& a, const Item* itp,
   const int nsteps = mk.nsteps;
   uint32_t voff[TG::loads_per_wave];
   block_lane_offsets<D>(voff, lane);
-  // The first steps' pages are among the leading ids: request them before
-  // waiting for the page table.
+  // The first two steps' pages are among the leading ids (they travel in
+  // the block record, one per lane): request them before the page windows
+  // arrive.
   for (int st = 0; st < 2 && st < nsteps; ++st)
-    issue_block_step<D>(ring[st], a, it, ptab, lead, mk, st, h, wave, voff);
-  __syncthreads();  // page table ready
+    issue_block_copy<D>(ring[st], a, __builtin_amdgcn_readfirstlane(__builtin_amdgcn_readlane(lead, step_entry(mk, st, wave))),
+                        h, wave, voff);
   // Two steps per barrier: at pair q (steps 2q, 2q + 1) wait for both
   // stages, meet (so the stages of the previous pair are free), refill them
   // with steps 2q + 2 and 2q + 3, and run the pair.  Unrolled by two pairs,
@@ -776,9 +816,11 @@ __device__ __forceinline__ void extend_block(const AttnArgs& a, const Item* itp,
       wait_vmcnt(0);
       __syncthreads();
       if (st + 2 < nsteps)
-        issue_block_step<D>(ring[(2 * k + 2) % NS], a, it, ptab, lead, mk, st + 2, h, wave, voff);
+        issue_block_copy<D>(ring[(2 * k + 2) % NS], a, window_page(pw, step_entry(mk, st + 2, wave), lane), h, wave,
+                            voff);
       if (st + 3 < nsteps)
-        issue_block_step<D>(ring[(2 * k + 3) % NS], a, it, ptab, lead, mk, st + 3, h, wave, voff);
+        issue_block_copy<D>(ring[(2 * k + 3) % NS], a, window_page(pw, step_entry(mk, st + 3, wave), lane), h, wave,
+                            voff);
       // An odd last step pairs with an empty one (its stage is not being
       // refilled).
       if (nb > 0) extend_pair<D, QBW>(ws, ring[2 * k], ring[2 * k + 1], qf, lim, it, st, two, mk, lane, a.scale_log2);
@@ -1010,8 +1052,10 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
   }
 }
 
-// Decode rows: the log-sum-exp merge of the pieces' states (Sec. 4.2,
-// Eq. (8)).  One thread per (token, query head, group grp, block pair): it
+// Decode rows: the log-sum-exp merge of the pieces' states (softmax over a
+// union of disjoint key ranges, recombined exactly from each range's maximum,
+// sum and weighted values; the paper itself states no attention numerics).
+// One thread per (token, query head, group grp, block pair): it
 // reads elements i = 0..3 of blocks blk, blk + 1 of every piece, i.e. dims
 // 16 blk + 4 grp + i and 16 (blk + 1) + 4 grp + i, and writes them as two
 // runs of four bf16.  The first kMergeBatch pieces are all requested before
@@ -1174,16 +1218,11 @@ extern "C" int pfx_plan_upload(pfx_plan* p, void* ws, size_t bytes, void* stream
   return PFX_OK;
 }
 
-extern "C" int pfx_append_kv(const pfx_pool* pool, const pfx_plan* p, const void* k_new, const void* v_new,
-                             void* stream) {
-  int rc = check_pool_matches(pool, p, "pfx_append_kv");
-  if (rc) return rc;
-  if (p->num_tokens == 0) return PFX_OK;
-  if (!k_new || !v_new) return fail(PFX_EINVAL, "pfx_append_kv: k_new or v_new is NULL");
-  const DevPlan dp = dev_plan(p);
+// The KV append of a plan whose tables sit at dp (validated by the caller).
+static int launch_append(const pfx_pool* pool, const pfx_plan* p, const DevPlan& dp, const void* k_new,
+                         const void* v_new, hipStream_t s, const char* who) {
   const size_t total = 2 * size_t(p->num_tokens) * p->hkv * (p->d / 8);
   const dim3 grid((total + 255) / 256);
-  hipStream_t s = static_cast<hipStream_t>(stream);
   auto kn = static_cast<const uint16_t*>(k_new);
   auto vn = static_cast<const uint16_t*>(v_new);
   auto kp = static_cast<uint16_t*>(pool->k_pages);
@@ -1192,15 +1231,13 @@ extern "C" int pfx_append_kv(const pfx_pool* pool, const pfx_plan* p, const void
     hipLaunchKernelGGL(append_kernel<128>, grid, dim3(256), 0, s, kn, vn, kp, vp, dp.tok_slot, p->num_tokens, p->hkv);
   else
     hipLaunchKernelGGL(append_kernel<64>, grid, dim3(256), 0, s, kn, vn, kp, vp, dp.tok_slot, p->num_tokens, p->hkv);
-  return check_launch("pfx_append_kv");
+  return check_launch(who);
 }
 
-extern "C" int pfx_attention(const pfx_pool* pool, const pfx_plan* p, const void* q, void* o, float* lse,
-                             float sm_scale, void* stream) {
-  int rc = check_pool_matches(pool, p, "pfx_attention");
-  if (rc) return rc;
-  if (p->num_items == 0 && p->num_segs == 0) return PFX_OK;
-  if (!q || !o) return fail(PFX_EINVAL, "pfx_attention: q or o is NULL");
+// The attention launches of a plan whose tables and partial states sit at
+// dp (validated by the caller).
+static int launch_attention(const pfx_pool* pool, const pfx_plan* p, const DevPlan& dp, const void* q, void* o,
+                            float* lse, float sm_scale, hipStream_t s, const char* who) {
   if (!(sm_scale > 0.f)) sm_scale = 1.0f / sqrtf(float(p->d));
   AttnArgs a;
   a.kpool = static_cast<const uint16_t*>(pool->k_pages);
@@ -1208,7 +1245,7 @@ extern "C" int pfx_attention(const pfx_pool* pool, const pfx_plan* p, const void
   a.q = static_cast<const uint16_t*>(q);
   a.o = static_cast<uint16_t*>(o);
   a.lse = lse;
-  a.plan = dev_plan(p);
+  a.plan = dp;
   a.hq = p->hq;
   a.hkv = p->hkv;
   a.group = p->group;
@@ -1218,9 +1255,27 @@ extern "C" int pfx_attention(const pfx_pool* pool, const pfx_plan* p, const void
   // By default one workgroup per piece: the dispatcher hands them out as
   // compute units free up (two fit on one), in list order, longest first.
   a.num_workers = p->decode_workers > 0 ? p->decode_workers : p->num_segs;
-  hipStream_t s = static_cast<hipStream_t>(stream);
   if (p->d == 128) launch_all<128>(a, p, s); else launch_all<64>(a, p, s);
-  return check_launch("pfx_attention");
+  return check_launch(who);
+}
+
+extern "C" int pfx_append_kv(const pfx_pool* pool, const pfx_plan* p, const void* k_new, const void* v_new,
+                             void* stream) {
+  int rc = check_pool_matches(pool, p, "pfx_append_kv");
+  if (rc) return rc;
+  if (p->num_tokens == 0) return PFX_OK;
+  if (!k_new || !v_new) return fail(PFX_EINVAL, "pfx_append_kv: k_new or v_new is NULL");
+  return launch_append(pool, p, dev_plan(p), k_new, v_new, static_cast<hipStream_t>(stream), "pfx_append_kv");
+}
+
+extern "C" int pfx_attention(const pfx_pool* pool, const pfx_plan* p, const void* q, void* o, float* lse,
+                             float sm_scale, void* stream) {
+  int rc = check_pool_matches(pool, p, "pfx_attention");
+  if (rc) return rc;
+  if (p->num_items == 0 && p->num_segs == 0) return PFX_OK;
+  if (!q || !o) return fail(PFX_EINVAL, "pfx_attention: q or o is NULL");
+  return launch_attention(pool, p, dev_plan(p), q, o, lse, sm_scale, static_cast<hipStream_t>(stream),
+                          "pfx_attention");
 }
 
 extern "C" int pfx_merge_states(const float* o_parts, const float* lse_parts, int32_t num_parts, int32_t rows,

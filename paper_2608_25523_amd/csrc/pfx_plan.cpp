@@ -45,8 +45,8 @@ constexpr int32_t kDefaultPieceSteps = 16;
 constexpr int32_t kLongPieceSteps = 64;
 constexpr int64_t kLongPiecesFrom = 32768;
 
-DevPlan dev_plan(const pfx_plan* p) {
-  unsigned char* base = static_cast<unsigned char*>(p->dev_ws);
+DevPlan dev_plan(const pfx_plan* p, void* ws) {
+  unsigned char* base = static_cast<unsigned char*>(ws);
   DevPlan d;
   d.items = reinterpret_cast<const Item*>(base + p->off_items);
   d.row_tok = reinterpret_cast<const int32_t*>(base + p->off_row_tok);
@@ -231,18 +231,6 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   if (R > 0 && b->suffix_indptr[R] > 0 && !b->suffix_page_ids)
     return fail(PFX_EINVAL, "pfx_plan_create: suffix_page_ids is NULL");
 
-  // An extend row block streams its agent's whole prefix and its suffix in
-  // one workgroup whose page table holds kMaxTilePages ids.
-  for (int32_t r = 0; r < R; ++r) {
-    const int64_t n = int64_t(b->q_indptr[r + 1]) - b->q_indptr[r];
-    if (n * G <= kTileCols) continue;
-    const int32_t a = b->agent[r];
-    const int64_t pages = (a >= 0 ? pages_for(pt->prefix_len[a]) : 0) + pages_for(b->suffix_len[r]);
-    if (pages > kMaxTilePages)
-      return fail(PFX_EUNSUPPORTED, "pfx_plan_create: request %d extends over %lld pages (at most %d)", r,
-                  (long long)pages, kMaxTilePages);
-  }
-
   // ---- Sec. 3, Eq. (2): prefixes counted once, plus every request's own KV ----
   std::vector<uint8_t> referenced(A, 0);
   for (int32_t r = 0; r < R; ++r)
@@ -401,8 +389,8 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
 
   // ---- partial slots: a decode row of KV head h is seen by the pieces of
   // its prefix item (slots 0 ..) and then of its suffix item; every piece
-  // leaves its unnormalised state in a slot and the merge (Sec. 4.2,
-  // Eq. (8)) combines them into the row (a lone piece is just normalised) ----
+  // leaves its unnormalised state in a slot and the log-sum-exp merge
+  // combines them into the row (a lone piece is just normalised) ----
   // A decode request's rows are consecutive in the merge list, from
   // req_mrow[r]; merge_head[row * Hkv + h] holds their first slot and count.
   std::vector<int32_t> np_prefix(size_t(R) * hkv, 0), np_total(size_t(R) * hkv, 0), req_mrow(R, -1);

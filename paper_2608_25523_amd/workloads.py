@@ -358,3 +358,81 @@ def replicas(batch: Batch, count: int, seed: int) -> list:
         out.append(Batch(batch.num_q_heads, batch.num_kv_heads, batch.head_dim, batch.num_pages, batch.prefix_len,
                          pp, batch.agent, batch.suffix_len, batch.n_rows, sp, dict(batch.meta, replica=len(out))))
     return out
+
+
+def host_values_shaped(batch: Batch, seed: int, key_gain=None, q_gain: float = 1.0,
+                       v_gain: float = 1.0) -> HostValues:
+    """Like ``host_values``, with every value drawn N(0, 1) and multiplied
+    before rounding to bf16: a key at absolute position p (prefix token j of
+    an agent sits at p = j, suffix token j of request r at p = l_a(r) + j)
+    by ``key_gain(p)``, queries by ``q_gain`` and values by ``v_gain``.
+    A key gain that grows with p makes the largest scores rise along the
+    sequence, so a running maximum keeps being raised."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    hkv, d = batch.num_kv_heads, batch.head_dim
+    gain = key_gain or (lambda p: 1.0)
+    pages = np.unique(batch.used_pages())
+    index = {int(p): i for i, p in enumerate(pages)}
+    kp = np.full((len(pages), hkv, PAGE_SIZE, d), POISON_BF16, dtype=np.uint16)
+    vp = np.full_like(kp, POISON_BF16)
+
+    def draw(shape, g):
+        return bf16_round(rng.standard_normal(size=shape, dtype=np.float32) * np.float32(g))
+
+    def fill(page_list, length, base):
+        for j in range(length):
+            i = index[int(page_list[j // PAGE_SIZE])]
+            kp[i, :, j % PAGE_SIZE, :] = draw((hkv, d), gain(base + j))
+            vp[i, :, j % PAGE_SIZE, :] = draw((hkv, d), v_gain)
+
+    for a, pl in enumerate(batch.prefix_pages):
+        fill(pl, int(batch.prefix_len[a]), 0)
+    t = batch.num_tokens
+    kn = np.zeros((t, hkv, d), np.uint16)
+    vn = np.zeros_like(kn)
+    row = 0
+    for r, pl in enumerate(batch.suffix_pages):
+        a = int(batch.agent[r])
+        base = int(batch.prefix_len[a]) if a >= 0 else 0
+        n, L = int(batch.n_rows[r]), int(batch.suffix_len[r])
+        fill(pl, L - n, base)
+        for i in range(n):
+            kn[row] = draw((hkv, d), gain(base + L - n + i))
+            vn[row] = draw((hkv, d), v_gain)
+            row += 1
+    q = draw((t, batch.num_q_heads, d), q_gain)
+    return HostValues(pages, kp, vp, q, kn, vn)
+
+
+def plant_one_hot(batch: Batch, hv: HostValues, seed: int, alpha_log2: int = 4) -> HostValues:
+    """Queries aimed at one key each: for every query row and head, a seeded
+    visible key j* (its agent's prefix, or its own suffix up to and including
+    the row's own token) and q = 2^alpha_log2 * k[j*] (exact in bf16), so
+    that one score stands far above all others."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    index = {int(p): i for i, p in enumerate(hv.pages)}
+    g = batch.group
+    q = hv.q.copy()
+    shift = np.uint16(alpha_log2 << 7)   # add alpha_log2 to the bf16 exponent field
+    row = 0
+    for r in range(len(batch.agent)):
+        a = int(batch.agent[r])
+        P = int(batch.prefix_len[a]) if a >= 0 else 0
+        n, L = int(batch.n_rows[r]), int(batch.suffix_len[r])
+        for i in range(n):
+            visible = P + L - n + i + 1
+            for h in range(batch.num_q_heads):
+                j = int(rng.integers(0, visible))
+                if j < P:
+                    pg, slot = batch.prefix_pages[a][j // PAGE_SIZE], j % PAGE_SIZE
+                    k = hv.k_pages[index[int(pg)], h // g, slot]
+                elif j - P < L - n:
+                    s = j - P
+                    pg, slot = batch.suffix_pages[r][s // PAGE_SIZE], s % PAGE_SIZE
+                    k = hv.k_pages[index[int(pg)], h // g, slot]
+                else:
+                    k = hv.k_new[row - i + (j - P - (L - n)), h // g]
+                nz = (k & np.uint16(0x7F80)) != 0   # zeros stay zero; normal values scale exactly
+                q[row, h] = np.where(nz, k + shift, k)
+            row += 1
+    return HostValues(hv.pages, hv.k_pages, hv.v_pages, q, hv.k_new, hv.v_new)

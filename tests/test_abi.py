@@ -247,9 +247,14 @@ def enumerate_coverage(plan, batch):
     return counts, outs
 
 
-@pytest.mark.parametrize("case", ["small", "split", "g1", "g16", "decode_only"])
+@pytest.mark.parametrize("case", ["small", "split", "g1", "g2", "g16", "decode_only"])
 def test_plan_covers_every_visible_key_once(case):
-    if case == "small":
+    if case == "g2":
+        reqs = [(0, 140, 140), (0, 19, 3), (0, 5, 1), (0, 44, 8), (-1, 9, 9)] + [(1, 3 + i, 1) for i in range(40)]
+        b = W.make_batch(8, num_q_heads=16, num_kv_heads=8, head_dim=64, num_pages=256, prefix_len=[70, 33],
+                         agent=[r[0] for r in reqs], suffix_len=[r[1] for r in reqs], n_rows=[r[2] for r in reqs])
+        kw = dict(piece_steps=1)
+    elif case == "small":
         b, kw = small_batch(), {}
     elif case == "split":
         b, kw = small_batch(prefix_len=[100, 17], suffix_len=[70, 20, 33, 3, 40]), dict(decode_workers=7)
@@ -444,3 +449,16 @@ def test_default_piece_length_follows_the_launch_size():
     assert int(p.export(3)[:, 3].max()) == 16
     with pytest.raises(B.PfxError):
         plan_for(W.config_batch(2), piece_steps=65)
+
+
+
+def test_extend_blocks_take_any_key_count():
+    """An extend request over a 24,576-token prefix and a 17,000-token suffix
+    (2,600 pages, far more than a block could hold in a fixed table) plans:
+    only head_dim, page size and the query group are unsupported."""
+    b = W.make_batch(24, num_q_heads=32, num_kv_heads=8, head_dim=128, num_pages=4096, prefix_len=[24576],
+                     agent=[0, -1], suffix_len=[300, 17000], n_rows=[300, 64])
+    s = plan_for(b, mode=B.PFX_MODE_EXTEND).stats()
+    assert s.num_extend_items == 8 * (10 + 2) and s.num_tokens == 364   # 32 rows x 4 heads per block
+    blocks = plan_for(b, mode=B.PFX_MODE_EXTEND).export(0)
+    assert blocks[:, 6].max() == 24576                   # s0_kend: the whole prefix in one block's first segment

@@ -33,20 +33,58 @@ def _gpu():
     torch.cuda.synchronize()
 
 
-def run_and_check(batch, hv, label, rows=None, host_resident=(), check_pages=True, **kw):
+def assert_untouched(ds, used_pages, label, chunk=8192):
+    """Every pool page outside ``used_pages`` still holds the poison pattern
+    it was filled with (no stray append, gather or attention write); checked
+    on the device, chunk by chunk."""
+    import torch as T
+
+    used = T.zeros(ds.batch.num_pages, dtype=T.bool, device=ds.k_pool.device)
+    used[T.from_numpy(np.asarray(used_pages, np.int64)).to(ds.k_pool.device)] = True
+    for pool, name in ((ds.k_pool, "K"), (ds.v_pool, "V")):
+        bits = pool.view(T.int16)
+        for s in range(0, ds.batch.num_pages, chunk):
+            e = min(ds.batch.num_pages, s + chunk)
+            off = bits[s:e].reshape(e - s, -1).ne(W.POISON_BF16).any(dim=1) & ~used[s:e]
+            assert not bool(off.any()), f"{label}: {name} pool page {s + int(off.nonzero()[0, 0])} was written"
+
+
+def run_and_check(batch, hv, label, rows=None, host_resident=(), check_pages=True, parallel=False, sm_scale=0.0,
+                  with_lse=True, **kw):
     announce(f"{label}: tokens={batch.num_tokens} reqs={len(batch.agent)} Hq={batch.num_q_heads} "
-             f"Hkv={batch.num_kv_heads} d={batch.head_dim} pool={batch.num_pages} {kw}")
+             f"Hkv={batch.num_kv_heads} d={batch.head_dim} pool={batch.num_pages} sm_scale={sm_scale} "
+             f"lse={'yes' if with_lse else 'NULL'} {kw}")
     ds = RN.DeviceStep(batch, hv, host_resident=host_resident, **kw)
     ds.gather_evicted()
-    ds.step()
+    ds.append()
+    if with_lse:
+        ds.attention(sm_scale)
+    else:
+        ds.lse.fill_(float("nan"))
+        B.pfx_attention(ds.pool, ds.plan, ds.q, ds.o, None, sm_scale)
     B.pfx_sync_check()
     o_bits, lse = ds.outputs()
+    if not with_lse:
+        assert np.isnan(lse).all(), f"{label}: LSE written although none was passed"
+        lse = None
     exp_k, exp_v = PT.expected_pools(batch, hv)
     if check_pages:
         gk, gv = ds.read_pages(hv.pages)
         assert np.array_equal(gk, exp_k), f"{label}: K pool differs from the oracle's append"
         assert np.array_equal(gv, exp_v), f"{label}: V pool differs from the oracle's append"
-    o_ref, l_ref = PT.reference(batch, hv, (exp_k, exp_v), rows=rows)
+        if kw.get("poison", True):
+            assert_untouched(ds, hv.pages, label)
+    scale = sm_scale if sm_scale > 0 else None
+    if parallel:
+        want = rows if rows is not None else PT.all_rows(batch)
+        ck = PT.checker()
+        h = ck.submit(batch, hv.pages, exp_k, exp_v, PT.gather_rows(hv.q, batch, want),
+                      PT.gather_rows(o_bits, batch, want), None if lse is None else PT.gather_rows(lse, batch, want),
+                      want, scale=scale)
+        res = ck.collect(h, label)
+        announce(f"{label}: rows={res[3]} max_abs={res[0]:.2e} rel={res[1]:.2e} lse={res[2]:.2e}")
+        return ds, o_bits, lse
+    o_ref, l_ref = PT.reference(batch, hv, (exp_k, exp_v), rows=rows, scale=scale)
     res = PT.compare(batch, o_bits, lse, o_ref, l_ref, label)
     announce(f"{label}: max_abs={res[0]:.2e} rel={res[1]:.2e} lse={res[2]:.2e}")
     return ds, o_bits, lse
@@ -116,6 +154,12 @@ SMALL_CASES = [
     (6, 32, 8, 128, [16], [(0, 1, 0), (0, 33, 1), (-1, 64, 64)], {}),                 # a request with no rows
     # two workers asked for; the 16-segment limit of a worker adds more
     (7, 32, 8, 128, [50], [(0, 1 + i % 20, 1) for i in range(40)] + [(-1, 7, 4)], dict(decode_workers=2)),
+    # G = 2: 64-row extend blocks, 32-row prefix blocks (agent 1 has 40 decode rows: two blocks), multi-row
+    # causal decode requests (n * G <= 16), a request with no prefix
+    (8, 16, 8, 64, [70, 33], [(0, 140, 140), (0, 19, 3), (0, 5, 1), (0, 44, 8), (-1, 9, 9)]
+     + [(1, 3 + i, 1) for i in range(40)], {}),
+    (9, 16, 8, 128, [70, 33], [(0, 140, 140), (0, 19, 3), (0, 5, 1), (0, 44, 8), (-1, 9, 9)]
+     + [(1, 3 + i, 1) for i in range(40)], dict(piece_steps=1)),
 ]
 
 
@@ -126,6 +170,58 @@ def test_small_batches(case):
                      agent=[r[0] for r in reqs], suffix_len=[r[1] for r in reqs], n_rows=[r[2] for r in reqs])
     hv = W.host_values(b, seed + 50)
     run_and_check(b, hv, f"small{seed}", **opts)
+
+
+def small_batch(case):
+    seed, hq, hkv, d, plen, reqs, opts = case
+    need = sum((p + 15) // 16 for p in plen) + sum((r[1] + 15) // 16 for r in reqs)
+    b = W.make_batch(seed, num_q_heads=hq, num_kv_heads=hkv, head_dim=d, num_pages=max(256, 2 * need), prefix_len=plen,
+                     agent=[r[0] for r in reqs], suffix_len=[r[1] for r in reqs], n_rows=[r[2] for r in reqs])
+    return b, opts
+
+
+@pytest.mark.parametrize("sm_scale,with_lse", [(0.125, True), (0.02, False), (1.0 / math.sqrt(128), False)])
+def test_explicit_scale_and_no_lse(sm_scale, with_lse):
+    """sm_scale > 0 overrides 1/sqrt(d); a NULL lse pointer leaves the LSE
+    untouched while O is still written (extend, multi-row decode and shared
+    prefix decode rows)."""
+    b, opts = small_batch(SMALL_CASES[1])
+    hv = W.host_values(b, 60)
+    run_and_check(b, hv, f"scale{sm_scale:.4f}-lse{int(with_lse)}", sm_scale=sm_scale, with_lse=with_lse, **opts)
+
+
+# Peaked scores: the lazy rescale of the running maximum (raised only past a
+# slack) must take its non-trivial branch, with 0 < alpha < 1, mid-block and
+# mid-piece.
+PEAKED = [
+    # (seed, Hq, Hkv, d, prefix_len, reqs, opts)
+    (21, 32, 8, 128, [2048, 700], [(0, 300, 300), (1, 90, 90), (0, 200, 1), (1, 40, 1), (0, 37, 3)]
+     + [(i % 2, 30 + 11 * i, 1) for i in range(24)], dict(piece_steps=8)),
+    (22, 16, 8, 64, [1500], [(0, 257, 257), (0, 33, 1), (-1, 400, 400), (0, 120, 4)]
+     + [(0, 20 + 3 * i, 1) for i in range(30)], dict(piece_steps=3)),
+]
+
+
+@pytest.mark.parametrize("case", PEAKED, ids=[f"one-hot{c[0]}" for c in PEAKED])
+def test_peaked_one_hot(case):
+    """q = 16 k[j*] for a seeded visible key j* per row and head: one score
+    stands ~100 nats above the rest, and the output is v[j*]."""
+    seed, hq, hkv, d, plen, reqs, opts = case
+    b, _ = small_batch((seed, hq, hkv, d, plen, reqs, opts))
+    hv = W.plant_one_hot(b, W.host_values(b, seed + 1), seed + 2, alpha_log2=4)
+    run_and_check(b, hv, f"one-hot{seed}", **opts)
+
+
+@pytest.mark.parametrize("case", PEAKED, ids=[f"rising{c[0]}" for c in PEAKED])
+def test_peaked_rising_scores(case):
+    """Key norms growing along the sequence (gain 1 + p/256 at absolute
+    position p) and queries x4: the largest score rises step after step, so
+    the running maximum is raised again and again within blocks and pieces."""
+    seed, hq, hkv, d, plen, reqs, opts = case
+    b, _ = small_batch((seed, hq, hkv, d, plen, reqs, opts))
+    hv = W.host_values_shaped(b, seed + 3, key_gain=lambda p: 1.0 + p / 256.0, q_gain=4.0, v_gain=0.25)
+    run_and_check(b, hv, f"rising{seed}", **opts)
+    run_and_check(b, hv, f"rising{seed}-scale", sm_scale=0.25, **opts)
 
 
 def test_graph_replay_matches_eager():
@@ -265,11 +361,13 @@ def sample_rows(batch, rng, per=16):
     return rows
 
 
-def test_config3_extend_sampled_rows():
+@pytest.mark.timeout(600)
+def test_config3_extend_every_row():
+    """Extend-8B: all 36k rows x 32 heads against the oracle (run in parallel
+    worker processes, one job per request and KV head)."""
     b = W.config_batch(3)
     hv = W.host_values_fast(b, 2003)
-    rows = sample_rows(b, np.random.default_rng(3))
-    run_and_check(b, hv, "config3", rows=rows)
+    run_and_check(b, hv, "config3", parallel=True)
 
 
 def test_config3_shape_small_full():
@@ -281,18 +379,33 @@ def test_config3_shape_small_full():
     run_and_check(b, hv, "config3-small")
 
 
+@pytest.mark.parametrize("d,hq", [(128, 32), (64, 16)])
+def test_long_prefix_and_suffix(d, hq):
+    """A 24,576-token prefix (1536 pages) extended and decoded against, and a
+    17,000-token suffix with 64 query rows at its end: extend blocks stream
+    more page ids than any fixed table would hold."""
+    reqs = [(0, 300, 300), (0, 50, 1), (0, 1, 1), (-1, 17000, 64), (1, 40, 40), (0, 70, 1), (0, 33, 3)]
+    b = W.make_batch(24, num_q_heads=hq, num_kv_heads=8, head_dim=d, num_pages=4096, prefix_len=[24576, 1000],
+                     agent=[r[0] for r in reqs], suffix_len=[r[1] for r in reqs], n_rows=[r[2] for r in reqs])
+    hv = W.host_values_fast(b, 25)
+    run_and_check(b, hv, f"long-prefix-d{d}", parallel=True)
+
+
+@pytest.mark.timeout(600)
 def test_config4_gather_evicted_then_decode():
     b = W.config_batch(4)
     hv = W.host_values_fast(b, 2004)
     evicted = [int(a) for a in b.meta["evicted"]]
-    run_and_check(b, hv, "config4", host_resident=evicted)
+    run_and_check(b, hv, "config4", host_resident=evicted, parallel=True)
 
 
-@pytest.mark.timeout(600)
-def test_config5_80_layers_sampled():
+@pytest.mark.timeout(900)
+def test_config5_80_layers_every_layer():
     """70B-like mixed batch over 80 layers with independent pools (device-drawn
-    values); layer 0 and one seeded layer fully on decode rows and 16 rows per
-    extend request, 10% of decode requests on the other layers."""
+    values).  Every layer is checked: layer 0 and one seeded layer on all 448
+    decode rows and 16 rows per extend request, every other layer on a seeded
+    10% of the decode requests and 2 rows per extend request.  The oracle
+    runs in worker processes while the next layers compute."""
     b = W.config_batch(5)
     layers = int(b.meta["layers"])
     hkv, d, hq = b.num_kv_heads, b.head_dim, b.num_q_heads
@@ -325,43 +438,55 @@ def test_config5_80_layers_sampled():
     dec = [r for r in range(len(b.agent)) if b.n_rows[r] == 1]
     q_bits = RN.to_host_bits(q)
     kn_bits, vn_bits = RN.to_host_bits(kn), RN.to_host_bits(vn)
+    q_indptr = b.q_indptr()
+    ck = PT.checker()
+    pending = []
+
+    def finish(entry):
+        layer, nrows, h = entry
+        res = ck.collect(h, f"config5 layer {layer}")
+        announce(f"config5 layer {layer}: rows={nrows} max_abs={res[0]:.2e} rel={res[1]:.2e} lse={res[2]:.2e}")
+
     for layer in range(layers):
         pool = B.make_pool(b.num_pages, hkv, d, pools_k[layer], pools_v[layer])
         B.pfx_append_kv(pool, plan, kn, vn)
         B.pfx_attention(pool, plan, q, o, lse)
-        if layer not in full_layers and layer % 8 != 3:
-            continue
-        B.pfx_sync_check()
         if layer in full_layers:
             rows = {r: [0] for r in dec}
             rows.update({r: v for r, v in sample_rows(b, rng, per=16).items() if r in ext})
         else:
             rows = {int(r): [0] for r in rng.choice(dec, size=len(dec) // 10, replace=False)}
+            rows.update({r: sorted(set(rng.integers(0, int(b.n_rows[r]), size=2).tolist())) for r in ext})
         need = set()
         for r in rows:
-            a = int(b.agent[r])
-            need.update(int(p) for p in b.prefix_pages[a])
-            need.update(int(p) for p in b.suffix_pages[r])
+            need.update(int(p) for p in b.prefix_pages[int(b.agent[r])])
+            L, n = int(b.suffix_len[r]), int(b.n_rows[r])
+            last = L - n + max(rows[r])                       # the last key any checked row sees
+            need.update(int(p) for p in b.suffix_pages[r][:last // 16 + 1])
         pages = np.array(sorted(need), np.int64)
         idx = torch.from_numpy(pages).cuda()
+        tok = torch.from_numpy(np.array([q_indptr[r] + i for r in sorted(rows) for i in rows[r]], np.int64)).cuda()
+        B.pfx_sync_check()
         kp = pools_k[layer].view(torch.int16).index_select(0, idx).cpu().numpy().view(np.uint16)
         vp = pools_v[layer].view(torch.int16).index_select(0, idx).cpu().numpy().view(np.uint16)
+        o_rows = o.view(torch.int16).index_select(0, tok).cpu().numpy().view(np.uint16)
+        l_rows = lse.index_select(0, tok).cpu().numpy()
+        # append bit-exactness on the checked requests' new-token slots
         index = {int(p): i for i, p in enumerate(pages)}
-        pp = [np.array([index.get(int(p), 0) for p in pl]) for pl in b.prefix_pages]
-        sp = [np.array([index.get(int(p), 0) for p in pl]) for pl in b.suffix_pages]
-        # append bit-exactness on the sampled requests' new-token slots
-        q_indptr = b.q_indptr()
-        for r in list(rows)[:20]:
+        for r in list(rows)[:24]:
             n, L = int(b.n_rows[r]), int(b.suffix_len[r])
-            for i in (0, n - 1):
+            for i in rows[r]:
                 pos = L - n + i
-                pg = sp[r][pos // 16]
-                assert np.array_equal(kp[pg, :, pos % 16], kn_bits[q_indptr[r] + i])
-                assert np.array_equal(vp[pg, :, pos % 16], vn_bits[q_indptr[r] + i])
-        ro, rl = oracle.prefix_shared_attention(kp, vp, pp, b.prefix_len, b.agent, sp, b.suffix_len, b.n_rows,
-                                                q_bits, hq, rows=rows)
-        res = PT.compare(b, RN.to_host_bits(o), lse.cpu().numpy(), ro, rl, f"config5 layer {layer}")
-        announce(f"config5 layer {layer}: rows={sum(len(v) for v in rows.values())} max_abs={res[0]:.2e} "
-                 f"rel={res[1]:.2e}")
+                pg = index[int(b.suffix_pages[r][pos // 16])]
+                assert np.array_equal(kp[pg, :, pos % 16], kn_bits[q_indptr[r] + i]), f"layer {layer}: K append"
+                assert np.array_equal(vp[pg, :, pos % 16], vn_bits[q_indptr[r] + i]), f"layer {layer}: V append"
+        h = ck.submit(b, pages, kp, vp, PT.gather_rows(q_bits, b, rows), o_rows, l_rows, rows, split_heads=False,
+                      partial_pages=True)
+        pending.append((layer, sum(len(v) for v in rows.values()), h))
+        del kp, vp
+        while len(pending) > 3:
+            finish(pending.pop(0))
+    while pending:
+        finish(pending.pop(0))
     del pools_k, pools_v
     torch.cuda.empty_cache()
