@@ -29,7 +29,9 @@
  *     device surface through pfx_sync_check().
  *   - All buffers are borrowed from the caller: the library never frees them
  *     and never allocates device memory.  A buffer must stay valid until the
- *     stream work that uses it has finished.
+ *     stream work that uses it has finished.  The one piece of device memory
+ *     the library holds itself is the static array behind
+ *     pfx_attention_noalloc (PFX_NOALLOC_MAX_WORKSPACE bytes per GPU).
  *   - bf16 means IEEE binary32 truncated to its upper 16 bits (bfloat16).
  *   - Page size is fixed at 16 tokens; head_dim must be 64 or 128; the query
  *     group G = num_q_heads / num_kv_heads must be 1, 2, 4, 8 or 16; query
@@ -278,6 +280,31 @@ size_t pfx_page_copy_workspace_bytes(int32_t n);
 int pfx_page_copy(const pfx_pool* dst, const pfx_pool* src, const int32_t* dst_pages,
                   const int32_t* src_pages, int32_t n, void* dev_workspace, size_t workspace_bytes,
                   void* hip_stream);
+
+/* ---------------------------------------------------------------------
+ * Allocation-free attention step, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Same results as pfx_append_kv (when k_new and v_new
+ * are given) followed by pfx_attention on the same plan, bit for bit; the
+ * plan need not be uploaded and no caller workspace is used.  Instead the
+ * plan's tables (copied from its host image on the stream at every call)
+ * and the decode pieces' partial states live in a static device array of
+ * PFX_NOALLOC_MAX_WORKSPACE bytes, which each GPU the library runs on holds
+ * until the process ends.  The call allocates nothing: no hipMalloc, no
+ * hipFree.
+ *   k_new, v_new  as pfx_append_kv, or both NULL to skip the append;
+ *   q, o, lse, sm_scale  as pfx_attention.
+ * Errors: PFX_ENOMEM, before anything runs, when the plan's workspace
+ * (pfx_plan_workspace_bytes) exceeds PFX_NOALLOC_MAX_WORKSPACE; PFX_EINVAL
+ * when only one of k_new, v_new is NULL; otherwise as pfx_append_kv and
+ * pfx_attention.
+ * All calls on one GPU share that GPU's array and leave their contents in
+ * it: calls that may overlap on one GPU (several streams or threads) race,
+ * and the caller must serialise them.
+ * --------------------------------------------------------------------- */
+#define PFX_NOALLOC_MAX_WORKSPACE ((size_t)128 << 20) /* 128 MiB per GPU */
+int pfx_attention_noalloc(const pfx_pool* pool, const pfx_plan* plan, const void* k_new, const void* v_new,
+                          const void* q, void* o, float* lse, float sm_scale, void* hip_stream);
 
 /* Wait for the stream and report any device-side error as PFX_EHIP. */
 int pfx_sync_check(void* hip_stream);

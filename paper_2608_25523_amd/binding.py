@@ -25,6 +25,7 @@ PFX_PAGE_SIZE = 16
 PFX_MODE_EXTEND = 1
 PFX_MODE_DECODE = 2
 PFX_MODE_MIXED = 3
+PFX_NOALLOC_MAX_WORKSPACE = 128 << 20
 
 _ERR_NAMES = {PFX_EINVAL: "PFX_EINVAL", PFX_ERANGE: "PFX_ERANGE", PFX_ENOMEM: "PFX_ENOMEM",
               PFX_EUNSUPPORTED: "PFX_EUNSUPPORTED", PFX_EHIP: "PFX_EHIP"}
@@ -35,7 +36,7 @@ EXPORTED = [
     "pfx_plan_create", "pfx_plan_workspace_bytes", "pfx_plan_get_stats", "pfx_plan_export",
     "pfx_plan_upload", "pfx_plan_destroy",
     "pfx_append_kv", "pfx_attention", "pfx_merge_states",
-    "pfx_page_copy_workspace_bytes", "pfx_page_copy", "pfx_sync_check",
+    "pfx_page_copy_workspace_bytes", "pfx_page_copy", "pfx_sync_check", "pfx_attention_noalloc",
 ]
 
 
@@ -111,6 +112,7 @@ def _load(path: str = LIB_PATH):
         "pfx_page_copy_workspace_bytes": ([i32], sz),
         "pfx_page_copy": ([C.POINTER(pfx_pool), C.POINTER(pfx_pool), P, P, i32, P, sz, P], C.c_int),
         "pfx_sync_check": ([P], C.c_int),
+        "pfx_attention_noalloc": ([C.POINTER(pfx_pool), P, P, P, P, P, P, C.c_float, P], C.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -271,6 +273,12 @@ def pfx_append_kv(pool: pfx_pool, plan: Plan, k_new, v_new, stream=None):
 def pfx_attention(pool: pfx_pool, plan: Plan, q, o, lse=None, sm_scale: float = 0.0, stream=None):
     _check(LIB.pfx_attention(C.byref(pool), plan.h, _ptr(q), _ptr(o), _ptr(lse), C.c_float(sm_scale),
                              _stream(stream)))
+
+
+def pfx_attention_noalloc(pool: pfx_pool, plan: Plan, q, o, lse=None, k_new=None, v_new=None,
+                          sm_scale: float = 0.0, stream=None):
+    _check(LIB.pfx_attention_noalloc(C.byref(pool), plan.h, _ptr(k_new), _ptr(v_new), _ptr(q), _ptr(o), _ptr(lse),
+                                     C.c_float(sm_scale), _stream(stream)))
 
 
 def pfx_merge_states(o_parts, lse_parts, o, lse=None, stream=None):

@@ -29,6 +29,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <mutex>
 
 #include "pfx_internal.h"
 
@@ -1276,6 +1277,81 @@ extern "C" int pfx_attention(const pfx_pool* pool, const pfx_plan* p, const void
   if (!q || !o) return fail(PFX_EINVAL, "pfx_attention: q or o is NULL");
   return launch_attention(pool, p, dev_plan(p), q, o, lse, sm_scale, static_cast<hipStream_t>(stream),
                           "pfx_attention");
+}
+
+// ---------------------------------------------------------------------------
+// Allocation-free variant: the plan's tables and the decode pieces' partial
+// states live in one file-scope device array instead of a caller workspace.
+// Each GPU holds its own copy until the process ends; host code reaches it
+// only through the address hipGetSymbolAddress returns for the current
+// device (the array's name is a host-side stand-in, not a device address).
+// ---------------------------------------------------------------------------
+namespace pfx {
+constexpr size_t kScratchBytes = PFX_NOALLOC_MAX_WORKSPACE;
+constexpr int kMaxScratchDevices = 64;
+}  // namespace pfx
+
+static __device__ __align__(256) unsigned char scratch[pfx::kScratchBytes];
+
+namespace pfx {
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kMaxScratchDevices];
+
+// Device address of `scratch` on the current device, looked up on the first
+// call on each device and kept.
+static int scratch_address(void** out, const char* who) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, who);
+  if (dev < 0 || dev >= kMaxScratchDevices) return fail(PFX_EINVAL, "%s: device %d out of range", who, dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!ptr || reinterpret_cast<uintptr_t>(ptr) % 256)
+      return fail(PFX_EHIP, "%s: scratch address %p is not 256-byte aligned", who, ptr);
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return PFX_OK;
+}
+}  // namespace pfx
+
+extern "C" int pfx_attention_noalloc(const pfx_pool* pool, const pfx_plan* p, const void* k_new,
+                                     const void* v_new, const void* q, void* o, float* lse, float sm_scale,
+                                     void* stream) {
+  const char* who = "pfx_attention_noalloc";
+  if (!pool) return fail(PFX_EINVAL, "%s: pool is NULL", who);
+  if (!p) return fail(PFX_EINVAL, "%s: plan is NULL", who);
+  if (pool->page_size != PFX_PAGE_SIZE || pool->num_kv_heads != p->hkv || pool->head_dim != p->d ||
+      pool->num_pages != p->num_pages)
+    return fail(PFX_EINVAL, "%s: pool shape differs from the one the plan was built for", who);
+  if (!pool->k_pages || !pool->v_pages) return fail(PFX_EINVAL, "%s: pool pointers are NULL", who);
+  if ((k_new == nullptr) != (v_new == nullptr))
+    return fail(PFX_EINVAL, "%s: k_new and v_new must both be given or both be NULL", who);
+  const bool attend = p->num_items > 0 || p->num_segs > 0;
+  if (attend && (!q || !o)) return fail(PFX_EINVAL, "%s: q or o is NULL", who);
+  if (p->total_bytes > kScratchBytes)
+    return fail(PFX_ENOMEM, "%s: the plan needs %zu bytes of workspace, the static scratch holds %zu", who,
+                p->total_bytes, kScratchBytes);
+  const bool append = k_new != nullptr && p->num_tokens > 0;
+  if (!append && !attend) return PFX_OK;
+  void* ws = nullptr;
+  int rc = scratch_address(&ws, who);
+  if (rc) return rc;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  // The tables, stream-ordered after any earlier call's kernels that read
+  // them; the partial states need no clearing (every slot is written by its
+  // piece before the merge reads it).
+  if (p->blob_bytes) {
+    hipError_t e = hipMemcpyAsync(ws, p->blob.data(), p->blob_bytes, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return hip_fail(e, "pfx_attention_noalloc: hipMemcpyAsync");
+  }
+  const DevPlan dp = dev_plan(p, ws);
+  if (append && (rc = launch_append(pool, p, dp, k_new, v_new, s, who))) return rc;
+  if (attend) return launch_attention(pool, p, dp, q, o, lse, sm_scale, s, who);
+  return PFX_OK;
 }
 
 extern "C" int pfx_merge_states(const float* o_parts, const float* lse_parts, int32_t num_parts, int32_t rows,

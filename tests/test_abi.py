@@ -462,3 +462,37 @@ def test_extend_blocks_take_any_key_count():
     assert s.num_extend_items == 8 * (10 + 2) and s.num_tokens == 364   # 32 rows x 4 heads per block
     blocks = plan_for(b, mode=B.PFX_MODE_EXTEND).export(0)
     assert blocks[:, 6].max() == 24576                   # s0_kend: the whole prefix in one block's first segment
+
+
+class _FakeBuffer:
+    """Stands in for a device tensor: a nonzero address that no call here
+    ever dereferences (every case below fails validation first)."""
+
+    def __init__(self, addr):
+        self.addr = addr
+
+    def data_ptr(self):
+        return self.addr
+
+
+def test_noalloc_validates_before_touching_the_device():
+    b = small_batch()
+    fake = [_FakeBuffer(0x10000 * (i + 1)) for i in range(6)]
+    pool = B.make_pool(b.num_pages, b.num_kv_heads, b.head_dim, fake[0], fake[1])
+    plan = plan_for(b, pool)
+    # only one of k_new / v_new
+    expect_error(B.PFX_EINVAL, lambda: B.pfx_attention_noalloc(pool, plan, fake[2], fake[3], k_new=fake[4], stream=0))
+    # no q / o
+    expect_error(B.PFX_EINVAL, lambda: B.pfx_attention_noalloc(pool, plan, None, fake[3], stream=0))
+    # a pool of another shape
+    other = B.make_pool(b.num_pages + 1, b.num_kv_heads, b.head_dim, fake[0], fake[1])
+    expect_error(B.PFX_EINVAL, lambda: B.pfx_attention_noalloc(other, plan, fake[2], fake[3], stream=0))
+    # a plan whose workspace exceeds the static array (checked before any HIP call)
+    big = W.make_batch(14, num_q_heads=32, num_kv_heads=8, head_dim=128, num_pages=65536, prefix_len=[30000],
+                       agent=[0] * 120, suffix_len=[40] * 120, n_rows=[1] * 120)
+    bpool = B.make_pool(big.num_pages, 8, 128, fake[0], fake[1])
+    bplan = plan_for(big, bpool, B.PFX_MODE_DECODE, piece_steps=1)
+    assert bplan.workspace_bytes() > B.PFX_NOALLOC_MAX_WORKSPACE
+    expect_error(B.PFX_ENOMEM, lambda: B.pfx_attention_noalloc(bpool, bplan, fake[2], fake[3], fake[5],
+                                                                 k_new=fake[4], v_new=fake[4], stream=0))
+    assert "static scratch" in B.pfx_last_error()
