@@ -505,8 +505,9 @@ def bench_movement(torch, B, RN, W):
     """Prefix movement (Eq. (8)): B_swap per direction fitted from timed
     evictions and loads of 512, 2048 and 8192-token prefixes (mu = tau bytes
     per token); a serialized transition (two prefixes out, one in) against
-    the model; and a 64 MB load on a second stream beside the decode-8B
-    attention calls on the first."""
+    the model; and a 134 MB load on a second stream beside the decode-8B
+    attention calls on the first, by the copy kernel and by the copy
+    engines."""
     import numpy as np
 
     from paper_2608_25523_amd import movement as MV
@@ -515,12 +516,23 @@ def bench_movement(torch, B, RN, W):
     ds = RN.DeviceStep(b, W.host_values_fast(b, 7), poison=False)
     hkv, d = b.num_kv_heads, b.head_dim
     tau = hkv * d * 2 * 2
-    used = set(int(p) for p in b.used_pages())
+    # Four replicas of the batch on disjoint pages (416 MB, more than the
+    # 256 MB last-level cache), attention rotating over them, so the
+    # attention figures alone and beside a load are both taken cold.
+    reps = W.replicas(b, 4, 78)
+    src = torch.from_numpy(b.used_pages()).cuda()
+    plans = [ds.plan]
+    for rb in reps[1:]:
+        dst = torch.from_numpy(rb.used_pages()).cuda()
+        ds.k_pool.view(torch.int16).index_copy_(0, dst, ds.k_pool.view(torch.int16).index_select(0, src))
+        ds.v_pool.view(torch.int16).index_copy_(0, dst, ds.v_pool.view(torch.int16).index_select(0, src))
+        plans.append(B.plan_from_batch(ds.pool, rb, B.PFX_MODE_DECODE).upload())
+    used = set(int(p) for rb in reps for p in rb.used_pages())
     spare = np.array([p for p in range(b.num_pages) if p not in used], np.int32)
     rng = np.random.default_rng(77)
     spare = rng.permutation(spare)
     store = MV.HostStore(4096, hkv, d)
-    mover = MV.Mover(ds.pool, store, 4096)
+    mover = MV.Mover(ds.pool, store, 4096, staging=True)
     cal = MV.calibrate_swap(mover, [spare[:n] for n in (32, 128, 512)], tau)
     out = {"mu_bytes_per_token": tau, "b_swap_out_GBs": round(cal["b_out"] / 1e9, 2),
            "b_swap_in_GBs": round(cal["b_in"] / 1e9, 2),
@@ -544,7 +556,12 @@ def bench_movement(torch, B, RN, W):
     out["transition"] = {"tokens_out": tok_out, "tokens_in": tok_in, "measured_ms": round(t_meas * 1e3, 3),
                          "eq8_ms": round(t_model * 1e3, 3)}
     # Overlap: a 2048-page load on a second stream beside 30 attention calls.
-    attn = lambda: B.pfx_attention(ds.pool, ds.plan, ds.q, ds.o, ds.lse)
+    turn = [0]
+
+    def attn():
+        turn[0] += 1
+        B.pfx_attention(ds.pool, plans[turn[0] % len(plans)], ds.q, ds.o, ds.lse)
+
     load_pages, load_slots = spare[2048:4096], np.arange(2048, dtype=np.int32)
     a_alone = events_ms(attn, 30, torch)
     l_alone = events_ms(lambda: mover.load(load_pages, load_slots), 3, torch, warm=1)
@@ -565,6 +582,44 @@ def bench_movement(torch, B, RN, W):
                       "load_beside_attention_ms": round(s0.elapsed_time(s1), 3),
                       "attention_alone_us": round(a_alone * 1e3, 2),
                       "attention_beside_load_us": round(m0.elapsed_time(m1) / 30 * 1e3, 2)}
+    # The same load through the copy engines (store slots 0..2047 are one run).
+    d_alone = events_ms(lambda: mover.load_dma(load_pages, load_slots), 3, torch, warm=1)
+    torch.cuda.synchronize()
+    side.wait_stream(main)
+    s0.record(side)
+    mover.load_dma(load_pages, load_slots, stream=side.cuda_stream)
+    s1.record(side)
+    m0.record(main)
+    for _ in range(30):
+        attn()
+    m1.record(main)
+    torch.cuda.synchronize()
+    out["overlap_copy_engines"] = {"load_alone_ms": round(d_alone, 3),
+                                   "load_beside_attention_ms": round(s0.elapsed_time(s1), 3),
+                                   "attention_beside_load_us": round(m0.elapsed_time(m1) / 30 * 1e3, 2),
+                                   "note": "scattered pool pages: staged, then one device page copy"}
+    # ... and into 2048 consecutive pages (of a second pool, since the
+    # decode pool has no free run that long): straight copies, no kernel.
+    shape = (2048, hkv, 16, d)
+    tensors = (torch.empty(shape, dtype=torch.bfloat16, device="cuda"),
+               torch.empty(shape, dtype=torch.bfloat16, device="cuda"))
+    mover2 = MV.Mover(B.make_pool(2048, hkv, d, *tensors), store, 4096)
+    run_pages = np.arange(2048, dtype=np.int32)
+    r_alone = events_ms(lambda: mover2.load_dma(run_pages, load_slots, pool_tensors=tensors), 3, torch, warm=1)
+    torch.cuda.synchronize()
+    side.wait_stream(main)
+    s0.record(side)
+    mover2.load_dma(run_pages, load_slots, stream=side.cuda_stream, pool_tensors=tensors)
+    s1.record(side)
+    m0.record(main)
+    for _ in range(30):
+        attn()
+    m1.record(main)
+    torch.cuda.synchronize()
+    out["overlap_copy_engines_direct"] = {"load_alone_ms": round(r_alone, 3),
+                                          "load_beside_attention_ms": round(s0.elapsed_time(s1), 3),
+                                          "attention_beside_load_us": round(m0.elapsed_time(m1) / 30 * 1e3, 2),
+                                          "note": "2048 consecutive pool pages: one copy per tensor"}
     del ds, store, mover
     torch.cuda.empty_cache()
     return out

@@ -35,16 +35,29 @@ class Mover:
     """Evicts and loads page lists between one device pool and one host
     store.  Each instance owns a device workspace for the page-id lists of
     one transfer at a time (stream-ordered reuse: a transfer must not start
-    on a different stream before the previous one on this mover finished)."""
+    on a different stream before the previous one on this mover finished),
+    and, for the copy-engine paths, a device staging area of max_pages
+    pages."""
 
-    def __init__(self, pool: B.pfx_pool, store: HostStore, max_pages: int, device="cuda"):
+    def __init__(self, pool: B.pfx_pool, store: HostStore, max_pages: int, device="cuda", staging: bool = False):
         self.pool, self.store = pool, store
         self.ws = torch.empty(B.pfx_page_copy_workspace_bytes(max_pages) + 256, dtype=torch.uint8, device=device)
         self.max_pages = max_pages
+        self.stage = None
+        if staging:
+            shape = (max_pages,) + tuple(store.k.shape[1:])
+            self.stage_k = torch.empty(shape, dtype=torch.bfloat16, device=device)
+            self.stage_v = torch.empty(shape, dtype=torch.bfloat16, device=device)
+            self.stage = B.make_pool(max_pages, shape[1], shape[3], self.stage_k, self.stage_v)
 
     def _check(self, pool_pages, slots):
         if len(pool_pages) != len(slots) or len(pool_pages) > self.max_pages:
             raise ValueError("page lists differ in length or exceed the mover's workspace")
+        pool_pages, slots = np.asarray(pool_pages), np.asarray(slots)
+        if len(pool_pages) and (pool_pages.min() < 0 or pool_pages.max() >= self.pool.num_pages):
+            raise ValueError("a pool page id is out of range")
+        if len(slots) and (slots.min() < 0 or slots.max() >= self.store.pool.num_pages):
+            raise ValueError("a store slot is out of range")
 
     def evict(self, pool_pages, slots, stream=None):
         """Pool pages -> store slots (device to host)."""
@@ -55,6 +68,73 @@ class Mover:
         """Store slots -> pool pages (host to device)."""
         self._check(pool_pages, slots)
         B.pfx_page_copy(self.pool, self.store.pool, pool_pages, slots, self.ws, stream=stream)
+
+    @staticmethod
+    def _runs(slots):
+        """Maximal runs of consecutive store slots: (list index, first slot, length)."""
+        slots = np.asarray(slots, np.int64)
+        cut = np.nonzero(np.diff(slots) != 1)[0] + 1
+        starts = np.concatenate([[0], cut])
+        ends = np.concatenate([cut, [len(slots)]])
+        return [(int(a), int(slots[a]), int(b - a)) for a, b in zip(starts, ends)]
+
+    def _on(self, stream):
+        return torch.cuda.ExternalStream(stream) if stream is not None else torch.cuda.current_stream()
+
+    # Runs of at least this many pages that are consecutive both in the
+    # store and in the pool cross the host link straight into the pool.
+    DIRECT_RUN = 8
+
+    def load_dma(self, pool_pages, slots, stream=None, pool_tensors=None):
+        """Store slots -> pool pages through the copy engines (no compute
+        units wait on the host link).  Runs of pages consecutive in the store
+        and in the pool (``pool_tensors``: the pool's K and V tensors) are
+        copied straight into the pool, one asynchronous memory copy per run
+        and tensor.  The other pages cross, run by run of consecutive store
+        slots, into the device staging area, and one device-to-device page
+        copy then places them."""
+        self._check(pool_pages, slots)
+        pool_pages = np.asarray(pool_pages, np.int64)
+        slots = np.asarray(slots, np.int64)
+        staged = np.ones(len(slots), bool)
+        with torch.cuda.stream(self._on(stream)):
+            if pool_tensors is not None:
+                pk, pv = pool_tensors
+                for i0, s0, ln in self._runs(slots):
+                    # split the slot run where the pool pages stop being consecutive
+                    pp = pool_pages[i0:i0 + ln]
+                    for j0, p0, m in self._runs(pp):
+                        if m < self.DIRECT_RUN:
+                            continue
+                        a = s0 + j0
+                        pk[p0:p0 + m].copy_(self.store.k[a:a + m], non_blocking=True)
+                        pv[p0:p0 + m].copy_(self.store.v[a:a + m], non_blocking=True)
+                        staged[i0 + j0:i0 + j0 + m] = False
+            if not staged.any():
+                return
+            if self.stage is None:
+                raise RuntimeError("this mover has no staging area (staging=True)")
+            idx = np.nonzero(staged)[0]
+            for i0, s0, ln in self._runs(slots[idx]):
+                self.stage_k[i0:i0 + ln].copy_(self.store.k[s0:s0 + ln], non_blocking=True)
+                self.stage_v[i0:i0 + ln].copy_(self.store.v[s0:s0 + ln], non_blocking=True)
+        B.pfx_page_copy(self.pool, self.stage, pool_pages[idx].astype(np.int32), np.arange(len(idx), dtype=np.int32),
+                        self.ws, stream=stream)
+
+    def evict_dma(self, pool_pages, slots, stream=None):
+        """Pool pages -> store slots through the copy engines: one device
+        page copy gathers the pages into the staging area, then every run of
+        consecutive store slots crosses the host link by one asynchronous
+        memory copy."""
+        self._check(pool_pages, slots)
+        if self.stage is None:
+            raise RuntimeError("this mover has no staging area (staging=True)")
+        n = len(pool_pages)
+        B.pfx_page_copy(self.stage, self.pool, np.arange(n, dtype=np.int32), pool_pages, self.ws, stream=stream)
+        with torch.cuda.stream(self._on(stream)):
+            for i0, s0, ln in self._runs(slots):
+                self.store.k[s0:s0 + ln].copy_(self.stage_k[i0:i0 + ln], non_blocking=True)
+                self.store.v[s0:s0 + ln].copy_(self.stage_v[i0:i0 + ln], non_blocking=True)
 
 
 def t_move(mu: float, b_swap: float, tokens_out, tokens_in) -> float:

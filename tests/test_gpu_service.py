@@ -1,10 +1,14 @@
 """Service-time tables measured on the GPU (Sec. 4.2: profiled T_prefill and
 T_decode).  Properties the method fixes: prefill time grows with the input,
 and one grouped decode step for 64 requests of an agent costs far less than
-64 single-request steps, since the prefix is read once for the group."""
+64 single-request steps, since the prefix is read once for the group.  The
+table's fallback estimate and redo charge equal the reference formulas of
+oracle/service.py evaluated on the same measured times."""
 
+import numpy as np
 import pytest
 
+from oracle import service as OSV
 from paper_2608_25523_amd import service as SV
 
 pytestmark = pytest.mark.gpu
@@ -13,9 +17,15 @@ pytestmark = pytest.mark.gpu
 @pytest.mark.timeout(300)
 def test_service_tables():
     print("[gpu-test] service tables: prefill over a 4096-token prefix, decode steps over 2048", flush=True)
-    pre = SV.profile_prefill([256, 1024, 4096], prefix_len=4096, reps=3)
+    lengths = [256, 1024, 4096]
+    pre = SV.profile_prefill(lengths, prefix_len=4096, reps=3)
     assert pre[256] < pre[1024] < pre[4096]
     dec = SV.profile_decode([1, 64], prefix_len=2048, suffix_len=288, reps=10)
     assert 0 < dec[1] and dec[64] < 16 * dec[1]
     tab = SV.ServiceTable(pre, dec[64])
-    assert tab.estimate(1024, 100) == pytest.approx(pre[1024] + 100 * dec[64])
+    # the reference's T_prefill: straight lines between the measured points
+    t_prefill = lambda L: float(np.interp(L, lengths, [pre[k] for k in lengths]))
+    for L, m in ((256, 0), (1024, 100), (640, 17), (3000, 256), (4096, 1)):
+        assert tab.estimate(L, m) == pytest.approx(OSV.fallback_estimate(t_prefill, dec[64], L, m), rel=1e-12)
+    ys = [0, 3, 250, 17]
+    assert tab.j_redo(ys) == pytest.approx(OSV.j_redo(dec[64], ys), rel=1e-12)
