@@ -468,14 +468,23 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
         if (ins.second) chunks.emplace_back();
         chunks[ins.first->second].push_back(rank[k]);
       }
+      // Chunks with the same number of blocks go together, so a group of
+      // eight has complete rounds: its first `common` blocks are laid out
+      // eight apart, and blocks past a shorter chunk's end go to the end of
+      // the run (placed there, they would shift every later position).
+      std::stable_sort(chunks.begin(), chunks.end(),
+                       [](const std::vector<int32_t>& x, const std::vector<int32_t>& y) { return x.size() > y.size(); });
+      std::vector<int32_t> leftover;
       for (size_t g = 0; g < chunks.size(); g += 8) {
         const size_t g1 = std::min(chunks.size(), g + 8);
-        size_t blocks = 0;
-        for (size_t c = g; c < g1; ++c) blocks = std::max(blocks, chunks[c].size());
-        for (size_t bj = 0; bj < blocks; ++bj)
-          for (size_t c = g; c < g1; ++c)
-            if (bj < chunks[c].size()) order.push_back(chunks[c][bj]);
+        size_t common = chunks[g].size();
+        for (size_t c = g; c < g1; ++c) common = std::min(common, chunks[c].size());
+        for (size_t bj = 0; bj < common; ++bj)
+          for (size_t c = g; c < g1; ++c) order.push_back(chunks[c][bj]);
+        for (size_t c = g; c < g1; ++c)
+          for (size_t bj = common; bj < chunks[c].size(); ++bj) leftover.push_back(chunks[c][bj]);
       }
+      order.insert(order.end(), leftover.begin(), leftover.end());
       i = j;
     }
   }

@@ -496,3 +496,28 @@ def test_noalloc_validates_before_touching_the_device():
     expect_error(B.PFX_ENOMEM, lambda: B.pfx_attention_noalloc(bpool, bplan, fake[2], fake[3], fake[5],
                                                                  k_new=fake[4], v_new=fake[4], stream=0))
     assert "static scratch" in B.pfx_last_error()
+
+
+def test_prefix_chunk_blocks_share_an_xcd():
+    """Column blocks of one prefix chunk (same KV head and first page block)
+    sit a multiple of eight positions apart in the launch order, so they run
+    on one XCD and read the chunk through its L2; only blocks beyond the
+    shortest chunk of their group of eight may break the pattern."""
+    n = [150, 70, 300]        # 4 KV heads, 3 pieces per prefix: groups of eight mix agents
+    mixed = W.make_batch(3, num_q_heads=32, num_kv_heads=4, head_dim=128, num_pages=20000, prefix_len=[1536] * 3,
+                         agent=np.concatenate([np.full(k, a) for a, k in enumerate(n)]),
+                         suffix_len=np.full(sum(n), 40), n_rows=np.ones(sum(n), np.int32))
+    for b, allowed in ((W.config_batch(5), 0.0), (W.config_batch(4), 0.0), (mixed, 0.11)):
+        segs = plan_for(b).export(3)
+        first = {}
+        off = total = 0
+        for pos, row in enumerate(segs):
+            if row[0] != 0:                      # prefix pieces only
+                continue
+            key = (int(row[1]), int(row[144]), int(row[3]))
+            if key in first:
+                total += 1
+                off += (pos - first[key]) % 8 != 0
+            else:
+                first[key] = pos
+        assert total > 0 and off <= allowed * total, (off, total)
