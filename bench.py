@@ -2,9 +2,10 @@
 (TFLOP/s) at the Llama-3-8B attention-layer shape, on one MI355X.
 
 A step is one pass of the hot path over one batch: the KV append of the
-step's new tokens, then attention for every query row (the decode launch:
-agent prefixes shared by their decode rows and each request's own suffix,
-cut into pieces; then the log-sum-exp merge of the pieces).  Inputs are
+step's new tokens and attention for every query row, one pfx_step call (the
+decode launch -- agent prefixes shared by their decode rows and each
+request's own suffix, cut into pieces -- writes the new tokens into the
+pool as it reads them; then the log-sum-exp merge of the pieces).  Inputs are
 resident in HBM before timing starts.
 
 Primary line (``value``): decode-8B -- Hq 32 / Hkv 8 / d 128, 4 agent
@@ -115,19 +116,25 @@ def bench_decode(args, torch, B, RN, W):
     torch.cuda.synchronize()
 
     def step(i):
-        plan = plans[i % len(plans)]
-        B.pfx_append_kv(ds.pool, plan, ds.k_new, ds.v_new)
-        B.pfx_attention(ds.pool, plan, ds.q, ds.o, ds.lse)
+        # append + attention in one call: the decode launch appends as it goes
+        B.pfx_step(ds.pool, plans[i % len(plans)], ds.k_new, ds.v_new, ds.q, ds.o, ds.lse)
 
     def attn(i):
         B.pfx_attention(ds.pool, plans[i % len(plans)], ds.q, ds.o, ds.lse)
 
+    def unfused(i):
+        plan = plans[i % len(plans)]
+        B.pfx_append_kv(ds.pool, plan, ds.k_new, ds.v_new)
+        B.pfx_attention(ds.pool, plan, ds.q, ds.o, ds.lse)
+
     ms, attn_ms, spread = timed_steps(step, attn, args.steps, args.warmup, torch)
+    unfused_ms, _ = attention_ms(unfused, max(args.steps, MIN_ATTN_CALLS), torch)
     B.pfx_sync_check()
     graph_ms = graph_replay_ms(plans, ds, args.steps, torch, B)
     side = side_costs(b, ds, plans, args.steps, torch, B)
     u = b.unique_kv_bytes()
     st = ds.plan.stats()
+    side["unfused_step_us"] = round(unfused_ms * 1e3, 3)
     return dict(batch=b, hv=hv, ms=ms, attn_ms=attn_ms, spread=spread, graph_ms=graph_ms, unique_bytes=u,
                 replicas=len(plans), stats=st, side=side)
 
@@ -167,8 +174,7 @@ def graph_replay_ms(plans, ds, steps, torch, B):
     with torch.cuda.graph(g, stream=s):
         cs = torch.cuda.current_stream().cuda_stream
         for p in plans:
-            B.pfx_append_kv(ds.pool, p, ds.k_new, ds.v_new, stream=cs)
-            B.pfx_attention(ds.pool, p, ds.q, ds.o, ds.lse, stream=cs)
+            B.pfx_step(ds.pool, p, ds.k_new, ds.v_new, ds.q, ds.o, ds.lse, stream=cs)
     torch.cuda.synchronize()
     reps = max(2, steps // len(plans))
     for _ in range(2):

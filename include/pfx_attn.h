@@ -188,7 +188,9 @@ typedef struct pfx_plan_stats {
   int32_t pages_needed;        /* left-hand side of the Eq. (2) check, in pages */
   int32_t num_decode_steps;    /* 32-key steps of all decode items */
   int32_t num_decode_pieces;   /* runs of at most piece_steps steps of one decode item */
-  int32_t reserved[2];
+  int32_t num_wide_blocks;     /* prefix pieces of agents with more than 64 decode columns per KV head,
+                                  run 128 columns at a time (counted apart from num_decode_pieces) */
+  int32_t reserved;
   int64_t workspace_bytes;
 } pfx_plan_stats;
 
@@ -202,10 +204,12 @@ int pfx_plan_workspace_bytes(const pfx_plan* plan, size_t* bytes);
 int pfx_plan_get_stats(const pfx_plan* plan, pfx_plan_stats* out);
 
 /* Copy one of the plan's host arrays out, for inspection and tests:
- * which = 0: extend blocks, 32 int32 each; 1: their row-token list;
- * 2: page list; 3: decode pieces, 272 int32 each (header, row tokens,
- * output rows, page blocks of the steps); 6: tokens whose rows are merged;
- * 7: their (base, count) of partial slots per KV head.
+ * which = 0: extend blocks, then wide prefix blocks, 32 int32 each;
+ * 1: their row-token list; 8: the partial row base of each of those rows
+ * (-1 for extend rows); 2: page list; 3: decode pieces, 272 int32 each
+ * (header, row tokens, output rows, page blocks of the steps); 6: tokens
+ * whose rows are merged; 7: their (base, count) of partial slots per KV
+ * head.
  * Writes min(cap, size) values and sets *count to the full size. */
 int pfx_plan_export(const pfx_plan* plan, int32_t which, int32_t* out, int64_t cap, int64_t* count);
 
@@ -248,6 +252,21 @@ int pfx_append_kv(const pfx_pool* pool, const pfx_plan* plan, const void* k_new,
  * --------------------------------------------------------------------- */
 int pfx_attention(const pfx_pool* pool, const pfx_plan* plan, const void* q, void* o, float* lse,
                   float sm_scale, void* hip_stream);
+
+/* ---------------------------------------------------------------------
+ * One step: the KV append of the step's new tokens (as pfx_append_kv)
+ * followed by attention for every query row (as pfx_attention), with the
+ * same results bit for bit, in the fewest launches.  When the plan has no
+ * extend blocks, the decode launch appends as it goes: a decode request's
+ * new tokens are read straight from k_new / v_new into the step that
+ * attends them and written into their pool slots by the same workgroup (no
+ * other work of the launch reads those slots).  Extend blocks read one
+ * another's new tokens, so with extend blocks the append runs first as its
+ * own launch.  Arguments as pfx_append_kv and pfx_attention; k_new and
+ * v_new may be NULL only when the plan has no query rows.
+ * --------------------------------------------------------------------- */
+int pfx_step(const pfx_pool* pool, const pfx_plan* plan, const void* k_new, const void* v_new, const void* q,
+             void* o, float* lse, float sm_scale, void* hip_stream);
 
 /* ---------------------------------------------------------------------
  * Log-sum-exp merge of attention results computed over disjoint key ranges

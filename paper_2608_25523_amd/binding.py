@@ -35,7 +35,7 @@ EXPORTED = [
     "pfx_alloc_create", "pfx_alloc_pages", "pfx_free_pages", "pfx_alloc_num_free", "pfx_alloc_destroy",
     "pfx_plan_create", "pfx_plan_workspace_bytes", "pfx_plan_get_stats", "pfx_plan_export",
     "pfx_plan_upload", "pfx_plan_destroy",
-    "pfx_append_kv", "pfx_attention", "pfx_merge_states",
+    "pfx_append_kv", "pfx_attention", "pfx_step", "pfx_merge_states",
     "pfx_page_copy_workspace_bytes", "pfx_page_copy", "pfx_sync_check", "pfx_attention_noalloc",
 ]
 
@@ -71,11 +71,11 @@ class pfx_plan_stats(C.Structure):
                 ("num_prefix_items", C.c_int32), ("num_suffix_items", C.c_int32),
                 ("num_extend_items", C.c_int32), ("num_partial_rows", C.c_int32),
                 ("pages_needed", C.c_int32), ("num_decode_steps", C.c_int32), ("num_decode_pieces", C.c_int32),
-                ("reserved", C.c_int32 * 2), ("workspace_bytes", C.c_int64)]
+                ("num_wide_blocks", C.c_int32), ("reserved", C.c_int32), ("workspace_bytes", C.c_int64)]
 
 
 # Shapes of the arrays pfx_plan_export returns (int32 columns per record).
-EXPORT_WIDTH = {0: 32, 1: 1, 2: 1, 3: 272, 6: 1, 7: 2}
+EXPORT_WIDTH = {0: 32, 1: 1, 2: 1, 3: 272, 6: 1, 7: 2, 8: 1}
 
 
 def _load(path: str = LIB_PATH):
@@ -108,6 +108,7 @@ def _load(path: str = LIB_PATH):
         "pfx_plan_destroy": ([P], None),
         "pfx_append_kv": ([C.POINTER(pfx_pool), P, P, P, P], C.c_int),
         "pfx_attention": ([C.POINTER(pfx_pool), P, P, P, P, C.c_float, P], C.c_int),
+        "pfx_step": ([C.POINTER(pfx_pool), P, P, P, P, P, P, C.c_float, P], C.c_int),
         "pfx_merge_states": ([P, P, i32, i32, i32, P, P, P], C.c_int),
         "pfx_page_copy_workspace_bytes": ([i32], sz),
         "pfx_page_copy": ([C.POINTER(pfx_pool), C.POINTER(pfx_pool), P, P, i32, P, sz, P], C.c_int),
@@ -273,6 +274,11 @@ def pfx_append_kv(pool: pfx_pool, plan: Plan, k_new, v_new, stream=None):
 def pfx_attention(pool: pfx_pool, plan: Plan, q, o, lse=None, sm_scale: float = 0.0, stream=None):
     _check(LIB.pfx_attention(C.byref(pool), plan.h, _ptr(q), _ptr(o), _ptr(lse), C.c_float(sm_scale),
                              _stream(stream)))
+
+
+def pfx_step(pool: pfx_pool, plan: Plan, k_new, v_new, q, o, lse=None, sm_scale: float = 0.0, stream=None):
+    _check(LIB.pfx_step(C.byref(pool), plan.h, _ptr(k_new), _ptr(v_new), _ptr(q), _ptr(o), _ptr(lse),
+                        C.c_float(sm_scale), _stream(stream)))
 
 
 def pfx_attention_noalloc(pool: pfx_pool, plan: Plan, q, o, lse=None, k_new=None, v_new=None,

@@ -25,16 +25,22 @@ constexpr int kStepKeys = 32;
 
 enum ItemKind : int32_t { kPrefixItem = 0, kSuffixItem = 1, kExtendItem = 2 };
 
-// One extend block, run by one workgroup.  Its query columns are row_count
-// tokens (row_tok[row_begin ...]) times the G query heads of KV head
-// kv_head.  Keys come from two segments of the plan's page list:
+// One block of query columns run by one workgroup with 32 columns per wave.
+// Its columns are row_count tokens (row_tok[row_begin ...]) times the G
+// query heads of KV head kv_head.  Keys come from two segments of the
+// plan's page list:
 //   segment 0 (no mask):  keys [s0_kbeg, s0_kend) of the list at s0_page_off;
 //   segment 1 (causal):   keys [s1_kbeg, s1_kend) of the list at s1_page_off,
 //                         key k visible to token t iff k <= t + causal_base.
-// Rows are written final (out_slot = -1).  tok0 >= 0: the tokens are tok0,
-// tok0 + 1, ... (one request).  first_pages: the first kItemPages page ids
-// of the keys in order (segment 0's pages, then segment 1's), so the first
-// steps can be requested before the rest of the page list arrives.
+// kind kExtendItem: an extend block; its rows are written final
+// (out_slot = -1) and its tokens are tok0, tok0 + 1, ... (one request).
+// kind kPrefixItem: a wide prefix block, one piece of an agent's prefix
+// (segment 0 only) against up to 128 of the agent's decode columns; its
+// tokens are row_tok[row_begin + j] (tok0 = -1) and it leaves partial states
+// (out_slot = its slot) at partial rows row_out[row_begin + j] + g.
+// first_pages: the first kItemPages page ids of the keys in order (segment
+// 0's pages, then segment 1's), so the first steps can be requested before
+// the rest of the page list arrives.
 constexpr int kItemPages = 16;
 struct alignas(16) Item {
   int32_t kv_head;
@@ -102,8 +108,9 @@ struct MergeHead {
 
 // Device pointers into an uploaded workspace.
 struct DevPlan {
-  const Item* items;            // extend blocks
+  const Item* items;            // extend blocks, then wide prefix blocks
   const int32_t* row_tok;
+  const int32_t* row_out;       // partial row base of each row of a wide prefix block
   const int32_t* page_list;
   const int32_t* tok_slot;      // page * 16 + slot of every new token (append)
   const Seg* segs;              // decode pieces, longest first
@@ -126,7 +133,8 @@ struct pfx_plan {
   int32_t decode_workers = 0;  // decode workgroups requested (0: one per piece)
   int32_t num_reqs = 0, num_tokens = 0;
   int32_t num_items = 0;       // extend blocks (their records live in the blob at off_items)
-  std::vector<int32_t> row_tok, page_list, tok_req, tok_slot;
+  int32_t num_wide = 0;        // wide prefix blocks, after the extend blocks in the same array
+  std::vector<int32_t> row_tok, row_out, page_list, tok_req, tok_slot;
   std::vector<pfx::ReqInfo> req;
   int32_t num_segs = 0;        // decode pieces (their records live in the blob at off_segs)
   int64_t num_decode_steps = 0;
@@ -136,7 +144,7 @@ struct pfx_plan {
   int32_t n_prefix_items = 0, n_suffix_items = 0, n_extend_items = 0;
   int32_t pages_needed = 0;
   // byte offsets inside the workspace
-  size_t off_items = 0, off_row_tok = 0, off_page_list = 0, off_tok_slot = 0, off_segs = 0,
+  size_t off_items = 0, off_row_tok = 0, off_row_out = 0, off_page_list = 0, off_tok_slot = 0, off_segs = 0,
          off_merge_tok = 0, off_merge_head = 0, off_opart = 0, off_lpart = 0, total_bytes = 0, blob_bytes = 0;
   std::vector<unsigned char> blob;  // host image of [0, blob_bytes)
   const pfx::Item* host_items() const { return reinterpret_cast<const pfx::Item*>(blob.data() + off_items); }

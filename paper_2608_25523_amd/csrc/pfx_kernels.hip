@@ -111,6 +111,16 @@ struct AttnArgs {
   int32_t num_workers;  // decode launch: persistent workgroups
   int32_t num_pieces;   // decode pieces in the plan
   float scale_log2;  // sm_scale * log2(e)
+  // Decode with the KV append folded in: a suffix piece takes its new
+  // tokens' K/V rows straight from k_new / v_new (rows [T][Hkv][D], token
+  // order) and the merge launch writes them into the pool.  fuse_append ==
+  // 0: the append ran before the launch and the pool already holds them.
+  const uint16_t* k_new;
+  const uint16_t* v_new;
+  int32_t fuse_append;
+  // Decode launch: its first num_wide workgroups run the wide prefix blocks
+  // items[wide_first ...], the others the decode pieces.
+  int32_t num_wide, wide_first;
 };
 
 // Geometry of one 32-key step of an item.
@@ -769,13 +779,15 @@ __device__ __forceinline__ void extend_block(const AttnArgs& a, const Item* itp,
   bf16x8 qf[QBW][KS];
   int lim[QBW];
   int orow[QBW];
+  int prow[QBW];  // wide prefix blocks: the partial row of each column
 #pragma unroll
   for (int b = 0; b < QBW; ++b) {
     const int c = (wave * QBW + b) * kTileCols + col;
     int j = c >> a.group_shift;
     const int gg = c & (G - 1);
     if (j >= it.row_count) j = 0;
-    const int tok = it.tok0 + j;
+    const int tok = it.tok0 >= 0 ? it.tok0 + j : a.plan.row_tok[it.row_begin + j];
+    prow[b] = it.out_slot >= 0 ? a.plan.row_out[it.row_begin + j] + gg : -1;
     lim[b] = tok + it.causal_base;
     orow[b] = tok * a.hq + h * G + gg;
     if (b < nb) {
@@ -830,7 +842,17 @@ __device__ __forceinline__ void extend_block(const AttnArgs& a, const Item* itp,
 #pragma unroll
   for (int b = 0; b < QBW; ++b) {
     const int c = (wave * QBW + b) * kTileCols + col;
-    write_rows<D>(a, ws.acc[b], ws.m[b], ws.lv[b][0], orow[b], b < nb && (c >> a.group_shift) < it.row_count, grp);
+    const bool valid = b < nb && (c >> a.group_shift) < it.row_count;
+    if (it.out_slot < 0) {
+      write_rows<D>(a, ws.acc[b], ws.m[b], ws.lv[b][0], orow[b], valid, grp);
+    } else if (valid) {
+      // A wide prefix block's state, as a decode piece leaves it:
+      // accumulators in register order, (m, l) once per column.
+      float* out = a.plan.o_part + size_t(prow[b]) * D + grp * (4 * (D / 16));
+#pragma unroll
+      for (int jj = 0; jj < D / 16; ++jj) *reinterpret_cast<f32x4*>(out + 4 * jj) = ws.acc[b][jj];
+      if (grp == 0) *reinterpret_cast<f32x2*>(a.plan.l_part + 2 * size_t(prow[b])) = f32x2{ws.m[b], ws.lv[b][0]};
+    }
   }
 }
 
@@ -869,18 +891,50 @@ __device__ __forceinline__ int piece_window(const Seg& sg, int wave, int lane) {
   return lane < kPieceSteps ? sg.steps[2 * lane + (wave & 1)] : 0;
 }
 
+// Where a suffix piece's new tokens are, for the folded-in append: keys
+// [first_new, kend) of its item (the item's last ncols / G keys); first_new
+// is past every key for other pieces.
+struct NewRows {
+  int32_t k0, kend, first_new, head;
+};
+
 // Issue this wave's copies of stage k of a piece (k < 0: its Q stage);
 // returns how many copies it issued (a wave with no columns copies no Q).
-template <int D>
+// F: the append is folded in, and a tile holding new tokens takes their
+// rows from k_new / v_new.
+template <int D, bool F>
 __device__ __forceinline__ int issue_piece_stage(unsigned char* stage, const AttnArgs& a, const Seg& sg, int win,
                                                  int k, int ncols, int qh0, int wave, int lane,
-                                                 const uint32_t (&voff)[TileGeom<D>::loads_per_wave]) {
+                                                 const uint32_t (&voff)[TileGeom<D>::loads_per_wave],
+                                                 const NewRows& nr) {
   using TG = TileGeom<D>;
   const uint32_t dst = lds_address(stage) + wave * TG::page_bytes;
   if (k >= 0) {
     // K/V: tile (wave & 1) of K (waves 0, 1) or V (waves 2, 3), swizzled.
     const int blk = __builtin_amdgcn_readlane(win, k);
     const uint16_t* base = ((wave >> 1) ? a.vpool : a.kpool) + size_t(blk) * (16 * D);
+    if constexpr (F) {
+      const int tk0 = nr.k0 + kStepKeys * k + 16 * (wave & 1);
+      if (tk0 + 16 > nr.first_new && tk0 < nr.kend) {
+        // This tile holds some of the piece's new tokens: their rows come
+        // from k_new / v_new, the others from the pool, one copy per lane
+        // with its own address.
+        PFX_KEEP_BRANCH();
+        const uint16_t* fresh = (wave >> 1) ? a.v_new : a.k_new;
+#pragma unroll
+        for (int j = 0; j < TG::loads_per_wave; ++j) {
+          const int t = (64 * j + lane) / TG::chunks;
+          const int c = (lane % TG::chunks) ^ row_key<TG::chunks>(t);
+          const int key = tk0 + t;
+          const bool is_new = key >= nr.first_new && key < nr.kend;
+          const int row = is_new ? key - nr.first_new : 0;
+          const uint16_t* src =
+              is_new ? fresh + (size_t(sg.tok[row]) * a.hkv + nr.head) * D + 8 * c : base + t * D + 8 * c;
+          copy16_to_lds(src, dst + 1024 * j);
+        }
+        return TG::loads_per_wave;
+      }
+    }
     copy_block_to_lds(base, voff, dst);
     return TG::loads_per_wave;
   }
@@ -899,7 +953,8 @@ __device__ __forceinline__ int issue_piece_stage(unsigned char* stage, const Att
   return TG::loads_per_wave;
 }
 
-template <int D>
+// F: the append is folded in.  W: the launch starts with wide prefix blocks.
+template <int D, bool F, bool W>
 __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
   using TG = TileGeom<D>;
   constexpr int KS = D / 32;
@@ -909,12 +964,20 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
   constexpr int kVecs = int(sizeof(Seg)) / 16;
   static_assert(kVecs > 64 && kVecs <= 128, "a descriptor is two copy instructions");
   __shared__ __attribute__((aligned(1024))) unsigned char smem[decode_smem_bytes<D>()];
+  if constexpr (W) {
+    if (int(blockIdx.x) < a.num_wide) {
+      // A wide prefix block: 128 decode columns against one piece of their
+      // agent's prefix, the extend block's two-steps-per-barrier pipeline.
+      extend_block<D, 2>(a, a.plan.items + a.wide_first + blockIdx.x, smem);
+      return;
+    }
+  }
   auto ring = reinterpret_cast<unsigned char (*)[TG::stage_bytes]>(smem);
   Seg* slots = reinterpret_cast<Seg*>(smem + NS * TG::stage_bytes);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
-  const int S = gridDim.x, b = blockIdx.x;
+  const int S = int(gridDim.x) - a.num_wide, b = int(blockIdx.x) - a.num_wide;
   const int np = a.num_pieces;
 
   // The first two descriptors.
@@ -931,6 +994,7 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
   // Issue side: piece iord of the list, its next stage ik (-1: Q), and what
   // the issue needs of it.
   int iord = 0, ik = -1, inst = 0, incols = 0, iqh0 = 0, iwin = 0;
+  NewRows inew = {0, 0, 0x7fffffff, 0};
   bool in_piece = false, ended = false;
   // Per ring stage (16 bits each), what was issued into it: bit 9 valid,
   // bits 7-8 slot, bits 0-6 step + 1 (0: Q).  ops: copies this wave issued
@@ -952,13 +1016,21 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
         incols = __builtin_amdgcn_readfirstlane(h[2]);
         inst = __builtin_amdgcn_readfirstlane(h[3]);
         iwin = piece_window(sg, wave, lane);
+        if constexpr (F) {
+          const i32x4 h1 = *reinterpret_cast<const i32x4*>(&sg.h.k0);  // k0, kend, causal_base, slot
+          inew.k0 = __builtin_amdgcn_readfirstlane(h1[0]);
+          inew.kend = __builtin_amdgcn_readfirstlane(h1[1]);
+          inew.first_new = __builtin_amdgcn_readfirstlane(h[0]) == kSuffixItem ? inew.kend - (incols >> a.group_shift)
+                                                                             : 0x7fffffff;
+          inew.head = __builtin_amdgcn_readfirstlane(h[1]);
+        }
         ik = -1;
         in_piece = true;
       }
     }
     if (in_piece) {
       const int q = iord % K;
-      n_ops = issue_piece_stage<D>(ring[r], a, slots[q], iwin, ik, incols, iqh0, wave, lane, voff);
+      n_ops = issue_piece_stage<D, F>(ring[r], a, slots[q], iwin, ik, incols, iqh0, wave, lane, voff, inew);
       if (ik < 0 && wave == 0) {
         // The descriptor two pieces ahead, into the slot of the piece two back.
         const int nxt = piece_of(b, iord + 2, S);
@@ -1020,6 +1092,7 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
           k0 = __builtin_amdgcn_readfirstlane(h1[0]);
           kend = __builtin_amdgcn_readfirstlane(h1[1]);
           causal = __builtin_amdgcn_readfirstlane(h2[2]);
+          // New tokens of a suffix piece: its item's last ncols / G keys.
           has_cols = 16 * wave < ncols;
           const int c = 16 * wave + col;
           valid = c < ncols;
@@ -1033,19 +1106,21 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
             for (int s = 0; s < KS; ++s)
               qf[0][s] = *reinterpret_cast<const bf16x8*>(qb + 16 * (col * TG::chunks + 4 * s + grp));
           }
-        } else if (has_cols) {
-          attend_step<D, 1>(ws, stage, qf, lim, k0 + kStepKeys * k, kend, causal != 0, 1, lane, a.scale_log2);
-          if (k == cnst - 1) {
-            // The piece's state goes out as it stands: accumulators in their
-            // register order (group, block, element), (m, l) once per column.
-            const float l = ws.lv[0][0];  // the whole column sum in the group-0 lanes
-            if (valid) {
-              float* out = a.plan.o_part + size_t(orow) * D + grp * (4 * CH);
+        } else {
+          if (has_cols) {
+            attend_step<D, 1>(ws, stage, qf, lim, k0 + kStepKeys * k, kend, causal != 0, 1, lane, a.scale_log2);
+            if (k == cnst - 1) {
+              // The piece's state goes out as it stands: accumulators in their
+              // register order (group, block, element), (m, l) once per column.
+              const float l = ws.lv[0][0];  // the whole column sum in the group-0 lanes
+              if (valid) {
+                float* out = a.plan.o_part + size_t(orow) * D + grp * (4 * CH);
 #pragma unroll
-              for (int jj = 0; jj < CH; ++jj) *reinterpret_cast<f32x4*>(out + 4 * jj) = ws.acc[0][jj];
-              if (grp == 0) *reinterpret_cast<f32x2*>(a.plan.l_part + 2 * size_t(orow)) = f32x2{ws.m[0], l};
+                for (int jj = 0; jj < CH; ++jj) *reinterpret_cast<f32x4*>(out + 4 * jj) = ws.acc[0][jj];
+                if (grp == 0) *reinterpret_cast<f32x2*>(a.plan.l_part + 2 * size_t(orow)) = f32x2{ws.m[0], l};
+              }
+              reset_state(ws);
             }
-            reset_state(ws);
           }
         }
       }
@@ -1063,7 +1138,11 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
 // any is used.
 constexpr int kMergeBatch = 8;
 
-template <int D>
+// F: the append of this step is folded in.  The decode launch read every
+// decode token's new K/V straight from k_new / v_new; the merge, which runs
+// after it, writes them into their pool slots (2 Hkv D / 8 chunks of 16
+// bytes per token, spread over the token's threads).
+template <int D, bool F>
 __global__ __launch_bounds__(256) void merge_rows_kernel(AttnArgs a, int n_tok) {
   constexpr int CH = D / 16;
   constexpr int SL = D / 8;  // threads per row: 4 groups x CH/2 pairs
@@ -1073,6 +1152,27 @@ __global__ __launch_bounds__(256) void merge_rows_kernel(AttnArgs a, int n_tok) 
   const int grp = sl / (CH / 2), blk = 2 * (sl % (CH / 2));
   const int qh = int((t / SL) % a.hq);
   const int m = int(t / (size_t(SL) * a.hq));
+  // The append's chunks (at most two per thread: 2 Hkv <= 2 Hq), loaded
+  // beside the merge's own loads and stored at the end.
+  constexpr int kAppendPerThread = 2;
+  u32x4 app_val[kAppendPerThread];
+  uint16_t* app_dst[kAppendPerThread] = {nullptr, nullptr};
+  if constexpr (F) {
+    const int tok = a.plan.merge_tok[m];
+    const int slot = a.plan.tok_slot[tok];
+    const int per = a.hkv * SL;  // chunks of K (or V) per token
+#pragma unroll
+    for (int i = 0; i < kAppendPerThread; ++i) {
+      const int e = qh * SL + sl + i * a.hq * SL;
+      if (e < 2 * per) {
+        const bool is_v = e >= per;
+        const int hh = (e % per) / SL, c = e % SL;
+        app_val[i] = *reinterpret_cast<const u32x4*>((is_v ? a.v_new : a.k_new) + (size_t(tok) * a.hkv + hh) * D + 8 * c);
+        app_dst[i] = const_cast<uint16_t*>(is_v ? a.vpool : a.kpool) +
+                     ((size_t(slot >> 4) * a.hkv + hh) * 16 + (slot & 15)) * D + 8 * c;
+      }
+    }
+  }
   const MergeHead mh = a.plan.merge_head[size_t(m) * a.hkv + (qh >> a.group_shift)];
   const int tok = a.plan.merge_tok[m];
   const size_t row0 = size_t(mh.base) * a.group + (qh & (a.group - 1));
@@ -1118,6 +1218,11 @@ __global__ __launch_bounds__(256) void merge_rows_kernel(AttnArgs a, int n_tok) 
   *reinterpret_cast<u32x2*>(out + 16) =
       u32x2{pack_bf16(acc1[0] * inv, acc1[1] * inv), pack_bf16(acc1[2] * inv, acc1[3] * inv)};
   if (a.lse && sl == 0) a.lse[size_t(tok) * a.hq + qh] = (mx + log2f(z)) * kLn2;
+  if constexpr (F) {
+#pragma unroll
+    for (int i = 0; i < kAppendPerThread; ++i)
+      if (app_dst[i]) *reinterpret_cast<u32x4*>(app_dst[i]) = app_val[i];
+  }
 }
 
 template <int D>
@@ -1189,14 +1294,24 @@ static int check_pool_matches(const pfx_pool* pool, const pfx_plan* p, const cha
 template <int D>
 static void launch_all(AttnArgs a, const pfx_plan* p, hipStream_t s) {
   if (p->num_items > 0) hipLaunchKernelGGL((extend_kernel<D>), dim3(p->num_items), dim3(256), 0, s, a);
-  if (p->num_segs > 0) {
+  if (p->num_segs > 0 || p->num_wide > 0) {
     const int S = std::min<int>(a.num_workers, p->num_segs);
-    hipLaunchKernelGGL((decode_kernel<D>), dim3(S), dim3(256), 0, s, a);
+    const dim3 grid(p->num_wide + S);
+    if (a.fuse_append) {
+      if (p->num_wide) hipLaunchKernelGGL((decode_kernel<D, true, true>), grid, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((decode_kernel<D, true, false>), grid, dim3(256), 0, s, a);
+    } else {
+      if (p->num_wide) hipLaunchKernelGGL((decode_kernel<D, false, true>), grid, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((decode_kernel<D, false, false>), grid, dim3(256), 0, s, a);
+    }
   }
   const int n_tok = static_cast<int>(p->merge_tok.size());
   if (n_tok) {
     const size_t threads = size_t(n_tok) * p->hq * (D / 8);
-    hipLaunchKernelGGL((merge_rows_kernel<D>), dim3((threads + 255) / 256), dim3(256), 0, s, a, n_tok);
+    if (a.fuse_append)
+      hipLaunchKernelGGL((merge_rows_kernel<D, true>), dim3((threads + 255) / 256), dim3(256), 0, s, a, n_tok);
+    else
+      hipLaunchKernelGGL((merge_rows_kernel<D, false>), dim3((threads + 255) / 256), dim3(256), 0, s, a, n_tok);
   }
 }
 
@@ -1238,9 +1353,13 @@ static int launch_append(const pfx_pool* pool, const pfx_plan* p, const DevPlan&
 // The attention launches of a plan whose tables and partial states sit at
 // dp (validated by the caller).
 static int launch_attention(const pfx_pool* pool, const pfx_plan* p, const DevPlan& dp, const void* q, void* o,
-                            float* lse, float sm_scale, hipStream_t s, const char* who) {
+                            float* lse, float sm_scale, hipStream_t s, const char* who, const void* k_new = nullptr,
+                            const void* v_new = nullptr) {
   if (!(sm_scale > 0.f)) sm_scale = 1.0f / sqrtf(float(p->d));
   AttnArgs a;
+  a.k_new = static_cast<const uint16_t*>(k_new);
+  a.v_new = static_cast<const uint16_t*>(v_new);
+  a.fuse_append = k_new != nullptr;
   a.kpool = static_cast<const uint16_t*>(pool->k_pages);
   a.vpool = static_cast<const uint16_t*>(pool->v_pages);
   a.q = static_cast<const uint16_t*>(q);
@@ -1256,6 +1375,8 @@ static int launch_attention(const pfx_pool* pool, const pfx_plan* p, const DevPl
   // By default one workgroup per piece: the dispatcher hands them out as
   // compute units free up (two fit on one), in list order, longest first.
   a.num_workers = p->decode_workers > 0 ? p->decode_workers : p->num_segs;
+  a.num_wide = p->num_wide;
+  a.wide_first = p->num_items;
   if (p->d == 128) launch_all<128>(a, p, s); else launch_all<64>(a, p, s);
   return check_launch(who);
 }
@@ -1273,10 +1394,38 @@ extern "C" int pfx_attention(const pfx_pool* pool, const pfx_plan* p, const void
                              float sm_scale, void* stream) {
   int rc = check_pool_matches(pool, p, "pfx_attention");
   if (rc) return rc;
-  if (p->num_items == 0 && p->num_segs == 0) return PFX_OK;
+  if (p->num_items == 0 && p->num_segs == 0 && p->num_wide == 0) return PFX_OK;
   if (!q || !o) return fail(PFX_EINVAL, "pfx_attention: q or o is NULL");
   return launch_attention(pool, p, dev_plan(p), q, o, lse, sm_scale, static_cast<hipStream_t>(stream),
                           "pfx_attention");
+}
+
+// The append and the attention of one step in the fewest launches: with no
+// extend blocks (which read each other's new tokens) the decode pieces take
+// their new tokens straight from k_new / v_new and write them into the pool
+// themselves; otherwise the append kernel runs first.
+static int step_launches(const pfx_pool* pool, const pfx_plan* p, const DevPlan& dp, const void* k_new,
+                         const void* v_new, const void* q, void* o, float* lse, float sm_scale, hipStream_t s,
+                         const char* who) {
+  const bool attend = p->num_items > 0 || p->num_segs > 0 || p->num_wide > 0;
+  if (p->num_tokens > 0 && (p->num_items > 0 || !attend)) {
+    int rc = launch_append(pool, p, dp, k_new, v_new, s, who);
+    if (rc || !attend) return rc;
+    return launch_attention(pool, p, dp, q, o, lse, sm_scale, s, who);
+  }
+  if (!attend) return PFX_OK;
+  return launch_attention(pool, p, dp, q, o, lse, sm_scale, s, who, k_new, v_new);
+}
+
+extern "C" int pfx_step(const pfx_pool* pool, const pfx_plan* p, const void* k_new, const void* v_new,
+                        const void* q, void* o, float* lse, float sm_scale, void* stream) {
+  int rc = check_pool_matches(pool, p, "pfx_step");
+  if (rc) return rc;
+  if (p->num_tokens > 0 && (!k_new || !v_new)) return fail(PFX_EINVAL, "pfx_step: k_new or v_new is NULL");
+  if ((p->num_items > 0 || p->num_segs > 0 || p->num_wide > 0) && (!q || !o))
+    return fail(PFX_EINVAL, "pfx_step: q or o is NULL");
+  return step_launches(pool, p, dev_plan(p), k_new, v_new, q, o, lse, sm_scale, static_cast<hipStream_t>(stream),
+                       "pfx_step");
 }
 
 // ---------------------------------------------------------------------------
@@ -1330,7 +1479,7 @@ extern "C" int pfx_attention_noalloc(const pfx_pool* pool, const pfx_plan* p, co
   if (!pool->k_pages || !pool->v_pages) return fail(PFX_EINVAL, "%s: pool pointers are NULL", who);
   if ((k_new == nullptr) != (v_new == nullptr))
     return fail(PFX_EINVAL, "%s: k_new and v_new must both be given or both be NULL", who);
-  const bool attend = p->num_items > 0 || p->num_segs > 0;
+  const bool attend = p->num_items > 0 || p->num_segs > 0 || p->num_wide > 0;
   if (attend && (!q || !o)) return fail(PFX_EINVAL, "%s: q or o is NULL", who);
   if (p->total_bytes > kScratchBytes)
     return fail(PFX_ENOMEM, "%s: the plan needs %zu bytes of workspace, the static scratch holds %zu", who,
@@ -1349,9 +1498,8 @@ extern "C" int pfx_attention_noalloc(const pfx_pool* pool, const pfx_plan* p, co
     if (e != hipSuccess) return hip_fail(e, "pfx_attention_noalloc: hipMemcpyAsync");
   }
   const DevPlan dp = dev_plan(p, ws);
-  if (append && (rc = launch_append(pool, p, dp, k_new, v_new, s, who))) return rc;
-  if (attend) return launch_attention(pool, p, dp, q, o, lse, sm_scale, s, who);
-  return PFX_OK;
+  if (append) return step_launches(pool, p, dp, k_new, v_new, q, o, lse, sm_scale, s, who);
+  return launch_attention(pool, p, dp, q, o, lse, sm_scale, s, who);
 }
 
 extern "C" int pfx_merge_states(const float* o_parts, const float* lse_parts, int32_t num_parts, int32_t rows,

@@ -50,6 +50,7 @@ DevPlan dev_plan(const pfx_plan* p, void* ws) {
   DevPlan d;
   d.items = reinterpret_cast<const Item*>(base + p->off_items);
   d.row_tok = reinterpret_cast<const int32_t*>(base + p->off_row_tok);
+  d.row_out = reinterpret_cast<const int32_t*>(base + p->off_row_out);
   d.page_list = reinterpret_cast<const int32_t*>(base + p->off_page_list);
   d.tok_slot = reinterpret_cast<const int32_t*>(base + p->off_tok_slot);
   d.segs = reinterpret_cast<const Seg*>(base + p->off_segs);
@@ -314,6 +315,7 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
     int32_t row_first, rows;  // tokens drow_tok[row_first .. + rows)
     int64_t step_first;
     int32_t npieces;
+    int32_t wide;             // a prefix item of up to 128 columns, run as wide blocks (32 columns per wave)
   };
   std::vector<DItem> dit;
   std::vector<int32_t> drow_tok;
@@ -321,15 +323,24 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   for (int32_t a = 0; a < A; ++a) {
     if (!referenced[a] || pt->prefix_len[a] == 0) continue;
     std::vector<int32_t> members;
+    int64_t agent_cols = 0;
     for (int32_t r = 0; r < R; ++r)
-      if (b->agent[r] == a && is_decode_class(r)) members.push_back(r);
+      if (b->agent[r] == a && is_decode_class(r)) {
+        members.push_back(r);
+        agent_cols += int64_t(p->req[r].n) * G;
+      }
+    // An agent with more decode columns per KV head than one 64-column
+    // piece holds reads each prefix step for up to 128 columns at once
+    // (wide blocks): half the stages, each with twice the products.
+    const int32_t wide = agent_cols > kDecodeTileCols;
+    const int32_t block_cols = wide ? kExtendTileCols : kDecodeTileCols;
     size_t i = 0;
     while (i < members.size()) {
-      // A block of rows whose columns (rows x G) fit one 64-column item.
+      // A block of rows whose columns (rows x G) fit one item.
       const int32_t first = static_cast<int32_t>(drow_tok.size());
       int32_t cols = 0;
       std::vector<int32_t> in_block;
-      while (i < members.size() && cols + p->req[members[i]].n * G <= kDecodeTileCols) {
+      while (i < members.size() && cols + p->req[members[i]].n * G <= block_cols) {
         const int32_t r = members[i++];
         for (int32_t t = 0; t < p->req[r].n; ++t) drow_tok.push_back(p->req[r].q_start + t);
         cols += p->req[r].n * G;
@@ -338,7 +349,7 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
       const int32_t rows = static_cast<int32_t>(drow_tok.size()) - first;
       for (int32_t h = 0; h < hkv; ++h) {
         for (int32_t r : in_block) pf_item[size_t(r) * hkv + h] = static_cast<int32_t>(dit.size());
-        dit.push_back(DItem{kPrefixItem, h, pt->prefix_len[a], prefix_off[a], 0, first, rows, 0, 0});
+        dit.push_back(DItem{kPrefixItem, h, pt->prefix_len[a], prefix_off[a], 0, first, rows, 0, 0, wide});
         ++p->n_prefix_items;
       }
     }
@@ -351,7 +362,7 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
     for (int32_t t = 0; t < ri.n; ++t) drow_tok.push_back(ri.q_start + t);
     for (int32_t h = 0; h < hkv; ++h) {
       sf_item[size_t(r) * hkv + h] = static_cast<int32_t>(dit.size());
-      dit.push_back(DItem{kSuffixItem, h, L, suffix_off[r], L - ri.n - ri.q_start, first, ri.n, 0, 0});
+      dit.push_back(DItem{kSuffixItem, h, L, suffix_off[r], L - ri.n - ri.q_start, first, ri.n, 0, 0, 0});
       ++p->n_suffix_items;
     }
   }
@@ -425,13 +436,16 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   p->num_part_rows = part_units * G;
 
   // Longest first: a prefix step multiplies 64 query columns, a suffix step
-  // at most 16, so prefix steps weigh a little more; every piece also has a
-  // stage for its query rows.
-  const size_t nsegs = pcs.size();
+  // at most 16, so prefix steps weigh a little more (a wide prefix step,
+  // 128 columns, twice as much); every piece also has a stage for its query
+  // rows.
+  const size_t npcs = pcs.size();
   auto is_prefix = [&](int32_t k) { return dit[pcs[k].item].kind == kPrefixItem; };
-  std::vector<int32_t> pcost(nsegs), rank(nsegs);
-  for (size_t k = 0; k < nsegs; ++k) {
-    pcost[k] = (is_prefix(int32_t(k)) ? 11 : 10) * (pcs[k].s1 - pcs[k].s0) + 10;
+  auto is_wide = [&](int32_t k) { return dit[pcs[k].item].wide != 0; };
+  std::vector<int32_t> pcost(npcs), rank(npcs);
+  for (size_t k = 0; k < npcs; ++k) {
+    const int32_t w = is_wide(int32_t(k)) ? 22 : is_prefix(int32_t(k)) ? 11 : 10;
+    pcost[k] = w * (pcs[k].s1 - pcs[k].s0) + 10;
     rank[k] = static_cast<int32_t>(k);
   }
   std::stable_sort(rank.begin(), rank.end(), [&](int32_t x, int32_t y) { return pcost[x] > pcost[y]; });
@@ -446,14 +460,14 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   // behind one L2 and read it from HBM about once.  Only the order changes
   // (every piece keeps its partial slot), so results do not.
   std::vector<int32_t> order;
-  order.reserve(nsegs);
+  order.reserve(npcs);
   {
     size_t i = 0;
-    while (i < nsegs) {
+    while (i < npcs) {
       const int32_t cost = pcost[rank[i]];
       const bool prefix = is_prefix(rank[i]);
       size_t j = i;
-      while (j < nsegs && pcost[rank[j]] == cost && is_prefix(rank[j]) == prefix) ++j;
+      while (j < npcs && pcost[rank[j]] == cost && is_prefix(rank[j]) == prefix) ++j;
       if (!prefix) {
         order.insert(order.end(), rank.begin() + i, rank.begin() + j);
         i = j;
@@ -489,7 +503,14 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
     }
   }
 
-  if (nsegs > size_t(INT32_MAX)) return delete p, fail(PFX_ERANGE, "pfx_plan_create: too many decode pieces");
+  // Wide pieces run as blocks of the attention launch ahead of the decode
+  // pieces (in this order, so a chunk's blocks still sit eight apart); the
+  // others are decode pieces.
+  std::vector<int32_t> wide_order, seg_order;
+  for (int32_t k : order) (is_wide(k) ? wide_order : seg_order).push_back(k);
+  const size_t nsegs = seg_order.size();
+  if (nsegs > size_t(INT32_MAX) || wide_order.size() > size_t(INT32_MAX))
+    return delete p, fail(PFX_ERANGE, "pfx_plan_create: too many decode pieces");
 
   // ---- extend blocks (Sec. 3): up to 128 query columns of one request,
   // over the whole prefix (no mask) then the suffix (causal), written
@@ -515,19 +536,39 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
       xbs.push_back(XBlock{r, i0, i1, rbeg, int64_t(P) + (L - ri.n + i1)});
     }
   }
+  // Rows of the wide prefix blocks: their tokens and the partial row each
+  // (token, slot) leaves its state in (extend rows have no partial row).
+  p->row_out.assign(p->row_tok.size(), -1);
+  std::vector<int32_t> wide_rbeg(wide_order.size());
+  for (size_t w = 0; w < wide_order.size(); ++w) {
+    const Piece& pc = pcs[wide_order[w]];
+    const DItem& x = dit[pc.item];
+    wide_rbeg[w] = static_cast<int32_t>(p->row_tok.size());
+    for (int32_t j = 0; j < x.rows; ++j) {
+      const int32_t tok = drow_tok[x.row_first + j];
+      const int32_t r = p->tok_req[tok];
+      const size_t mrow = size_t(req_mrow[r]) + (tok - p->req[r].q_start);
+      p->row_tok.push_back(tok);
+      p->row_out.push_back((p->merge_head[mrow * hkv + x.h].base + pc.piece) * G);
+    }
+  }
+
   // Longest key ranges first keeps the tail of the launch short (the KV
   // heads of one block stay together, in order).
   std::vector<int32_t> xrank(xbs.size());
   for (size_t k = 0; k < xbs.size(); ++k) xrank[k] = static_cast<int32_t>(k);
   std::stable_sort(xrank.begin(), xrank.end(), [&](int32_t x, int32_t y) { return xbs[x].cost > xbs[y].cost; });
   const size_t nitems = xbs.size() * size_t(hkv);
-  if (nitems > size_t(INT32_MAX)) return delete p, fail(PFX_ERANGE, "pfx_plan_create: too many extend blocks");
+  if (nitems + wide_order.size() > size_t(INT32_MAX))
+    return delete p, fail(PFX_ERANGE, "pfx_plan_create: too many extend blocks");
   p->n_extend_items = static_cast<int32_t>(nitems);
+  p->num_wide = static_cast<int32_t>(wide_order.size());
 
   // ---- workspace layout ----
   size_t off = 0;
-  p->off_items = off;      off = align256(off + nitems * sizeof(Item));
+  p->off_items = off;      off = align256(off + (nitems + wide_order.size()) * sizeof(Item));
   p->off_row_tok = off;    off = align256(off + p->row_tok.size() * 4);
+  p->off_row_out = off;    off = align256(off + p->row_out.size() * 4);
   p->off_page_list = off;  off = align256(off + p->page_list.size() * 4);
   p->off_tok_slot = off;   off = align256(off + p->tok_slot.size() * 4);
   p->off_segs = off;       off = align256(off + nsegs * sizeof(Seg));
@@ -550,6 +591,7 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
     if (bytes) std::memcpy(p->blob.data() + at, src, bytes);
   };
   put(p->off_row_tok, p->row_tok.data(), p->row_tok.size() * 4);
+  put(p->off_row_out, p->row_out.data(), p->row_out.size() * 4);
   put(p->off_page_list, p->page_list.data(), p->page_list.size() * 4);
   put(p->off_tok_slot, p->tok_slot.data(), p->tok_slot.size() * 4);
   put(p->off_merge_tok, p->merge_tok.data(), p->merge_tok.size() * 4);
@@ -591,10 +633,33 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
     }
   }
 
+  // The wide prefix blocks, after the extend blocks: one piece of the
+  // agent's prefix (segment 0) against the block's decode rows, leaving
+  // partial states.
+  for (size_t w = 0; w < wide_order.size(); ++w) {
+    const Piece& pc = pcs[wide_order[w]];
+    const DItem& x = dit[pc.item];
+    Item it{};
+    it.kv_head = x.h;
+    it.row_begin = wide_rbeg[w];
+    it.row_count = x.rows;
+    it.nblk = blocks_for(x.rows);
+    it.s0_page_off = x.page_off;
+    it.s0_kbeg = pc.s0 * kStepKeys;
+    it.s0_kend = std::min(pc.s1 * kStepKeys, x.keys);
+    it.out_slot = pc.piece;
+    it.kind = kPrefixItem;
+    it.req = -1;
+    it.tok0 = -1;
+    for (int32_t k = 0, pg = it.s0_kbeg >> 4; pg < (it.s0_kend + 15) >> 4 && k < kItemPages; ++pg)
+      it.first_pages[k++] = p->page_list[it.s0_page_off + pg];
+    new (items + nit++) Item(it);
+  }
+
   // The piece records, in launch order.
   Seg* segs = reinterpret_cast<Seg*>(p->blob.data() + p->off_segs);
   for (size_t k = 0; k < nsegs; ++k) {
-    const Piece& pc = pcs[order[k]];
+    const Piece& pc = pcs[seg_order[k]];
     const DItem& x = dit[pc.item];
     const int32_t npages = static_cast<int32_t>(pages_for(x.keys));
     Seg& sg = *new (segs + k) Seg{};
@@ -647,7 +712,8 @@ extern "C" int pfx_plan_get_stats(const pfx_plan* p, pfx_plan_stats* s) {
   s->pages_needed = p->pages_needed;
   s->num_decode_steps = static_cast<int32_t>(p->num_decode_steps);
   s->num_decode_pieces = p->num_segs;
-  s->reserved[0] = s->reserved[1] = 0;
+  s->num_wide_blocks = p->num_wide;
+  s->reserved = 0;
   s->workspace_bytes = static_cast<int64_t>(p->total_bytes);
   return PFX_OK;
 }
@@ -657,8 +723,9 @@ extern "C" int pfx_plan_export(const pfx_plan* p, int32_t which, int32_t* out, i
   const int32_t* src = nullptr;
   int64_t n = 0;
   switch (which) {
-    case 0: src = reinterpret_cast<const int32_t*>(p->host_items()); n = int64_t(p->num_items) * 32; break;
+    case 0: src = reinterpret_cast<const int32_t*>(p->host_items()); n = int64_t(p->num_items + p->num_wide) * 32; break;
     case 1: src = p->row_tok.data(); n = int64_t(p->row_tok.size()); break;
+    case 8: src = p->row_out.data(); n = int64_t(p->row_out.size()); break;
     case 2: src = p->page_list.data(); n = int64_t(p->page_list.size()); break;
     case 3: src = reinterpret_cast<const int32_t*>(p->host_segs()); n = int64_t(p->num_segs) * 272; break;
     case 6: src = p->merge_tok.data(); n = int64_t(p->merge_tok.size()); break;

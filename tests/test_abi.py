@@ -167,11 +167,38 @@ def enumerate_coverage(plan, batch):
     def hit(tok, qh, k):
         counts[(tok, qh, k)] = counts.get((tok, qh, k), 0) + 1
 
-    # Extend blocks: prefix then causal suffix, final rows.
+    # Extend blocks: prefix then causal suffix, final rows.  Then the wide
+    # prefix blocks: one piece of an agent's prefix against up to 128 of
+    # its decode columns, partial rows.
     items, row_tok, page_list = plan.export(0), plan.export(1), plan.export(2)
-    for it in items:
+    row_out = plan.export(8)
+    mtok0, mhead0 = plan.export(6), plan.export(7).reshape(-1, hkv, 2)
+    midx0 = {int(t): i for i, t in enumerate(mtok0)}
+    n_ext = plan.stats().num_extend_items
+    assert len(items) == n_ext + plan.stats().num_wide_blocks
+    for it in items[n_ext:]:
+        (h, rb, rc, nblk, s0p, s0b, s0e, s1p, s1b, s1e, cbase, slot, kind, req, tok0, _) = (int(x) for x in it[:16])
+        assert kind == 0 and slot >= 0 and tok0 == -1 and s1e == s1b and s0b % 32 == 0
+        assert 1 <= rc and rc * G <= 128 and nblk == (rc * G + 15) // 16
+        first = [int(x) for x in it[16:32]]
+        lead = [int(page_list[s0p + k]) for k in range(s0b // 16, (s0e + 15) // 16)]
+        assert first[:min(16, len(lead))] == lead[:16]
+        for j in range(rc):
+            tok = int(row_tok[rb + j])
+            r, a, plen, pos = req_info(tok)
+            assert s0e <= plen
+            for g in range(G):
+                qh = h * G + g
+                for k in range(s0b, s0e):
+                    assert int(page_list[s0p + k // 16]) == int(batch.prefix_pages[a][k // 16])
+                    hit(tok, qh, k)
+                base, np_ = mhead0[midx0[tok], h]
+                row = int(row_out[rb + j]) + g
+                assert 0 <= slot < np_ and row == (base + slot) * G + g
+                outs.setdefault((tok, qh), []).append(("part", slot, row))
+    for it in items[:n_ext]:
         (h, rb, rc, nblk, s0p, s0b, s0e, s1p, s1b, s1e, cbase, slot, kind, req, tok0, _) = it[:16]
-        assert kind == 2 and slot == -1
+        assert kind == 2 and slot == -1 and int(row_out[rb]) == -1
         first = [int(x) for x in it[16:32]]
         lead = [int(page_list[s0p + k]) for k in range(s0b // 16, (s0e + 15) // 16)] if s0e > s0b else []
         lead += [int(page_list[s1p + k]) for k in range(s1b // 16, (s1e + 15) // 16)] if s1e > s1b else []
@@ -247,9 +274,16 @@ def enumerate_coverage(plan, batch):
     return counts, outs
 
 
-@pytest.mark.parametrize("case", ["small", "split", "g1", "g2", "g16", "decode_only"])
+@pytest.mark.parametrize("case", ["small", "split", "g1", "g2", "g16", "decode_only", "wide"])
 def test_plan_covers_every_visible_key_once(case):
-    if case == "g2":
+    if case == "wide":
+        # agents with 70, 200 and 24 decode columns per KV head (G = 2): wide blocks for the first two
+        reqs = [(0, 5 + i, 1) for i in range(35)] + [(1, 3 + i % 50, 1) for i in range(96)] + \
+               [(1, 20, 2), (2, 9, 3)] + [(2, 4 + i, 1) for i in range(9)] + [(0, 300, 300), (-1, 30, 1)]
+        b = W.make_batch(9, num_q_heads=16, num_kv_heads=8, head_dim=64, num_pages=4096, prefix_len=[400, 1000, 90],
+                         agent=[r[0] for r in reqs], suffix_len=[r[1] for r in reqs], n_rows=[r[2] for r in reqs])
+        kw = dict(piece_steps=5)
+    elif case == "g2":
         reqs = [(0, 140, 140), (0, 19, 3), (0, 5, 1), (0, 44, 8), (-1, 9, 9)] + [(1, 3 + i, 1) for i in range(40)]
         b = W.make_batch(8, num_q_heads=16, num_kv_heads=8, head_dim=64, num_pages=256, prefix_len=[70, 33],
                          agent=[r[0] for r in reqs], suffix_len=[r[1] for r in reqs], n_rows=[r[2] for r in reqs])
@@ -299,7 +333,9 @@ def test_plan_covers_every_visible_key_once(case):
     assert len(part_rows) == len(set(part_rows)) == p.stats().num_partial_rows
     s = p.stats()
     segs = p.export(3)
-    assert s.num_decode_pieces == len(segs) and s.num_decode_steps == int(segs[:, 3].sum())
+    wide = p.export(0)[s.num_extend_items:]
+    wide_steps = int(sum((int(w[6]) - int(w[5]) + 31) // 32 for w in wide))
+    assert s.num_decode_pieces == len(segs) and s.num_decode_steps == int(segs[:, 3].sum()) + wide_steps
 
 
 def test_plan_is_deterministic_and_placement_independent():
@@ -343,24 +379,37 @@ def test_config_plans_build_and_group_prefixes():
 
 def test_prefix_chunk_blocks_are_dealt_to_one_xcd():
     """The column blocks of one prefix chunk (same KV head and steps, other
-    decode rows) sit eight pieces apart within one dealing round, so with 512
-    persistent workgroups they run on workgroups of one XCD residue (b mod 8)
-    and share its L2.  Config 4's chunks all do; config 5's do except where a
-    group of chunks straddles a round."""
+    decode rows) sit a multiple of eight apart: decode pieces within one
+    dealing round of 512 persistent workgroups (run on workgroups of one XCD
+    residue, b mod 8), wide prefix blocks in their list (block i runs on
+    workgroup i of the launch).  Configs 4 and 5 go wide for every agent
+    with more than one 64-column block."""
     S = 512
-    for cfg, least in ((4, 1.0), (5, 0.85)):
-        segs = plan_for(W.config_batch(cfg)).export(3)
+    b = W.make_batch(5, num_q_heads=32, num_kv_heads=8, head_dim=128, num_pages=65536, prefix_len=[3000, 2500],
+                     agent=np.arange(140) % 2, suffix_len=30 + np.arange(140), n_rows=np.ones(140, np.int32))
+    for batch in (W.config_batch(4), W.config_batch(5), b):
+        p = plan_for(batch)
+        segs = p.export(3)
         pos = {}
-        for p, sg in enumerate(segs):
+        for q, sg in enumerate(segs):
             if sg[0] == 0:                    # prefix piece; sg[144]: page block of its first step
-                pos.setdefault(int(sg[144]), []).append(p)
+                pos.setdefault(int(sg[144]), []).append(q)
         multi = [ps for ps in pos.values() if len(ps) > 1]
-        assert multi
-        def wg(p):
-            n, x = divmod(p, S)
+
+        def wg(q):
+            n, x = divmod(q, S)
             return x if n % 2 == 0 else S - 1 - x
-        ok = sum(len({p // S for p in ps}) == 1 and len({wg(p) % 8 for p in ps}) == 1 for ps in multi)
-        assert ok >= least * len(multi), (cfg, ok, len(multi))
+
+        assert all(len({q // S for q in ps}) == 1 and len({wg(q) % 8 for q in ps}) == 1 for ps in multi)
+        wide = p.export(0)[p.stats().num_extend_items:]
+        wpos = {}
+        for q, w in enumerate(wide):
+            wpos.setdefault((int(w[0]), int(w[16])), []).append(q)   # (KV head, first page of the piece)
+        wmulti = [ps for ps in wpos.values() if len(ps) > 1]
+        assert all(len({q % 8 for q in ps}) == 1 for ps in wmulti)
+        assert multi or wmulti
+        if batch is not b:
+            assert not multi and wmulti           # every multi-block agent went wide
 
 
 def test_upload_rejects_small_workspace_without_gpu_work():
@@ -500,24 +549,27 @@ def test_noalloc_validates_before_touching_the_device():
 
 def test_prefix_chunk_blocks_share_an_xcd():
     """Column blocks of one prefix chunk (same KV head and first page block)
-    sit a multiple of eight positions apart in the launch order, so they run
-    on one XCD and read the chunk through its L2; only blocks beyond the
-    shortest chunk of their group of eight may break the pattern."""
+    sit a multiple of eight positions apart in the launch order (decode
+    pieces, and wide prefix blocks within their list), so they run on one
+    XCD and read the chunk through its L2; only blocks beyond the shortest
+    chunk of their group of eight may break the pattern."""
     n = [150, 70, 300]        # 4 KV heads, 3 pieces per prefix: groups of eight mix agents
     mixed = W.make_batch(3, num_q_heads=32, num_kv_heads=4, head_dim=128, num_pages=20000, prefix_len=[1536] * 3,
                          agent=np.concatenate([np.full(k, a) for a, k in enumerate(n)]),
                          suffix_len=np.full(sum(n), 40), n_rows=np.ones(sum(n), np.int32))
     for b, allowed in ((W.config_batch(5), 0.0), (W.config_batch(4), 0.0), (mixed, 0.11)):
-        segs = plan_for(b).export(3)
-        first = {}
+        p = plan_for(b)
         off = total = 0
-        for pos, row in enumerate(segs):
-            if row[0] != 0:                      # prefix pieces only
-                continue
-            key = (int(row[1]), int(row[144]), int(row[3]))
-            if key in first:
-                total += 1
-                off += (pos - first[key]) % 8 != 0
-            else:
-                first[key] = pos
+        for rows, kind_col, key_cols in ((p.export(3), 0, (1, 144, 3)),
+                                         (p.export(0)[p.stats().num_extend_items:], 12, (0, 16, 5))):
+            first = {}
+            for pos, row in enumerate(rows):
+                if row[kind_col] != 0:           # prefix pieces / wide prefix blocks only
+                    continue
+                key = tuple(int(row[c]) for c in key_cols)
+                if key in first:
+                    total += 1
+                    off += (pos - first[key]) % 8 != 0
+                else:
+                    first[key] = pos
         assert total > 0 and off <= allowed * total, (off, total)

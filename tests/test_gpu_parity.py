@@ -490,3 +490,46 @@ def test_config5_80_layers_every_layer():
         finish(pending.pop(0))
     del pools_k, pools_v
     torch.cuda.empty_cache()
+
+
+STEP_CASES = [
+    # (label, batch factory, DeviceStep options)
+    ("mixed-extend", lambda: small_batch(SMALL_CASES[1])[0], {}),                       # append kernel first
+    ("decode-multirow-g1", lambda: W.make_batch(41, num_q_heads=8, num_kv_heads=8, head_dim=64, num_pages=512,
+                                                prefix_len=[300, 45], agent=[0, 1, 0, -1, 1, 0],
+                                                suffix_len=[40, 16, 33, 20, 1, 70], n_rows=[16, 16, 1, 9, 1, 13]),
+     dict(piece_steps=1)),                                                               # new rows over 2 steps / 2 pieces
+    ("decode-multirow-g2", lambda: W.make_batch(42, num_q_heads=16, num_kv_heads=8, head_dim=128, num_pages=512,
+                                                prefix_len=[130], agent=[0, 0, -1, 0],
+                                                suffix_len=[35, 8, 64, 100], n_rows=[8, 3, 8, 1]), {}),
+    ("decode-8B", lambda: W.config_batch(2), {}),
+]
+
+
+@pytest.mark.parametrize("case", STEP_CASES, ids=[c[0] for c in STEP_CASES])
+def test_step_equals_append_then_attention(case):
+    """pfx_step (the append folded into the decode launch when the plan has
+    no extend blocks) gives the outputs of pfx_append_kv + pfx_attention bit
+    for bit, and the pool the oracle's append, with every other page
+    untouched."""
+    label, make, opts = case
+    b = make()
+    hv = W.host_values_fast(b, 77) if b.num_pages > 10000 else W.host_values(b, 77)
+    announce(f"step {label}: tokens={b.num_tokens} reqs={len(b.agent)} G={b.group} {opts}")
+    ref = RN.DeviceStep(b, hv, **opts)
+    ref.step()
+    B.pfx_sync_check()
+    o_ref, l_ref = ref.outputs()
+    del ref
+    ds = RN.DeviceStep(b, hv, **opts)
+    B.pfx_step(ds.pool, ds.plan, ds.k_new, ds.v_new, ds.q, ds.o, ds.lse)
+    B.pfx_sync_check()
+    o, l = ds.outputs()
+    assert np.array_equal(o, o_ref) and np.array_equal(l, l_ref), f"{label}: step differs from append + attention"
+    exp_k, exp_v = PT.expected_pools(b, hv)
+    gk, gv = ds.read_pages(hv.pages)
+    assert np.array_equal(gk, exp_k) and np.array_equal(gv, exp_v), f"{label}: pool differs from the oracle's append"
+    assert_untouched(ds, hv.pages, label)
+    o_or, l_or = PT.reference(b, hv, (exp_k, exp_v))
+    res = PT.compare(b, o, l, o_or, l_or, label)
+    announce(f"step {label}: bit-identical to append + attention; oracle max_abs={res[0]:.2e} rel={res[1]:.2e}")
