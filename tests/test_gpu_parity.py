@@ -160,6 +160,11 @@ SMALL_CASES = [
      + [(1, 3 + i, 1) for i in range(40)], {}),
     (9, 16, 8, 128, [70, 33], [(0, 140, 140), (0, 19, 3), (0, 5, 1), (0, 44, 8), (-1, 9, 9)]
      + [(1, 3 + i, 1) for i in range(40)], dict(piece_steps=1)),
+    # G = 16, one KV head: agent 0's 9 decode rows are 144 columns (two wide blocks) over 5 one-step
+    # prefix pieces, 10 wide blocks beside 19 decode pieces.  The launch interleaves one round of
+    # 8 wide blocks and 8 pieces, then runs the other 11 pieces, then the 2 wide blocks left over.
+    (10, 16, 1, 128, [160, 40], [(0, 10 + 7 * i, 1) for i in range(9)] + [(1, 30, 1), (0, 50, 50), (-1, 9, 1)],
+     dict(piece_steps=1)),
 ]
 
 
