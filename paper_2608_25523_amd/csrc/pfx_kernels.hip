@@ -383,6 +383,7 @@ __device__ __forceinline__ uint32_t lds_address(const unsigned char* p) {
 
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) s16x4* lds_s16x4;
 
 // V^T operand of output block blk (dims 16 blk .. 16 blk + 15 as the MFMA
@@ -401,30 +402,40 @@ __device__ __forceinline__ bf16x8 v_operand_tr(const unsigned char* v0, const un
   const int off = 16 * swizzled_slot<chunks>(row, 2 * blk + (q >> 1)) + 8 * (q & 1);
   const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(v0 + off));
   const s16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(v1 + off));
-  const uint64_t ua = __builtin_bit_cast(uint64_t, a);
-  const uint64_t ub = __builtin_bit_cast(uint64_t, b);
-  u32x4 w = {uint32_t(ua), uint32_t(ua >> 32), uint32_t(ub), uint32_t(ub >> 32)};
-  return __builtin_bit_cast(bf16x8, w);
+  // Concatenated as 16-bit vectors: through 32-bit words, the compiler
+  // rebuilds the bf16 elements with a bitfield insert per register.
+  const s16x8 ab = __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8, ab);
 }
 
 // Zero, in a step's V^T operands, the keys at or past kend (their slots may
 // hold anything, and 0 * NaN is NaN).  Element e of each half of an operand
 // is key k0 + 16 t + 4 grp + e.
+// The masks are applied by an opaque AND: written as C, the compiler folds
+// them into bitfield inserts that it then also runs, as no-ops, on the steps
+// that need no zeroing.
+__device__ __forceinline__ uint32_t and_opaque(uint32_t x, uint32_t m) {
+  uint32_t r;
+  asm volatile("v_and_b32 %0, %1, %2" : "=v"(r) : "v"(x), "v"(m));
+  return r;
+}
 template <int D>
 __device__ __forceinline__ void zero_v_tail(bf16x8 (&vop)[D / 16], int k0, int kend, int grp) {
-  uint32_t keep[2][2] = {{~0u, ~0u}, {~0u, ~0u}};
+  uint32_t keep[2][2];
 #pragma unroll
   for (int t = 0; t < 2; ++t)
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
-      if (k0 + 16 * t + 4 * grp + e >= kend) keep[t][e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
+    for (int h2 = 0; h2 < 2; ++h2) {
+      const int key = k0 + 16 * t + 4 * grp + 2 * h2;  // element 2 h2 (low half) and 2 h2 + 1 (high half)
+      keep[t][h2] = (key < kend ? 0x0000FFFFu : 0u) | (key + 1 < kend ? 0xFFFF0000u : 0u);
+    }
 #pragma unroll
   for (int blk = 0; blk < D / 16; ++blk) {
     u32x4 w = __builtin_bit_cast(u32x4, vop[blk]);
-    w[0] &= keep[0][0];
-    w[1] &= keep[0][1];
-    w[2] &= keep[1][0];
-    w[3] &= keep[1][1];
+    w[0] = and_opaque(w[0], keep[0][0]);
+    w[1] = and_opaque(w[1], keep[0][1]);
+    w[2] = and_opaque(w[2], keep[1][0]);
+    w[3] = and_opaque(w[3], keep[1][1]);
     vop[blk] = __builtin_bit_cast(bf16x8, w);
   }
 }
