@@ -159,4 +159,22 @@ def test_prefix_round_trip_by_copy_engines():
     assert np.array_equal(k2, k0) and np.array_equal(v2, v0), "direct copies into consecutive pages differ"
     with pytest.raises(ValueError):
         mover.load_dma(run - run_at - 1, slots, pool_tensors=(ds.k_pool, ds.v_pool))
-    announce("movement (copy engines): round trip bit-exact, outputs bit-identical")
+    # Paced: the staged reload cut into parts, part i waiting for the i-th of
+    # the attention calls beside it.
+    ds.k_pool.view(torch.int16).index_fill_(0, idx, W.POISON_BF16)
+    ds.v_pool.view(torch.int16).index_fill_(0, idx, W.POISON_BF16)
+    side.wait_stream(main)
+    events = []
+    for _ in range(12):
+        B.pfx_attention(ds.pool, plan2, q2, o2, lse2)
+        ev = torch.cuda.Event()
+        ev.record(main)
+        events.append(ev)
+    mover.load_dma(pages, slots, stream=side.cuda_stream, after=events)
+    main.wait_stream(side)
+    torch.cuda.synchronize()
+    B.pfx_sync_check()
+    k3, v3 = ds.read_pages(pages)
+    assert np.array_equal(k3, k0) and np.array_equal(v3, v0), "paced reload differs"
+    assert np.array_equal(RN.to_host_bits(o2), o2_alone) and np.array_equal(lse2.cpu().numpy(), lse2_alone)
+    announce("movement (copy engines): round trip bit-exact, outputs bit-identical, paced reload bit-exact")

@@ -50,3 +50,21 @@ def test_cost_counts_each_waiting_task_once():
     t = 100 * MU / B_SWAP
     j = OM.movement_cost(MU, B_SWAP, lens, {0}, {0, 1}, [(4, 1), (4, 1), (5, 1), (6, 0)])
     assert j == pytest.approx(2 * t)
+
+
+def test_paced_load_parts_keep_every_copy_in_order():
+    """The copy-engine load cut into parts (one per event it waits for):
+    every page copied once, in order, the parts as even as the page counts
+    allow, and exactly as many parts as events."""
+    from paper_2608_25523_amd.movement import Mover
+
+    ops = [("k", "v", 0, 100, 10), ("k", "v", 50, 7, 3), ("k", "v", 200, 30, 20)]
+    want = [(d0 + i, s0 + i) for (_, _, d0, s0, m) in ops for i in range(m)]
+    for n in (1, 2, 4, 7, 33, 40):
+        parts = Mover._split(ops, n)
+        assert len(parts) == n
+        flat = [(d0 + i, s0 + i) for p in parts for (_, _, d0, s0, m) in p for i in range(m)]
+        assert flat == want
+        sizes = [sum(op[4] for op in p) for p in parts]
+        assert max(sizes) == -(-33 // n) or n > 33
+    assert Mover._split([], 3) == [[], [], []]
