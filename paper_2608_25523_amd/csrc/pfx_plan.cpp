@@ -553,11 +553,20 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
     }
   }
 
-  // Longest key ranges first keeps the tail of the launch short (the KV
-  // heads of one block stay together, in order).
+  // Blocks of one agent together, longest key ranges first within it.  The
+  // KV heads of one block stay together, in order, and the dispatcher deals
+  // workgroups to the 8 XCDs in turn, so with 8 KV heads an XCD runs one
+  // head: grouped by agent, the blocks it runs at a time read one prefix,
+  // about the same keys at about the same time, through its L2 (ordered by
+  // length alone, they read every agent's prefix at once).  The launch still
+  // ends on the shortest blocks of the last agent.
   std::vector<int32_t> xrank(xbs.size());
   for (size_t k = 0; k < xbs.size(); ++k) xrank[k] = static_cast<int32_t>(k);
-  std::stable_sort(xrank.begin(), xrank.end(), [&](int32_t x, int32_t y) { return xbs[x].cost > xbs[y].cost; });
+  std::stable_sort(xrank.begin(), xrank.end(), [&](int32_t x, int32_t y) {
+    const int32_t ax = b->agent[xbs[x].r], ay = b->agent[xbs[y].r];
+    if (ax != ay) return ax > ay;  // requests without a prefix (-1) last
+    return xbs[x].cost > xbs[y].cost;
+  });
   const size_t nitems = xbs.size() * size_t(hkv);
   if (nitems + wide_order.size() > size_t(INT32_MAX))
     return delete p, fail(PFX_ERANGE, "pfx_plan_create: too many extend blocks");
