@@ -30,6 +30,8 @@ import os
 import sys
 import time
 
+import numpy as np
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
@@ -129,6 +131,18 @@ def bench_decode(args, torch, B, RN, W):
 
     ms, attn_ms, spread = timed_steps(step, attn, args.steps, args.warmup, torch)
     unfused_ms, _ = attention_ms(unfused, max(args.steps, MIN_ATTN_CALLS), torch)
+    # The same attention with the decode pieces on the vector ALU (dot
+    # products instead of MFMA tiles), for the engine comparison.
+    vplans = [B.plan_from_batch(ds.pool, rb, B.PFX_MODE_DECODE, decode_engine=B.PFX_DECODE_VALU).upload()
+              for rb in reps]
+
+    def attn_valu(i):
+        B.pfx_attention(ds.pool, vplans[i % len(vplans)], ds.q, ds.o, ds.lse)
+
+    for i in range(args.warmup):
+        attn_valu(i)
+    valu_ms, valu_spread = attention_ms(attn_valu, max(args.steps, MIN_ATTN_CALLS), torch)
+    del vplans
     B.pfx_sync_check()
     graph_ms = graph_replay_ms(plans, ds, args.steps, torch, B)
     side = side_costs(b, ds, plans, args.steps, torch, B)
@@ -136,7 +150,48 @@ def bench_decode(args, torch, B, RN, W):
     st = ds.plan.stats()
     side["unfused_step_us"] = round(unfused_ms * 1e3, 3)
     return dict(batch=b, hv=hv, ms=ms, attn_ms=attn_ms, spread=spread, graph_ms=graph_ms, unique_bytes=u,
-                replicas=len(plans), stats=st, side=side)
+                replicas=len(plans), stats=st, side=side, valu_ms=valu_ms, valu_spread=valu_spread)
+
+
+def bench_prefix_engines(args, torch, B, RN, W):
+    """The grouped-decode prefix phase alone on each decode engine: decode-8B's
+    agents and prefixes with a one-token suffix per request, so nearly all of
+    the work is prefix steps shared by 64 columns.  Each engine at piece
+    lengths 4, 8 and 16 steps (one workgroup per piece: 1024, 768 and 640
+    workgroups), rotating over replicas as the decode-8B bench does."""
+    rng = np.random.Generator(np.random.PCG64(2608))
+    agents = np.repeat(np.arange(4), 16).astype(np.int32)[rng.permutation(64)]
+    b = W.make_batch(2608, num_q_heads=32, num_kv_heads=8, head_dim=128, num_pages=65536, prefix_len=[2048] * 4,
+                     agent=agents, suffix_len=np.ones(64, np.int32), n_rows=np.ones(64, np.int32))
+    ds = RN.DeviceStep(b, W.host_values_fast(b, 2609), poison=False)
+    reps = W.replicas(b, args.replicas, 79)
+    src = torch.from_numpy(b.used_pages()).cuda()
+    for rb in reps[1:]:
+        dst = torch.from_numpy(rb.used_pages()).cuda()
+        ds.k_pool.view(torch.int16).index_copy_(0, dst, ds.k_pool.view(torch.int16).index_select(0, src))
+        ds.v_pool.view(torch.int16).index_copy_(0, dst, ds.v_pool.view(torch.int16).index_select(0, src))
+    torch.cuda.synchronize()
+    out = {"workload": "decode-8B prefix phase: Hq32/Hkv8/d128, 4 prefixes x 2048, 64 decode reqs (16/agent) "
+                       "with a 1-token suffix each", "unique_kv_bytes": b.unique_kv_bytes(), "replicas": len(reps)}
+    for name, eng in (("mfma", B.PFX_DECODE_MFMA), ("valu", B.PFX_DECODE_VALU)):
+        by = {}
+        for ps in (4, 8, 16):
+            plans = [B.plan_from_batch(ds.pool, rb, B.PFX_MODE_DECODE, piece_steps=ps, decode_engine=eng).upload()
+                     for rb in reps]
+
+            def attn(i, plans=plans):
+                B.pfx_attention(ds.pool, plans[i % len(plans)], ds.q, ds.o, ds.lse)
+
+            for i in range(args.warmup):
+                attn(i)
+            ms, _ = attention_ms(attn, max(args.steps, MIN_ATTN_CALLS), torch)
+            by[ps] = round(ms * 1e3, 3)
+            del plans
+        best = min(by, key=by.get)
+        out[name] = {"attn_us": by[best], "piece_steps": best, "attn_us_by_piece_steps": by}
+    B.pfx_sync_check()
+    out["valu_over_mfma"] = round(out["valu"]["attn_us"] / out["mfma"]["attn_us"], 3)
+    return out
 
 
 def side_costs(b, ds, plans, steps, torch, B):
@@ -683,6 +738,8 @@ def main():
     ap.add_argument("--no-configs", action="store_true", help="skip configs 1, 4 and 5 (about a minute)")
     ap.add_argument("--more", action="store_true",
                     help="also time prefix movement, the rebuild of a preempted request and the service tables")
+    ap.add_argument("--engines-only", action="store_true",
+                    help="only the prefix-phase comparison of the two decode engines (for counter passes)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run a 1 GiB device copy (counter calibration for rocprofv3 --pmc runs)")
     args = ap.parse_args()
@@ -697,19 +754,26 @@ def main():
     from paper_2608_25523_amd import workloads as W
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.engines_only:
+        print(json.dumps({"prefix_phase_engines": bench_prefix_engines(args, torch, B, RN, W)}), flush=True)
+        return
     if args.calib_copy:
         log(f"calibration copy: {copy_calibration(torch, B)} bytes moved per launch")
     copy_gbs = measured_copy_peak(torch, B)
     log(f"measured device page copy: {copy_gbs:.0f} GB/s (read + write)")
     log("decode-8B: building inputs")
     dec = bench_decode(args, torch, B, RN, W)
-    log(f"decode-8B: {dec['ms'] * 1e3:.1f} us/step, attention {dec['attn_ms'] * 1e3:.1f} us")
+    log(f"decode-8B: {dec['ms'] * 1e3:.1f} us/step, attention {dec['attn_ms'] * 1e3:.1f} us "
+        f"(vector-ALU engine {dec['valu_ms'] * 1e3:.1f} us)")
     ext = None
     if not args.no_extend:
         log("extend-8B: building inputs")
         ext = bench_extend(args, torch, B, RN, W)
         log(f"extend-8B: {ext['ms']:.3f} ms/step, attention {ext['attn_ms']:.3f} ms, "
             f"append {ext['append_ms']:.3f} ms")
+    log("decode-8B prefix phase on both decode engines")
+    engines = bench_prefix_engines(args, torch, B, RN, W)
+    log(f"prefix phase: MFMA {engines['mfma']['attn_us']} us, VALU {engines['valu']['attn_us']} us")
     configs = None
     if not args.no_configs:
         log("configs 1, 4, 5")
@@ -758,6 +822,14 @@ def main():
                      "measured_peak_kind": "pfx_page_copy device to device, random 32 KiB pages, read + write",
                      "attn_us": round(dec["attn_ms"] * 1e3, 3), "attn_calls": dec["spread"]["calls"],
                      "attn_us_p10_p50_p90": [round(dec["spread"][k] * 1e3, 3) for k in ("p10", "p50", "p90")]},
+        "decode_valu_engine": {
+            "kernel": "pfx_attention with decode_engine = PFX_DECODE_VALU: decode_kernel on v_dot2_f32_bf16 "
+                      "+ merge_rows_kernel",
+            "attn_us": round(dec["valu_ms"] * 1e3, 3), "calls": dec["valu_spread"]["calls"],
+            "GBs": round(u / (dec["valu_ms"] * 1e-3) / 1e9, 2),
+            "frac": round(u / (dec["valu_ms"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "vs_mfma": round(dec["valu_ms"] / dec["attn_ms"], 3)},
+        "prefix_phase_engines": engines,
         "graph_ms_per_step": None if dec["graph_ms"] is None else round(dec["graph_ms"], 5),
         "step_parts": dec["side"],
         "cpu_baseline": cpu,

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define PFX_VERSION 20100 /* 2.1.0 */
+#define PFX_VERSION 20200 /* 2.2.0 */
 
 #define PFX_OK 0
 #define PFX_EINVAL (-1)       /* malformed argument (null pointer, bad CSR, overlapping pages, ...) */
@@ -174,8 +174,18 @@ typedef struct pfx_plan_opts {
    * balance the workgroups better but give each decode row more partial
    * results to merge. */
   int32_t piece_steps;
-  int32_t reserved[6]; /* must be zero */
+  /* Engine of the decode pieces: PFX_DECODE_MFMA (0, the default: matrix
+   * cores, and wide prefix blocks for agents with more than 64 decode
+   * columns per KV head) or PFX_DECODE_VALU (two-wide bf16 dot products on
+   * the vector ALU, no wide blocks).  Same results within rounding; the
+   * vector-ALU engine is slower and is kept to compare the two on hardware
+   * counters.  Extend blocks always run on the matrix cores. */
+  int32_t decode_engine;
+  int32_t reserved[5]; /* must be zero */
 } pfx_plan_opts;
+
+#define PFX_DECODE_MFMA 0
+#define PFX_DECODE_VALU 1
 
 typedef struct pfx_plan_stats {
   int32_t num_requests;

@@ -25,6 +25,8 @@ PFX_PAGE_SIZE = 16
 PFX_MODE_EXTEND = 1
 PFX_MODE_DECODE = 2
 PFX_MODE_MIXED = 3
+PFX_DECODE_MFMA = 0
+PFX_DECODE_VALU = 1
 PFX_NOALLOC_MAX_WORKSPACE = 128 << 20
 
 _ERR_NAMES = {PFX_EINVAL: "PFX_EINVAL", PFX_ERANGE: "PFX_ERANGE", PFX_ENOMEM: "PFX_ENOMEM",
@@ -63,7 +65,8 @@ class pfx_batch(C.Structure):
 
 
 class pfx_plan_opts(C.Structure):
-    _fields_ = [("decode_workers", C.c_int32), ("piece_steps", C.c_int32), ("reserved", C.c_int32 * 6)]
+    _fields_ = [("decode_workers", C.c_int32), ("piece_steps", C.c_int32), ("decode_engine", C.c_int32),
+                ("reserved", C.c_int32 * 5)]
 
 
 class pfx_plan_stats(C.Structure):
@@ -238,7 +241,7 @@ class Plan:
 
 def pfx_plan_create(pool: pfx_pool, prefix_page_indptr, prefix_page_ids, prefix_len, agent, suffix_indptr,
                     suffix_page_ids, suffix_len, q_indptr, num_q_heads: int, mode: int,
-                    decode_workers: int = 0, piece_steps: int = 0) -> Plan:
+                    decode_workers: int = 0, piece_steps: int = 0, decode_engine: int = 0) -> Plan:
     keep = []
 
     def arr(x):
@@ -250,7 +253,7 @@ def pfx_plan_create(pool: pfx_pool, prefix_page_indptr, prefix_page_ids, prefix_
     pt = pfx_prefix_table(num_agents, arr(prefix_page_indptr), arr(prefix_page_ids), arr(prefix_len))
     num_reqs = len(agent)
     b = pfx_batch(num_reqs, arr(agent), arr(suffix_indptr), arr(suffix_page_ids), arr(suffix_len), arr(q_indptr))
-    opts = pfx_plan_opts(decode_workers, piece_steps)
+    opts = pfx_plan_opts(decode_workers, piece_steps, decode_engine)
     h = C.c_void_p()
     _check(LIB.pfx_plan_create(C.byref(pool), C.byref(pt), C.byref(b), num_q_heads, mode, C.byref(opts),
                                C.byref(h)))

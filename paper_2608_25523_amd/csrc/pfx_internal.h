@@ -131,6 +131,7 @@ struct ReqInfo {
 struct pfx_plan {
   int32_t num_pages = 0, hkv = 0, d = 0, hq = 0, group = 0, mode = 0;
   int32_t decode_workers = 0;  // decode workgroups requested (0: one per piece)
+  int32_t decode_engine = 0;   // PFX_DECODE_MFMA or PFX_DECODE_VALU
   int32_t num_reqs = 0, num_tokens = 0;
   int32_t num_items = 0;       // extend blocks (their records live in the blob at off_items)
   int32_t num_wide = 0;        // wide prefix blocks, after the extend blocks in the same array

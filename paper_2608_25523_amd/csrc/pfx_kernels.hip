@@ -30,6 +30,7 @@
 #include <algorithm>
 #include <cmath>
 #include <mutex>
+#include <type_traits>
 
 #include "pfx_internal.h"
 
@@ -542,6 +543,246 @@ __device__ __forceinline__ void attend_step(WaveState<D, QB>& ws, const unsigned
   }
 }
 
+// ---------------------------------------------------------------------------
+// Decode on the vector ALU (a plan option): the same pieces, LDS ring and
+// online softmax as above, with both contractions done by two-wide bf16 dot
+// products (v_dot2_f32_bf16) instead of the matrix unit.  It exists to set
+// the two engines side by side on counters; the matrix unit is the default.
+//
+// Scores: lane (col, grp) holds its column's whole Q row and forms the
+// scores of keys 16 t + 4 grp + i, the MFMA layout, so masking and the
+// softmax are the same code.
+// P V: lane (c, grp) accumulates columns 4 grp .. 4 grp + 3 at dims
+// 16 blk + c over all 32 keys of a step.  V^T comes from the transposing LDS
+// read (two keys per word, as the MFMA path reads it, for all four key
+// groups), P from an exchange through LDS (each lane publishes the packed P
+// of its column and keys).  At the end of a piece the accumulators are
+// transposed into the MFMA state layout through LDS.
+// All exchanges stay inside one wave: LDS serves a wave's instructions in
+// order, and a wave-scope fence keeps the compiler from reordering them.
+// ---------------------------------------------------------------------------
+// LDS per wave: P exchange (4 key groups x 16 columns x 16 bytes), the
+// rescale factors of the 16 columns, and, at a piece end, a 16 x 36-float
+// transpose buffer over the same bytes.
+constexpr int kValuXchgBytes = 16 * 36 * 4;
+constexpr int kValuAlphaOffset = 1024;
+
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c, false);
+}
+
+template <int D>
+struct ValuState {
+  static constexpr int CH = D / 16;
+  float acc[4][CH];  // lane (c, grp): column 4 grp + j, dim 16 blk + c
+  float m;           // running max of the lane's column (log2 units), same in its four lanes
+  float l;           // running sum of P over the lane's keys
+};
+
+template <int D>
+__device__ __forceinline__ void reset_state(ValuState<D>& vs) {
+  vs.m = kNegBig;
+  vs.l = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int blk = 0; blk < D / 16; ++blk) vs.acc[j][blk] = 0.f;
+}
+
+// Lane offsets of the vector-ALU reads within a page tile.  The row key is
+// XOR-linear, so key(4 a + b) = key(4 a) ^ key(b) for b < 4; with it, one
+// offset per chunk position serves every key and block, and the rest of each
+// address is a compile-time immediate.
+//   k[w]: row 4 grp + i, chunk u sits at k[u ^ key(i)] + 16 chunks i;
+//   v[c]: the transposing read of key group kg, block blk sits at
+//         v[2 blk ^ key(4 kg)] + 16 chunks 4 kg (lane 4 e + q of a 16-lane
+//         group addresses row 4 kg + e, chunk 2 blk + q / 2, half q % 2).
+template <int D>
+struct ValuOffsets {
+  static constexpr int chunks = D / 8;
+  uint32_t k[chunks];
+  uint32_t v[chunks];
+};
+
+template <int D>
+__device__ __forceinline__ void valu_offsets(ValuOffsets<D>& o, int lane) {
+  constexpr int chunks = D / 8;
+  const int grp = lane >> 4, s = lane & 15, e = s >> 2, q = s & 3;
+  const int kgrp = row_key<chunks>(4 * grp);
+  const int lv = (q >> 1) ^ row_key<chunks>(e);
+#pragma unroll
+  for (int w = 0; w < chunks; ++w) {
+    o.k[w] = uint32_t(16 * (4 * grp * chunks + (w ^ kgrp)));
+    o.v[w] = uint32_t(16 * (e * chunks + (w ^ lv)) + 8 * (q & 1));
+  }
+}
+
+// O += P V for one step on the vector ALU: lane (c, grp) adds, for columns
+// 4 grp + j and dims 16 blk + c, the products over all 32 keys.  px: the
+// packed P of every (key group, column).  T: the step ends inside its keys,
+// whose V slots past kend may hold anything (0 * NaN is NaN) and are zeroed;
+// a separate instance, so the common path reads one key group's V^T at a
+// time instead of the whole step's before a branch.
+template <int D, bool T>
+__device__ __forceinline__ void valu_pv(ValuState<D>& vs, const unsigned char* stage, const ValuOffsets<D>& off,
+                                        const u32x4* px, int k0, int kend, int grp) {
+  using TG = TileGeom<D>;
+  constexpr int CH = D / 16;
+  constexpr int chunks = TG::chunks;
+  const unsigned char* v0 = stage + 2 * TG::page_bytes;
+  const unsigned char* v1 = stage + 3 * TG::page_bytes;
+#pragma unroll
+  for (int kg = 0; kg < 4; ++kg) {
+    u32x4 pj[4];  // P of columns 4 grp + j for key group kg
+#pragma unroll
+    for (int j = 0; j < 4; ++j) pj[j] = px[16 * kg + 4 * grp + j];
+    uint32_t keep[4] = {~0u, ~0u, ~0u, ~0u};
+    if constexpr (T) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2) {
+          const int key = k0 + 16 * t + 4 * kg + 2 * h2;  // the word's two keys: key, key + 1
+          keep[2 * t + h2] = (key < kend ? 0x0000FFFFu : 0u) | (key + 1 < kend ? 0xFFFF0000u : 0u);
+        }
+    }
+    const int kk = row_key<chunks>(4 * kg);
+#pragma unroll
+    for (int blk = 0; blk < CH; ++blk) {
+      const uint32_t o = off.v[(2 * blk) ^ kk] + 16 * chunks * 4 * kg;
+      const s16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(v0 + o));
+      const s16x4 y = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(v1 + o));
+      u32x4 vw = __builtin_bit_cast(u32x4, __builtin_shufflevector(x, y, 0, 1, 2, 3, 4, 5, 6, 7));
+      if constexpr (T) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) vw[w] &= keep[w];
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        float acc = vs.acc[j][blk];
+#pragma unroll
+        for (int w = 0; w < 4; ++w) acc = dot2_bf16(vw[w], pj[j][w], acc);
+        vs.acc[j][blk] = acc;
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// One 32-key step of a decode piece on the vector ALU (16 query columns per
+// wave, as attend_step with one block).  qrow: the lane's column's Q (D / 8
+// chunks); xchg: the wave's LDS exchange area.
+template <int D>
+__device__ __forceinline__ void attend_step_valu(ValuState<D>& vs, const unsigned char* stage,
+                                                 const u32x4 (&qrow)[D / 8], const ValuOffsets<D>& off, int lim,
+                                                 int k0, int kend, bool causal, int lane, float scale_log2,
+                                                 unsigned char* xchg) {
+  using TG = TileGeom<D>;
+  constexpr int CH = D / 16;
+  constexpr int chunks = TG::chunks;
+  const int col = lane & 15, grp = lane >> 4;
+  const bool tail = k0 + kStepKeys > kend;
+  float v[8];
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const unsigned char* krow = stage + t * TG::page_bytes + 16 * chunks * i;
+      const int ki = row_key<chunks>(i);
+      float sc = 0.f;
+#pragma unroll
+      for (int u = 0; u < chunks; ++u) {
+        const u32x4 kw = *reinterpret_cast<const u32x4*>(krow + off.k[u ^ ki]);
+#pragma unroll
+        for (int w = 0; w < 4; ++w) sc = dot2_bf16(kw[w], qrow[u][w], sc);
+      }
+      v[4 * t + i] = sc;
+    }
+  if (tail || causal) {
+    PFX_KEEP_BRANCH();
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = k0 + 16 * t + 4 * grp + i;
+        if (key >= kend || (causal && key > lim)) v[4 * t + i] = -INFINITY;
+      }
+  }
+  float mx = v[0];
+#pragma unroll
+  for (int i = 1; i < 8; ++i) mx = __builtin_elementwise_maximum(mx, v[i]);
+  if (__any(mx * scale_log2 > vs.m + kRescaleSlack)) {
+    PFX_KEEP_BRANCH();
+    mx = column_max(mx) * scale_log2;
+    const bool raise = mx > vs.m + kRescaleSlack;
+    const float mnew = raise ? mx : vs.m;
+    const float alpha = fast_exp2(vs.m - mnew);
+    vs.l *= alpha;
+    vs.m = mnew;
+    // The lane's accumulators belong to columns 4 grp .. 4 grp + 3.
+    float* al = reinterpret_cast<float*>(xchg + kValuAlphaOffset);
+    if (grp == 0) al[col] = alpha;
+    wave_lds_sync();
+    const f32x4 a4 = reinterpret_cast<const f32x4*>(al)[grp];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int blk = 0; blk < CH; ++blk) vs.acc[j][blk] *= a4[j];
+    wave_lds_sync();
+  }
+  const float neg_m = -vs.m;
+  float pr[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) pr[j] = fast_exp2(fmaf(v[j], scale_log2, neg_m));
+  const u32x4 pw = {pack_bf16(pr[0], pr[1]), pack_bf16(pr[2], pr[3]), pack_bf16(pr[4], pr[5]), pack_bf16(pr[6], pr[7])};
+  // The row sum of the rounded P, as the products see it.
+  float ps = 0.f;
+#pragma unroll
+  for (int w = 0; w < 4; ++w)
+    ps += __builtin_bit_cast(float, pw[w] << 16) + __builtin_bit_cast(float, pw[w] & 0xFFFF0000u);
+  vs.l += ps;
+  u32x4* px = reinterpret_cast<u32x4*>(xchg);  // [key group][column]
+  px[16 * grp + col] = pw;
+  wave_lds_sync();
+  if (tail) {
+    PFX_KEEP_BRANCH();
+    valu_pv<D, true>(vs, stage, off, px, k0, kend, grp);
+  } else {
+    valu_pv<D, false>(vs, stage, off, px, k0, kend, grp);
+  }
+  wave_lds_sync();
+}
+
+// End of a piece on the vector ALU: the column sum l, and the accumulators
+// transposed into the MFMA state layout (o[blk][i] = dim 16 blk + 4 grp + i
+// of column col), 32 dims at a time through a [16 columns][36 floats]
+// buffer (the padding spreads the 64 lanes' stores over all banks).
+template <int D>
+__device__ __forceinline__ void valu_finish(const ValuState<D>& vs, unsigned char* xchg, int lane, f32x4 (&o)[D / 16],
+                                            float& l) {
+  constexpr int CH = D / 16;
+  const int col = lane & 15, grp = lane >> 4;
+  l = column_sum(vs.l);
+  float* tb = reinterpret_cast<float*>(xchg);
+#pragma unroll
+  for (int p = 0; p < CH / 2; ++p) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int bb = 0; bb < 2; ++bb) tb[(4 * grp + j) * 36 + 16 * bb + col] = vs.acc[j][2 * p + bb];
+    wave_lds_sync();
+#pragma unroll
+    for (int bb = 0; bb < 2; ++bb) o[2 * p + bb] = *reinterpret_cast<const f32x4*>(tb + col * 36 + 16 * bb + 4 * grp);
+    wave_lds_sync();
+  }
+}
+
 // Two consecutive 32-key steps of an extend block under one barrier,
 // against the wave's QB blocks of 16 query columns (blocks past the wave's
 // columns compute on zero queries and are never written):
@@ -888,9 +1129,10 @@ __global__ __launch_bounds__(256, 2) void extend_kernel(AttnArgs a) {
 // issues with the Q stage two pieces earlier; it is complete once that stage
 // has been waited for, long before the issue reaches the piece.
 // ---------------------------------------------------------------------------
-template <int D>
+// V: the decode pieces run on the vector ALU, with a per-wave exchange area.
+template <int D, bool V>
 constexpr int decode_smem_bytes() {
-  return kStages * TileGeom<D>::stage_bytes + kPieceSlots * int(sizeof(Seg));
+  return kStages * TileGeom<D>::stage_bytes + kPieceSlots * int(sizeof(Seg)) + (V ? 4 * kValuXchgBytes : 0);
 }
 
 // Piece of workgroup b at position n of its list (>= num_pieces: none).
@@ -965,8 +1207,10 @@ __device__ __forceinline__ int issue_piece_stage(unsigned char* stage, const Att
 }
 
 // F: the append is folded in.  W: the launch starts with wide prefix blocks.
-template <int D, bool F, bool W>
+// V: the pieces run on the vector ALU (no wide blocks then).
+template <int D, bool F, bool W, bool V>
 __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
+  static_assert(!(V && W), "wide blocks run on the matrix unit");
   using TG = TileGeom<D>;
   constexpr int KS = D / 32;
   constexpr int CH = D / 16;
@@ -974,7 +1218,7 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
   constexpr int K = kPieceSlots;
   constexpr int kVecs = int(sizeof(Seg)) / 16;
   static_assert(kVecs > 64 && kVecs <= 128, "a descriptor is two copy instructions");
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[decode_smem_bytes<D>()];
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[decode_smem_bytes<D, V>()];
   if constexpr (W) {
     if (int(blockIdx.x) < a.num_wide) {
       // A wide prefix block: 128 decode columns against one piece of their
@@ -1066,9 +1310,13 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
   };
   for (int u = 0; u < NS - 1; ++u) issue_next(u);
 
-  WaveState<D, 1> ws;
+  std::conditional_t<V, ValuState<D>, WaveState<D, 1>> ws;
   reset_state(ws);
+  unsigned char* xchg = smem + NS * TG::stage_bytes + K * int(sizeof(Seg)) + wave * kValuXchgBytes;
   bf16x8 qf[1][KS];
+  u32x4 qrow[TG::chunks];  // vector-ALU engine: the lane's whole Q row
+  ValuOffsets<D> voffs;
+  if constexpr (V) valu_offsets<D>(voffs, lane);
   int lim[1] = {0};
   int orow = 0, k0 = 0, kend = 0, causal = 0, cnst = 0;
   bool has_cols = false, valid = false;
@@ -1113,22 +1361,42 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
           orow = sg.out[j] + (c & (a.group - 1));
           if (has_cols) {
             const unsigned char* qb = stage + wave * TG::page_bytes;
+            if constexpr (V) {
 #pragma unroll
-            for (int s = 0; s < KS; ++s)
-              qf[0][s] = *reinterpret_cast<const bf16x8*>(qb + 16 * (col * TG::chunks + 4 * s + grp));
+              for (int u = 0; u < TG::chunks; ++u)
+                qrow[u] = *reinterpret_cast<const u32x4*>(qb + 16 * (col * TG::chunks + u));
+            } else {
+#pragma unroll
+              for (int s = 0; s < KS; ++s)
+                qf[0][s] = *reinterpret_cast<const bf16x8*>(qb + 16 * (col * TG::chunks + 4 * s + grp));
+            }
           }
         } else {
           if (has_cols) {
-            attend_step<D, 1>(ws, stage, qf, lim, k0 + kStepKeys * k, kend, causal != 0, 1, lane, a.scale_log2);
+            if constexpr (V)
+              attend_step_valu<D>(ws, stage, qrow, voffs, lim[0], k0 + kStepKeys * k, kend, causal != 0, lane,
+                                  a.scale_log2, xchg);
+            else
+              attend_step<D, 1>(ws, stage, qf, lim, k0 + kStepKeys * k, kend, causal != 0, 1, lane, a.scale_log2);
             if (k == cnst - 1) {
               // The piece's state goes out as it stands: accumulators in their
               // register order (group, block, element), (m, l) once per column.
-              const float l = ws.lv[0][0];  // the whole column sum in the group-0 lanes
+              float l, m;
+              f32x4 acc[CH];
+              if constexpr (V) {
+                valu_finish<D>(ws, xchg, lane, acc, l);
+                m = ws.m;
+              } else {
+                l = ws.lv[0][0];  // the whole column sum in the group-0 lanes
+                m = ws.m[0];
+#pragma unroll
+                for (int jj = 0; jj < CH; ++jj) acc[jj] = ws.acc[0][jj];
+              }
               if (valid) {
                 float* out = a.plan.o_part + size_t(orow) * D + grp * (4 * CH);
 #pragma unroll
-                for (int jj = 0; jj < CH; ++jj) *reinterpret_cast<f32x4*>(out + 4 * jj) = ws.acc[0][jj];
-                if (grp == 0) *reinterpret_cast<f32x2*>(a.plan.l_part + 2 * size_t(orow)) = f32x2{ws.m[0], l};
+                for (int jj = 0; jj < CH; ++jj) *reinterpret_cast<f32x4*>(out + 4 * jj) = acc[jj];
+                if (grp == 0) *reinterpret_cast<f32x2*>(a.plan.l_part + 2 * size_t(orow)) = f32x2{m, l};
               }
               reset_state(ws);
             }
@@ -1308,12 +1576,15 @@ static void launch_all(AttnArgs a, const pfx_plan* p, hipStream_t s) {
   if (p->num_segs > 0 || p->num_wide > 0) {
     const int S = std::min<int>(a.num_workers, p->num_segs);
     const dim3 grid(p->num_wide + S);
-    if (a.fuse_append) {
-      if (p->num_wide) hipLaunchKernelGGL((decode_kernel<D, true, true>), grid, dim3(256), 0, s, a);
-      else hipLaunchKernelGGL((decode_kernel<D, true, false>), grid, dim3(256), 0, s, a);
+    if (p->decode_engine == PFX_DECODE_VALU) {
+      if (a.fuse_append) hipLaunchKernelGGL((decode_kernel<D, true, false, true>), grid, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((decode_kernel<D, false, false, true>), grid, dim3(256), 0, s, a);
+    } else if (a.fuse_append) {
+      if (p->num_wide) hipLaunchKernelGGL((decode_kernel<D, true, true, false>), grid, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((decode_kernel<D, true, false, false>), grid, dim3(256), 0, s, a);
     } else {
-      if (p->num_wide) hipLaunchKernelGGL((decode_kernel<D, false, true>), grid, dim3(256), 0, s, a);
-      else hipLaunchKernelGGL((decode_kernel<D, false, false>), grid, dim3(256), 0, s, a);
+      if (p->num_wide) hipLaunchKernelGGL((decode_kernel<D, false, true, false>), grid, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((decode_kernel<D, false, false, false>), grid, dim3(256), 0, s, a);
     }
   }
   const int n_tok = static_cast<int>(p->merge_tok.size());

@@ -175,15 +175,19 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
     return fail(PFX_EUNSUPPORTED, "pfx_plan_create: query group %d (1, 2, 4, 8 or 16 supported)", G);
   if (mode != PFX_MODE_EXTEND && mode != PFX_MODE_DECODE && mode != PFX_MODE_MIXED)
     return fail(PFX_EINVAL, "pfx_plan_create: mode %d", mode);
-  int32_t p_workers = 0, piece_steps = 0;
+  int32_t p_workers = 0, piece_steps = 0, engine = PFX_DECODE_MFMA;
   if (opts) {
-    for (int i = 0; i < 6; ++i)
+    for (int i = 0; i < 5; ++i)
       if (opts->reserved[i]) return fail(PFX_EINVAL, "pfx_plan_create: opts.reserved[%d] != 0", i);
     if (opts->decode_workers < 0 || opts->decode_workers > (1 << 20))
       return fail(PFX_EINVAL, "pfx_plan_create: decode_workers %d outside [0, %d]", opts->decode_workers, 1 << 20);
     if (opts->piece_steps < 0 || opts->piece_steps > kPieceSteps)
       return fail(PFX_EINVAL, "pfx_plan_create: piece_steps %d outside [0, %d]", opts->piece_steps, kPieceSteps);
+    if (opts->decode_engine != PFX_DECODE_MFMA && opts->decode_engine != PFX_DECODE_VALU)
+      return fail(PFX_EINVAL, "pfx_plan_create: decode_engine %d is neither PFX_DECODE_MFMA nor PFX_DECODE_VALU",
+                  opts->decode_engine);
     p_workers = opts->decode_workers;
+    engine = opts->decode_engine;
     if (opts->piece_steps) piece_steps = opts->piece_steps;
   }
   if (int64_t(pool->num_pages) * hkv > INT32_MAX)
@@ -273,6 +277,7 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   p->group = G;
   p->mode = mode;
   p->decode_workers = p_workers;
+  p->decode_engine = engine;
   p->num_reqs = R;
   p->num_tokens = static_cast<int32_t>(total_tokens);
   p->pages_needed = static_cast<int32_t>(need);
@@ -332,7 +337,7 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
     // An agent with more decode columns per KV head than one 64-column
     // piece holds reads each prefix step for up to 128 columns at once
     // (wide blocks): half the stages, each with twice the products.
-    const int32_t wide = agent_cols > kDecodeTileCols;
+    const int32_t wide = engine == PFX_DECODE_MFMA && agent_cols > kDecodeTileCols;
     const int32_t block_cols = wide ? kExtendTileCols : kDecodeTileCols;
     size_t i = 0;
     while (i < members.size()) {

@@ -34,7 +34,7 @@ class DeviceStep:
     """
 
     def __init__(self, batch: Batch, hv: HostValues, device="cuda", mode=B.PFX_MODE_MIXED,
-                 host_resident=(), decode_workers=0, piece_steps=0, poison=True):
+                 host_resident=(), decode_workers=0, piece_steps=0, poison=True, decode_engine=B.PFX_DECODE_MFMA):
         self.batch = batch
         self.device = device
         n, hkv, d = batch.num_pages, batch.num_kv_heads, batch.head_dim
@@ -71,7 +71,7 @@ class DeviceStep:
         self.lse = torch.empty((t, batch.num_q_heads), dtype=torch.float32, device=device)
         self.pool = B.make_pool(n, hkv, d, self.k_pool, self.v_pool)
         self.plan = B.plan_from_batch(self.pool, batch, mode, decode_workers=decode_workers,
-                                      piece_steps=piece_steps).upload(device=device)
+                                      piece_steps=piece_steps, decode_engine=decode_engine).upload(device=device)
 
     def _write_pages(self, pages, kp, vp, chunk=4096):
         for s in range(0, len(pages), chunk):

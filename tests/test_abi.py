@@ -35,7 +35,7 @@ def test_library_exports_every_declared_function():
 
 
 def test_version_and_error_text():
-    assert B.pfx_version() == 20100
+    assert B.pfx_version() == 20200
     with pytest.raises(B.PfxError):
         B.Allocator(-1)
     assert "num_pages" in B.pfx_last_error()
@@ -274,15 +274,17 @@ def enumerate_coverage(plan, batch):
     return counts, outs
 
 
-@pytest.mark.parametrize("case", ["small", "split", "g1", "g2", "g16", "decode_only", "wide"])
+@pytest.mark.parametrize("case", ["small", "split", "g1", "g2", "g16", "decode_only", "wide", "wide-valu"])
 def test_plan_covers_every_visible_key_once(case):
-    if case == "wide":
+    if case in ("wide", "wide-valu"):
         # agents with 70, 200 and 24 decode columns per KV head (G = 2): wide blocks for the first two
         reqs = [(0, 5 + i, 1) for i in range(35)] + [(1, 3 + i % 50, 1) for i in range(96)] + \
                [(1, 20, 2), (2, 9, 3)] + [(2, 4 + i, 1) for i in range(9)] + [(0, 300, 300), (-1, 30, 1)]
         b = W.make_batch(9, num_q_heads=16, num_kv_heads=8, head_dim=64, num_pages=4096, prefix_len=[400, 1000, 90],
                          agent=[r[0] for r in reqs], suffix_len=[r[1] for r in reqs], n_rows=[r[2] for r in reqs])
         kw = dict(piece_steps=5)
+        if case == "wide-valu":
+            kw["decode_engine"] = B.PFX_DECODE_VALU  # the same agents in 64-column pieces, no wide blocks
     elif case == "g2":
         reqs = [(0, 140, 140), (0, 19, 3), (0, 5, 1), (0, 44, 8), (-1, 9, 9)] + [(1, 3 + i, 1) for i in range(40)]
         b = W.make_batch(8, num_q_heads=16, num_kv_heads=8, head_dim=64, num_pages=256, prefix_len=[70, 33],
@@ -302,6 +304,8 @@ def test_plan_covers_every_visible_key_once(case):
                          agent=agents, suffix_len=(np.arange(70) % 40) + 1, n_rows=np.ones(70, np.int32))
         kw = dict(decode_workers=64)
     p = plan_for(b, **kw)
+    if case.startswith("wide"):
+        assert (p.stats().num_wide_blocks > 0) == (case == "wide")
     counts, outs = enumerate_coverage(p, b)
     q_indptr = b.q_indptr()
     expected = 0
@@ -498,6 +502,16 @@ def test_default_piece_length_follows_the_launch_size():
     assert int(p.export(3)[:, 3].max()) == 16
     with pytest.raises(B.PfxError):
         plan_for(W.config_batch(2), piece_steps=65)
+
+
+def test_decode_engine_option():
+    b = W.config_batch(4)       # agents with more than 64 decode columns per KV head
+    assert plan_for(b).stats().num_wide_blocks > 0
+    pv = plan_for(b, decode_engine=B.PFX_DECODE_VALU)
+    assert pv.stats().num_wide_blocks == 0
+    for bad in (2, -1):
+        msg = expect_error(B.PFX_EINVAL, lambda: plan_for(b, decode_engine=bad))
+        assert "decode_engine" in msg
 
 
 

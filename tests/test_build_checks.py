@@ -43,8 +43,9 @@ def test_no_packed_fp32(isa):
 def test_no_scratch_in_attention_kernels(isa):
     kernels = re.findall(r"^(_ZN3pfx\w*(?:decode|extend|merge_rows)_kernel\w*):", isa, flags=re.M)
     # extend; decode with and without the folded-in append and the wide
-    # prefix blocks; merge with and without the append; head dims 64 and 128
-    assert len(kernels) == 14
+    # prefix blocks, and on the vector ALU with and without the append; merge
+    # with and without the append; head dims 64 and 128
+    assert len(kernels) == 18
     for kernel in kernels:
         body = isa.split(kernel + ":", 1)[1].split("s_endpgm", 1)[0]
         assert "scratch_" not in body, kernel

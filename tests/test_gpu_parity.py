@@ -177,6 +177,18 @@ def test_small_batches(case):
     run_and_check(b, hv, f"small{seed}", **opts)
 
 
+@pytest.mark.parametrize("case", SMALL_CASES, ids=[f"valu-small{c[0]}" for c in SMALL_CASES])
+def test_small_batches_valu_engine(case):
+    """The decode pieces on the vector ALU (dot products instead of MFMA
+    tiles, no wide blocks) against the same oracle."""
+    seed, hq, hkv, d, plen, reqs, opts = case
+    b = W.make_batch(seed, num_q_heads=hq, num_kv_heads=hkv, head_dim=d, num_pages=256, prefix_len=plen,
+                     agent=[r[0] for r in reqs], suffix_len=[r[1] for r in reqs], n_rows=[r[2] for r in reqs])
+    hv = W.host_values(b, seed + 50)
+    ds, _, _ = run_and_check(b, hv, f"valu-small{seed}", decode_engine=B.PFX_DECODE_VALU, **opts)
+    assert ds.plan.stats().num_wide_blocks == 0
+
+
 def small_batch(case):
     seed, hq, hkv, d, plen, reqs, opts = case
     need = sum((p + 15) // 16 for p in plen) + sum((r[1] + 15) // 16 for r in reqs)
@@ -227,6 +239,18 @@ def test_peaked_rising_scores(case):
     hv = W.host_values_shaped(b, seed + 3, key_gain=lambda p: 1.0 + p / 256.0, q_gain=4.0, v_gain=0.25)
     run_and_check(b, hv, f"rising{seed}", **opts)
     run_and_check(b, hv, f"rising{seed}-scale", sm_scale=0.25, **opts)
+
+
+@pytest.mark.parametrize("case", PEAKED, ids=[f"valu-peaked{c[0]}" for c in PEAKED])
+def test_peaked_valu_engine(case):
+    """The vector-ALU decode engine under a one-hot row and rising scores:
+    its rescale exchanges every column's factor through LDS."""
+    seed, hq, hkv, d, plen, reqs, opts = case
+    b, _ = small_batch((seed, hq, hkv, d, plen, reqs, opts))
+    hv = W.plant_one_hot(b, W.host_values(b, seed + 1), seed + 2, alpha_log2=4)
+    run_and_check(b, hv, f"valu-one-hot{seed}", decode_engine=B.PFX_DECODE_VALU, **opts)
+    hv = W.host_values_shaped(b, seed + 3, key_gain=lambda p: 1.0 + p / 256.0, q_gain=4.0, v_gain=0.25)
+    run_and_check(b, hv, f"valu-rising{seed}", decode_engine=B.PFX_DECODE_VALU, **opts)
 
 
 def test_graph_replay_matches_eager():
@@ -345,6 +369,24 @@ def test_config2_decode_deterministic_and_placement_invariant():
     B.pfx_sync_check()
     o3, l3 = ds2.outputs()
     assert np.array_equal(o1, o3) and np.array_equal(l1, l3), "placement changed the result bits"
+
+
+def test_config2_valu_engine_every_row():
+    """Decode-8B with the decode pieces on the vector ALU: every row against
+    the oracle, and within the oracle tolerance of the MFMA engine."""
+    b = W.config_batch(2)
+    hv = W.host_values_fast(b, 2002)
+    ds, o_v, l_v = run_and_check(b, hv, "config2-valu", decode_engine=B.PFX_DECODE_VALU)
+    del ds
+    announce("config2 on the MFMA engine, for the engine-to-engine difference")
+    ds = RN.DeviceStep(b, hv)
+    ds.step()
+    B.pfx_sync_check()
+    o_m, l_m = ds.outputs()
+    diff = float(np.abs(oracle.bf16_bits_to_f64(o_v) - oracle.bf16_bits_to_f64(o_m)).max())
+    announce(f"config2 engines: max |O_valu - O_mfma| = {diff:.2e}")
+    assert diff <= PT.MAX_ABS, "the two engines differ by more than the oracle tolerance"
+    assert float(np.abs(l_v - l_m).max()) <= PT.LSE_ABS
 
 
 def sample_rows(batch, rng, per=16):
@@ -508,6 +550,11 @@ STEP_CASES = [
                                                 prefix_len=[130], agent=[0, 0, -1, 0],
                                                 suffix_len=[35, 8, 64, 100], n_rows=[8, 3, 8, 1]), {}),
     ("decode-8B", lambda: W.config_batch(2), {}),
+    ("decode-multirow-g1-valu", lambda: W.make_batch(41, num_q_heads=8, num_kv_heads=8, head_dim=64, num_pages=512,
+                                                     prefix_len=[300, 45], agent=[0, 1, 0, -1, 1, 0],
+                                                     suffix_len=[40, 16, 33, 20, 1, 70], n_rows=[16, 16, 1, 9, 1, 13]),
+     dict(piece_steps=1, decode_engine=B.PFX_DECODE_VALU)),
+    ("decode-8B-valu", lambda: W.config_batch(2), dict(decode_engine=B.PFX_DECODE_VALU)),
 ]
 
 
