@@ -344,6 +344,78 @@ def cpu_baseline_extend(res, W, seconds=12.0, rows_per_call=64):
                       f"fp64 numpy oracle, BLAS threads {threads}"}
 
 
+def cpu_baseline_config5(torch, b, pool_k, pool_v, q, kind, u_layer, f_layer, layers, seconds=8.0, block=16):
+    """The fp64 oracle on a bounded sample of one mixed-70B layer (layer 0's
+    pool), the rest extrapolated: decode requests whole (all 64 heads), or
+    extend blocks of ``block`` consecutive rows of one request (all heads),
+    requests in turn.  Each sample is handed to the oracle as a one-request
+    batch holding only its own pages (read back from the device beforehand,
+    outside the timing; an extend block is its request truncated after the
+    block's last row, which leaves every row's visible keys unchanged).
+    Decode is scored in unique KV bytes per second (each request's suffix
+    plus its share of its agent's prefix) and extrapolated to the 80 layers'
+    unique bytes; extend in causal-exact flop per second, extrapolated to the
+    80 layers' flops."""
+    import numpy as np
+
+    import oracle
+
+    hq, hkv, d = b.num_q_heads, b.num_kv_heads, b.head_dim
+    q_indptr = b.q_indptr()
+    reqs = [r for r in range(len(b.agent)) if int(b.n_rows[r]) > 0]
+    per_agent = {int(a): sum(1 for r in reqs if int(b.agent[r]) == a) for a in set(int(b.agent[r]) for r in reqs)}
+    rng = np.random.default_rng(5005)
+
+    def host_pages(pages):
+        idx = torch.from_numpy(np.asarray(pages, np.int64)).to(pool_k.device)
+        k = pool_k.view(torch.int16).index_select(0, idx).cpu().numpy().view(np.uint16)
+        v = pool_v.view(torch.int16).index_select(0, idx).cpu().numpy().view(np.uint16)
+        return k, v
+
+    # Samples prepared up front: enough for the time budget, cycled if it runs out.
+    prefix_cache, samples = {}, []
+    for r in reqs[:: max(1, len(reqs) // 24)][:24]:
+        a, n, L = int(b.agent[r]), int(b.n_rows[r]), int(b.suffix_len[r])
+        P = int(b.prefix_len[a]) if a >= 0 else 0
+        if a >= 0 and a not in prefix_cache:
+            prefix_cache[a] = host_pages(b.prefix_pages[a])
+        i0 = 0 if kind == "decode" else int(rng.integers(0, max(1, n - block + 1)))
+        m = n if kind == "decode" else min(block, n - i0)
+        keep_len = L - n + i0 + m                      # the suffix up to the sample's last row
+        sk, sv = host_pages(b.suffix_pages[r][: (keep_len + 15) // 16])
+        pk, pv = prefix_cache[a] if a >= 0 else (sk[:0], sv[:0])
+        qs = q[int(q_indptr[r]) + i0: int(q_indptr[r]) + i0 + m].view(torch.int16).cpu().numpy().view(np.uint16)
+        work = ((L + P / per_agent[a] if a >= 0 else L) * hkv * d * 4 if kind == "decode"
+                else sum(4 * d * hq * (P + L - n + i0 + j + 1) for j in range(m)))
+        samples.append((np.concatenate([pk, sk]), np.concatenate([pv, sv]), len(pk), P, a >= 0, keep_len, m, qs,
+                        work))
+    t0 = time.perf_counter()
+    done, work, rows = 0, 0.0, 0
+    while time.perf_counter() - t0 < seconds:
+        kp, vp, npp, P, has, keep_len, m, qs, w = samples[done % len(samples)]
+        oracle.prefix_shared_attention(kp, vp, [np.arange(npp)], [P], [0 if has else -1],
+                                       [np.arange(npp, len(kp))], [keep_len], [m], qs, hq)
+        work += w
+        rows += m
+        done += 1
+    dt = time.perf_counter() - t0
+    threads = os.environ.get("OMP_NUM_THREADS", "unset")
+    rate = work / dt
+    rec = {"cores": len(os.sched_getaffinity(0)), "kind": "oracle"}
+    if kind == "decode":
+        rec.update(value=round(rate / 1e9, 4), unit="GB/s",
+                   extrapolated_s_80_layers=round(u_layer * layers / rate, 1),
+                   sample=f"{done} decode requests of layer 0 (all {hq} heads each) in {dt:.1f} s, fp64 numpy "
+                          f"oracle, BLAS threads {threads}; extrapolated by unique KV bytes")
+    else:
+        rec.update(value=round(rate / 1e12, 6), unit="TFLOP/s",
+                   extrapolated_s_80_layers=round(f_layer * layers / rate, 1),
+                   sample=f"{rows} extend rows of layer 0 (all {hq} heads each) in {done} blocks of up to {block} "
+                          f"consecutive rows, in {dt:.1f} s, fp64 numpy oracle, BLAS threads {threads}; "
+                          f"extrapolated by causal-exact flops")
+    return rec
+
+
 def copy_calibration(torch, B):
     """A plain device-to-device copy of known size through pfx_page_copy
     (used to scale the HBM byte counters read by rocprofv3)."""
@@ -410,7 +482,7 @@ def events_ms(fn, n, torch, warm=3):
     return e0.elapsed_time(e1) / n
 
 
-def bench_configs(torch, B, RN, W):
+def bench_configs(torch, B, RN, W, cpu=True):
     """The other three workloads, in the default run: the tiny config-1
     extend and decode (launch-bound, reported only), config 4 (the
     pinned-host gather of 4 evicted prefixes, then decode over all 16 agents
@@ -496,6 +568,8 @@ def bench_configs(torch, B, RN, W):
         elif name == "extend":
             tf = f5 * layers / (ms * 1e-3) / 1e12
             rec.update(TFLOPs=round(tf, 1), frac=round(tf / BF16_PEAK_TFLOPS, 4))
+        if cpu and name in ("decode", "extend"):
+            rec["cpu_baseline"] = cpu_baseline_config5(torch, bb, keep[0][0], keep[0][1], q, name, u5, f5, layers)
         else:
             bound = max(u5 / (HBM_PEAK_GBS * 1e9),
                         (f5 + dec_only.attention_flops()) / (BF16_PEAK_TFLOPS * 1e12)) * layers * 1e3
@@ -777,7 +851,7 @@ def main():
     configs = None
     if not args.no_configs:
         log("configs 1, 4, 5")
-        configs = bench_configs(torch, B, RN, W)
+        configs = bench_configs(torch, B, RN, W, cpu=not args.no_cpu)
         log(f"config4 decode {configs['config4']['decode_attn_us']} us; config5 "
             f"decode {configs['config5']['decode']['ms_80_layers']} ms, extend "
             f"{configs['config5']['extend']['ms_80_layers']} ms (80 layers)")
