@@ -446,6 +446,16 @@ def test_config4_gather_evicted_then_decode():
     run_and_check(b, hv, "config4", host_resident=evicted, parallel=True)
 
 
+def test_config4_valu_engine_every_row():
+    """Hetero-8B on the vector-ALU decode engine: the Zipf-skewed agents that
+    the MFMA engine runs as wide blocks go in 64-column pieces here; every row
+    against the oracle."""
+    b = W.config_batch(4)
+    hv = W.host_values_fast(b, 2004)
+    ds, _, _ = run_and_check(b, hv, "config4-valu", parallel=True, decode_engine=B.PFX_DECODE_VALU)
+    assert ds.plan.stats().num_wide_blocks == 0
+
+
 @pytest.mark.timeout(900)
 def test_config5_80_layers_every_layer():
     """70B-like mixed batch over 80 layers with independent pools (device-drawn
