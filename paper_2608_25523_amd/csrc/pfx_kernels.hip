@@ -1123,16 +1123,21 @@ __global__ __launch_bounds__(256, 2) void extend_kernel(AttnArgs a) {
 // workgroup b piece r S + b on even rounds and r S + S - 1 - b on odd ones.
 // Every piece contributes a Q stage (its query rows, each wave's 16
 // columns in its quarter of the stage) and then its K/V steps, and stage u
-// is refilled with stage u + kStages - 1 whatever piece that belongs to, so
+// is refilled with stage u + kDecodeStages - 1 whatever piece that belongs to, so
 // a piece boundary does not drain the ring.  A piece's descriptor (header, rows, page blocks)
 // comes into one of kPieceSlots LDS slots by a direct copy that wave 0
 // issues with the Q stage two pieces earlier; it is complete once that stage
 // has been waited for, long before the issue reaches the piece.
 // ---------------------------------------------------------------------------
+// The decode ring has three stages (two in flight while one is consumed):
+// a decode step is short, and a fourth stage measured 1-2% slower (decode
+// steps queued behind the others' requests rather than adding bandwidth).
+constexpr int kDecodeStages = 3;
+
 // V: the decode pieces run on the vector ALU, with a per-wave exchange area.
 template <int D, bool V>
 constexpr int decode_smem_bytes() {
-  return kStages * TileGeom<D>::stage_bytes + kPieceSlots * int(sizeof(Seg)) + (V ? 4 * kValuXchgBytes : 0);
+  return kDecodeStages * TileGeom<D>::stage_bytes + kPieceSlots * int(sizeof(Seg)) + (V ? 4 * kValuXchgBytes : 0);
 }
 
 // Piece of workgroup b at position n of its list (>= num_pieces: none).
@@ -1214,11 +1219,13 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
   using TG = TileGeom<D>;
   constexpr int KS = D / 32;
   constexpr int CH = D / 16;
-  constexpr int NS = kStages;
+  constexpr int NS = kDecodeStages;
   constexpr int K = kPieceSlots;
   constexpr int kVecs = int(sizeof(Seg)) / 16;
   static_assert(kVecs > 64 && kVecs <= 128, "a descriptor is two copy instructions");
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[decode_smem_bytes<D, V>()];
+  // Wide prefix blocks run the extend block's four-stage ring in the same bytes.
+  constexpr int kSmem = W ? std::max(extend_smem_bytes<D>(), decode_smem_bytes<D, V>()) : decode_smem_bytes<D, V>();
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[kSmem];
   if constexpr (W) {
     if (int(blockIdx.x) < a.num_wide) {
       // A wide prefix block: 128 decode columns against one piece of their
