@@ -812,6 +812,8 @@ def main():
     ap.add_argument("--no-configs", action="store_true", help="skip configs 1, 4 and 5 (about a minute)")
     ap.add_argument("--more", action="store_true",
                     help="also time prefix movement, the rebuild of a preempted request and the service tables")
+    ap.add_argument("--no-engines", action="store_true",
+                    help="skip the prefix-phase comparison of the two decode engines (counter passes over the rest)")
     ap.add_argument("--engines-only", action="store_true",
                     help="only the prefix-phase comparison of the two decode engines (for counter passes)")
     ap.add_argument("--calib-copy", action="store_true",
@@ -845,9 +847,11 @@ def main():
         ext = bench_extend(args, torch, B, RN, W)
         log(f"extend-8B: {ext['ms']:.3f} ms/step, attention {ext['attn_ms']:.3f} ms, "
             f"append {ext['append_ms']:.3f} ms")
-    log("decode-8B prefix phase on both decode engines")
-    engines = bench_prefix_engines(args, torch, B, RN, W)
-    log(f"prefix phase: MFMA {engines['mfma']['attn_us']} us, VALU {engines['valu']['attn_us']} us")
+    engines = None
+    if not args.no_engines:
+        log("decode-8B prefix phase on both decode engines")
+        engines = bench_prefix_engines(args, torch, B, RN, W)
+        log(f"prefix phase: MFMA {engines['mfma']['attn_us']} us, VALU {engines['valu']['attn_us']} us")
     configs = None
     if not args.no_configs:
         log("configs 1, 4, 5")
