@@ -12,7 +12,9 @@
 // V^T is read from the LDS stage with ds_read_b64_tr_b16, which hands each
 // lane 4 keys of one head dim out of a key-major tile.
 //
-// Three launches per call, in stream order:
+// Up to three launches per call, in stream order (a batch with both extend
+// blocks and decode pieces runs the first two as one launch, the extend
+// blocks leading its grid):
 //   extend blocks: one workgroup per block of <= 128 query columns of one
 //     request and one KV head, streaming the prefix and the causal suffix
 //     through an LDS ring; rows written directly.
@@ -1577,22 +1579,39 @@ static int check_pool_matches(const pfx_pool* pool, const pfx_plan* p, const cha
   return PFX_OK;
 }
 
+// The decode launch alone: wide prefix blocks (if any) and the pieces.
+template <int D>
+static void launch_decode(const AttnArgs& a, const pfx_plan* p, hipStream_t s) {
+  const int S = std::min<int>(a.num_workers, p->num_segs);
+  const dim3 grid(p->num_wide + S);
+  if (p->decode_engine == PFX_DECODE_VALU) {
+    if (a.fuse_append) hipLaunchKernelGGL((decode_kernel<D, true, false, true>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((decode_kernel<D, false, false, true>), grid, dim3(256), 0, s, a);
+  } else if (a.fuse_append) {
+    if (p->num_wide) hipLaunchKernelGGL((decode_kernel<D, true, true, false>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((decode_kernel<D, true, false, false>), grid, dim3(256), 0, s, a);
+  } else {
+    if (p->num_wide) hipLaunchKernelGGL((decode_kernel<D, false, true, false>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((decode_kernel<D, false, false, false>), grid, dim3(256), 0, s, a);
+  }
+}
+
 template <int D>
 static void launch_all(AttnArgs a, const pfx_plan* p, hipStream_t s) {
-  if (p->num_items > 0) hipLaunchKernelGGL((extend_kernel<D>), dim3(p->num_items), dim3(256), 0, s, a);
-  if (p->num_segs > 0 || p->num_wide > 0) {
+  if (p->num_items > 0 && p->num_segs > 0 && p->decode_engine == PFX_DECODE_MFMA && !a.fuse_append) {
+    // A mixed batch in one launch: the extend blocks and the wide prefix
+    // blocks lead the grid (the same block routine as the extend launch, at
+    // the same block indices, so their XCD grouping holds), and the decode
+    // pieces follow, taking compute units as the extend blocks retire
+    // instead of waiting for the last of them.
+    AttnArgs m = a;
+    m.num_wide = p->num_items + p->num_wide;
+    m.wide_first = 0;
     const int S = std::min<int>(a.num_workers, p->num_segs);
-    const dim3 grid(p->num_wide + S);
-    if (p->decode_engine == PFX_DECODE_VALU) {
-      if (a.fuse_append) hipLaunchKernelGGL((decode_kernel<D, true, false, true>), grid, dim3(256), 0, s, a);
-      else hipLaunchKernelGGL((decode_kernel<D, false, false, true>), grid, dim3(256), 0, s, a);
-    } else if (a.fuse_append) {
-      if (p->num_wide) hipLaunchKernelGGL((decode_kernel<D, true, true, false>), grid, dim3(256), 0, s, a);
-      else hipLaunchKernelGGL((decode_kernel<D, true, false, false>), grid, dim3(256), 0, s, a);
-    } else {
-      if (p->num_wide) hipLaunchKernelGGL((decode_kernel<D, false, true, false>), grid, dim3(256), 0, s, a);
-      else hipLaunchKernelGGL((decode_kernel<D, false, false, false>), grid, dim3(256), 0, s, a);
-    }
+    hipLaunchKernelGGL((decode_kernel<D, false, true, false>), dim3(m.num_wide + S), dim3(256), 0, s, m);
+  } else {
+    if (p->num_items > 0) hipLaunchKernelGGL((extend_kernel<D>), dim3(p->num_items), dim3(256), 0, s, a);
+    if (p->num_segs > 0 || p->num_wide > 0) launch_decode<D>(a, p, s);
   }
   const int n_tok = static_cast<int>(p->merge_tok.size());
   if (n_tok) {
