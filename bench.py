@@ -19,7 +19,8 @@ working set exceeds the 256 MB last-level cache.
 U[256, 2048] prefilled against their agent's prefix; TFLOP/s over the
 causal-exact flop count.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-extend] [--no-configs] [--more]
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-extend] [--no-configs] [--no-engines]
+                       [--no-extras] [--engines-only] [--calib-copy]
 """
 
 from __future__ import annotations
@@ -583,7 +584,7 @@ def bench_configs(torch, B, RN, W, cpu=True):
 
 
 def bench_extras(torch, B, RN, W):
-    """Timed on request (--more): prefix movement, the rebuild of a
+    """Timed in the default run (skipped with --no-extras): prefix movement, the rebuild of a
     preempted request and the service-time tables."""
     res = {}
     res["movement"] = bench_movement(torch, B, RN, W)
@@ -810,8 +811,9 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-extend", action="store_true")
     ap.add_argument("--no-configs", action="store_true", help="skip configs 1, 4 and 5 (about a minute)")
-    ap.add_argument("--more", action="store_true",
-                    help="also time prefix movement, the rebuild of a preempted request and the service tables")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip prefix movement, the rebuild of a preempted request and the service tables")
+    ap.add_argument("--more", action="store_true", help="accepted for older command lines; the extras run by default")
     ap.add_argument("--no-engines", action="store_true",
                     help="skip the prefix-phase comparison of the two decode engines (counter passes over the rest)")
     ap.add_argument("--engines-only", action="store_true",
@@ -860,7 +862,7 @@ def main():
             f"decode {configs['config5']['decode']['ms_80_layers']} ms, extend "
             f"{configs['config5']['extend']['ms_80_layers']} ms (80 layers)")
     extras = None
-    if args.more:
+    if not args.no_extras:
         log("movement, rebuild, service tables")
         extras = bench_extras(torch, B, RN, W)
     cpu = cpu_ext = None
