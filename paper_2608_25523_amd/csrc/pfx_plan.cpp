@@ -599,8 +599,28 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   // The host image: the last destroyed plan's buffer is reused when it is
   // large enough (a serving loop builds a plan every step, and fresh pages
   // of a few hundred KiB cost more to fault in than to fill).
+  // Every byte of the image is written once: each section by its copy or
+  // its records below, the alignment gaps after the sections here (the
+  // reused buffer may still hold the last plan's bytes).
   p->blob.swap(spare_blob());
-  p->blob.assign(p->blob_bytes, 0);
+  p->blob.resize(p->blob_bytes);
+  {
+    const size_t sect[][2] = {
+        {p->off_items, (nitems + wide_order.size()) * sizeof(Item)},
+        {p->off_row_tok, p->row_tok.size() * 4},
+        {p->off_row_out, p->row_out.size() * 4},
+        {p->off_page_list, p->page_list.size() * 4},
+        {p->off_tok_slot, p->tok_slot.size() * 4},
+        {p->off_segs, nsegs * sizeof(Seg)},
+        {p->off_merge_tok, p->merge_tok.size() * 4},
+        {p->off_merge_head, p->merge_head.size() * sizeof(MergeHead)},
+    };
+    const size_t ns = sizeof(sect) / sizeof(sect[0]);
+    for (size_t i = 0; i < ns; ++i) {
+      const size_t end = sect[i][0] + sect[i][1], next = i + 1 < ns ? sect[i + 1][0] : p->blob_bytes;
+      if (next > end) std::memset(p->blob.data() + end, 0, next - end);
+    }
+  }
   auto put = [&](size_t at, const void* src, size_t bytes) {
     if (bytes) std::memcpy(p->blob.data() + at, src, bytes);
   };
