@@ -97,10 +97,12 @@ static_assert(sizeof(Seg) == 1088, "Seg is 272 int32");
 
 // Partial results of one (decode token, KV head): nparts slots of G rows at
 // o_part/l_part rows (base + slot) * G + g.  A partial row holds a piece's
-// unnormalised state: o_part the D accumulators sum_k p_k v_k in the order
-// the MFMA layout leaves them in (lane group grp, then block blk, then
-// element i: dim 16 blk + 4 grp + i), l_part the pair (m, l) of the
-// running maximum (log2 units, scaled) and the sum of 2^(s - m).
+// unnormalised state: in o_part the D accumulators sum_k p_k v_k, in l_part
+// the pair (m, l) of the running maximum (log2 units, scaled) and the sum of
+// 2^(s - m).  The D * G floats of a slot's rows hold 16-byte chunks in
+// chunk-major order: chunk c = 4 blk + grp of row g (dims 16 blk + 4 grp
+// .. + 3, one f32x4 of the MFMA accumulator layout) at float (c G + g) 4,
+// so that a wave stores each token's G rows as one contiguous run.
 struct MergeHead {
   int32_t base;
   int32_t nparts;

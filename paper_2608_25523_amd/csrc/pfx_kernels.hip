@@ -62,6 +62,23 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// A partial state's D accumulators in the plan's workspace.  The G rows of
+// one slot (one decode token against the G query heads of a KV head: rows
+// r0 .. r0 + G - 1, r0 a multiple of G) fill the G * D floats from float
+// r0 * D as 16-byte chunks, chunk-major: chunk c = 4 blk + grp of row g
+// (dims 16 blk + 4 grp .. + 3, one f32x4 of the MFMA accumulator layout)
+// at float (c * G + g) * 4.  A wave's store of one chunk then covers each
+// token's G rows as one run of 64 G bytes, not 4 G pieces of 16 bytes
+// strewn over as many cache lines.  The stores are non-temporal: whole
+// lines that the merge launch reads once, not kept dirty in the L2 of the
+// XCD that wrote them until the end of the launch.
+// Chunk grp of row `row` (query head g of its token); chunk c = 4 blk + grp
+// is at that pointer + part_chunk_stride(G) * blk.
+__device__ __forceinline__ float* part_chunk0(float* o_part, size_t row, int g, int G, int grp, int D) {
+  return o_part + (row - size_t(g)) * D + size_t(grp * G + g) * 4;
+}
+__device__ __forceinline__ int part_chunk_stride(int G) { return 16 * G; }
+
 // Placed inside a rarely taken branch (masking, rescaling): the compiler may
 // not turn the branch into always-executed selects.
 #define PFX_KEEP_BRANCH() asm volatile("" ::: "memory")
@@ -1101,10 +1118,11 @@ __device__ __forceinline__ void extend_block(const AttnArgs& a, const Item* itp,
       write_rows<D>(a, ws.acc[b], ws.m[b], ws.lv[b][0], orow[b], valid, grp);
     } else if (valid) {
       // A wide prefix block's state, as a decode piece leaves it:
-      // accumulators in register order, (m, l) once per column.
-      float* out = a.plan.o_part + size_t(prow[b]) * D + grp * (4 * (D / 16));
+      // accumulator chunks in the partial layout, (m, l) once per column.
+      float* out = part_chunk0(a.plan.o_part, size_t(prow[b]), c & (G - 1), G, grp, D);
 #pragma unroll
-      for (int jj = 0; jj < D / 16; ++jj) *reinterpret_cast<f32x4*>(out + 4 * jj) = ws.acc[b][jj];
+      for (int jj = 0; jj < D / 16; ++jj)
+        __builtin_nontemporal_store(ws.acc[b][jj], reinterpret_cast<f32x4*>(out + part_chunk_stride(G) * jj));
       if (grp == 0) *reinterpret_cast<f32x2*>(a.plan.l_part + 2 * size_t(prow[b])) = f32x2{ws.m[b], ws.lv[b][0]};
     }
   }
@@ -1388,8 +1406,9 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
             else
               attend_step<D, 1>(ws, stage, qf, lim, k0 + kStepKeys * k, kend, causal != 0, 1, lane, a.scale_log2);
             if (k == cnst - 1) {
-              // The piece's state goes out as it stands: accumulators in their
-              // register order (group, block, element), (m, l) once per column.
+              // The piece's state goes out as it stands: each f32x4 of the
+              // accumulators as one chunk of the partial layout, (m, l) once
+              // per column.
               float l, m;
               f32x4 acc[CH];
               if constexpr (V) {
@@ -1402,9 +1421,11 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
                 for (int jj = 0; jj < CH; ++jj) acc[jj] = ws.acc[0][jj];
               }
               if (valid) {
-                float* out = a.plan.o_part + size_t(orow) * D + grp * (4 * CH);
+                float* out =
+                    part_chunk0(a.plan.o_part, size_t(orow), (16 * wave + col) & (a.group - 1), a.group, grp, D);
 #pragma unroll
-                for (int jj = 0; jj < CH; ++jj) *reinterpret_cast<f32x4*>(out + 4 * jj) = acc[jj];
+                for (int jj = 0; jj < CH; ++jj)
+                  __builtin_nontemporal_store(acc[jj], reinterpret_cast<f32x4*>(out + part_chunk_stride(a.group) * jj));
                 if (grp == 0) *reinterpret_cast<f32x2*>(a.plan.l_part + 2 * size_t(orow)) = f32x2{m, l};
               }
               reset_state(ws);
@@ -1465,7 +1486,10 @@ __global__ __launch_bounds__(256) void merge_rows_kernel(AttnArgs a, int n_tok) 
   const int tok = a.plan.merge_tok[m];
   const size_t row0 = size_t(mh.base) * a.group + (qh & (a.group - 1));
   const size_t stride = size_t(a.group);  // rows between slots
-  const float* op = a.plan.o_part + row0 * D + grp * (4 * CH) + 4 * blk;
+  // Chunks 4 blk + grp and 4 (blk + 1) + grp of the row in slot 0.
+  const float* op =
+      part_chunk0(a.plan.o_part, row0, qh & (a.group - 1), a.group, grp, D) + part_chunk_stride(a.group) * blk;
+  const int op1 = part_chunk_stride(a.group);
   const f32x2* lp = reinterpret_cast<const f32x2*>(a.plan.l_part) + row0;
   f32x2 ml[kMergeBatch];
   f32x4 ov[kMergeBatch][2];
@@ -1474,7 +1498,7 @@ __global__ __launch_bounds__(256) void merge_rows_kernel(AttnArgs a, int n_tok) 
     if (k < mh.nparts) {
       ml[k] = lp[k * stride];
       ov[k][0] = *reinterpret_cast<const f32x4*>(op + k * stride * D);
-      ov[k][1] = *reinterpret_cast<const f32x4*>(op + k * stride * D + 4);
+      ov[k][1] = *reinterpret_cast<const f32x4*>(op + k * stride * D + op1);
     } else {
       ml[k] = f32x2{kNegBig, 0.f};
       ov[k][0] = ov[k][1] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -1498,7 +1522,7 @@ __global__ __launch_bounds__(256) void merge_rows_kernel(AttnArgs a, int n_tok) 
     const float w = fast_exp2(x[0] - mx);
     z += w * x[1];
     acc0 += w * *reinterpret_cast<const f32x4*>(op + k * stride * D);
-    acc1 += w * *reinterpret_cast<const f32x4*>(op + k * stride * D + 4);
+    acc1 += w * *reinterpret_cast<const f32x4*>(op + k * stride * D + op1);
   }
   const float inv = 1.0f / z;
   uint16_t* out = a.o + (size_t(tok) * a.hq + qh) * D + 16 * blk + 4 * grp;
