@@ -97,12 +97,13 @@ static_assert(sizeof(Seg) == 1088, "Seg is 272 int32");
 
 // Partial results of one (decode token, KV head): nparts slots of G rows at
 // o_part/l_part rows (base + slot) * G + g.  A partial row holds a piece's
-// unnormalised state: in o_part the D accumulators sum_k p_k v_k, in l_part
-// the pair (m, l) of the running maximum (log2 units, scaled) and the sum of
-// 2^(s - m).  The D * G floats of a slot's rows hold 16-byte chunks in
-// chunk-major order: chunk c = 4 blk + grp of row g (dims 16 blk + 4 grp
-// .. + 3, one f32x4 of the MFMA accumulator layout) at float (c G + g) 4,
-// so that a wave stores each token's G rows as one contiguous run.
+// state: in l_part the pair (m, l) of its running maximum (log2 units,
+// scaled) and its sum of 2^(s - m), in o_part its D accumulators
+// sum_k 2^(s_k - m) v_k divided by l, as bf16.  The D * G elements of a
+// slot's rows hold 16-byte units in unit-major order: unit u = 4 p + grp of
+// row g (dims 32 p + 4 grp .. + 3, then 32 p + 16 + 4 grp .. + 3) at
+// element (u G + g) 8, so that a wave stores each token's G rows as one
+// contiguous run.
 struct MergeHead {
   int32_t base;
   int32_t nparts;
@@ -118,7 +119,7 @@ struct DevPlan {
   const Seg* segs;              // decode pieces, longest first
   const int32_t* merge_tok;     // decode tokens (their rows are merged from pieces)
   const MergeHead* merge_head;  // [merge token][KV head]
-  float* o_part;                // [partial row][d]
+  uint16_t* o_part;             // [partial row][d] bf16, in the partial layout
   float* l_part;                // [partial row][2]
 };
 

@@ -62,22 +62,45 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// A partial state's D accumulators in the plan's workspace.  The G rows of
-// one slot (one decode token against the G query heads of a KV head: rows
-// r0 .. r0 + G - 1, r0 a multiple of G) fill the G * D floats from float
-// r0 * D as 16-byte chunks, chunk-major: chunk c = 4 blk + grp of row g
-// (dims 16 blk + 4 grp .. + 3, one f32x4 of the MFMA accumulator layout)
-// at float (c * G + g) * 4.  A wave's store of one chunk then covers each
-// token's G rows as one run of 64 G bytes, not 4 G pieces of 16 bytes
-// strewn over as many cache lines.  The stores are non-temporal: whole
-// lines that the merge launch reads once, not kept dirty in the L2 of the
-// XCD that wrote them until the end of the launch.
-// Chunk grp of row `row` (query head g of its token); chunk c = 4 blk + grp
-// is at that pointer + part_chunk_stride(G) * blk.
-__device__ __forceinline__ float* part_chunk0(float* o_part, size_t row, int g, int G, int grp, int D) {
-  return o_part + (row - size_t(g)) * D + size_t(grp * G + g) * 4;
+// Four bf16 (two packed words, low element first) as floats.
+__device__ __forceinline__ f32x4 unpack_bf16x4(uint32_t a, uint32_t b) {
+  return f32x4{__builtin_bit_cast(float, a << 16), __builtin_bit_cast(float, a & 0xFFFF0000u),
+               __builtin_bit_cast(float, b << 16), __builtin_bit_cast(float, b & 0xFFFF0000u)};
 }
-__device__ __forceinline__ int part_chunk_stride(int G) { return 16 * G; }
+
+// A partial state's D values in the plan's workspace: the piece's
+// accumulators divided by its own sum l (a convex combination of V rows, so
+// within V's range), as bf16.  The G rows of one slot (one decode token
+// against the G query heads of a KV head: rows r0 .. r0 + G - 1, r0 a
+// multiple of G) fill the G * D elements from element r0 * D as 16-byte
+// units, unit-major: unit u = 4 p + grp of row g holds dims 32 p + 4 grp
+// .. + 3 and 32 p + 16 + 4 grp .. + 3 (two f32x4 of the MFMA accumulator
+// layout, blocks 2 p and 2 p + 1) at element (u * G + g) * 8.  A wave's
+// store of one unit then covers each token's G rows as one run of 64 G
+// bytes.  The stores are non-temporal: whole lines that the merge launch
+// reads once, not kept dirty in the L2 of the XCD that wrote them until the
+// end of the launch.
+// Unit grp of row `row` (query head g of its token); unit 4 p + grp is at
+// that pointer + part_unit_stride(G) * p.
+__device__ __forceinline__ uint16_t* part_unit0(uint16_t* o_part, size_t row, int g, int G, int grp, int D) {
+  return o_part + (row - size_t(g)) * D + size_t(grp * G + g) * 8;
+}
+__device__ __forceinline__ int part_unit_stride(int G) { return 32 * G; }
+
+// Store a lane's accumulators (dims 16 blk + 4 grp + i) as its units of a
+// partial row, scaled by inv = 1 / l (0 for a piece that saw no key).
+template <int D>
+__device__ __forceinline__ void store_partial(uint16_t* o_part, size_t row, int g, int G, int grp,
+                                              const f32x4 (&acc)[D / 16], float inv) {
+  uint16_t* out = part_unit0(o_part, row, g, G, grp, D);
+#pragma unroll
+  for (int p = 0; p < D / 32; ++p) {
+    const f32x4 x = acc[2 * p], y = acc[2 * p + 1];
+    const u32x4 w = {pack_bf16(x[0] * inv, x[1] * inv), pack_bf16(x[2] * inv, x[3] * inv),
+                     pack_bf16(y[0] * inv, y[1] * inv), pack_bf16(y[2] * inv, y[3] * inv)};
+    __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(out + part_unit_stride(G) * p));
+  }
+}
 
 // Placed inside a rarely taken branch (masking, rescaling): the compiler may
 // not turn the branch into always-executed selects.
@@ -1119,11 +1142,9 @@ __device__ __forceinline__ void extend_block(const AttnArgs& a, const Item* itp,
     } else if (valid) {
       // A wide prefix block's state, as a decode piece leaves it:
       // accumulator chunks in the partial layout, (m, l) once per column.
-      float* out = part_chunk0(a.plan.o_part, size_t(prow[b]), c & (G - 1), G, grp, D);
-#pragma unroll
-      for (int jj = 0; jj < D / 16; ++jj)
-        __builtin_nontemporal_store(ws.acc[b][jj], reinterpret_cast<f32x4*>(out + part_chunk_stride(G) * jj));
-      if (grp == 0) *reinterpret_cast<f32x2*>(a.plan.l_part + 2 * size_t(prow[b])) = f32x2{ws.m[b], ws.lv[b][0]};
+      const float l = column_sum(ws.lv[b][0]);  // the column sum sits in the group-0 lanes
+      store_partial<D>(a.plan.o_part, size_t(prow[b]), c & (G - 1), G, grp, ws.acc[b], l > 0.f ? 1.0f / l : 0.f);
+      if (grp == 0) *reinterpret_cast<f32x2*>(a.plan.l_part + 2 * size_t(prow[b])) = f32x2{ws.m[b], l};
     }
   }
 }
@@ -1415,17 +1436,14 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
                 valu_finish<D>(ws, xchg, lane, acc, l);
                 m = ws.m;
               } else {
-                l = ws.lv[0][0];  // the whole column sum in the group-0 lanes
+                l = column_sum(ws.lv[0][0]);  // the column sum sits in the group-0 lanes
                 m = ws.m[0];
 #pragma unroll
                 for (int jj = 0; jj < CH; ++jj) acc[jj] = ws.acc[0][jj];
               }
               if (valid) {
-                float* out =
-                    part_chunk0(a.plan.o_part, size_t(orow), (16 * wave + col) & (a.group - 1), a.group, grp, D);
-#pragma unroll
-                for (int jj = 0; jj < CH; ++jj)
-                  __builtin_nontemporal_store(acc[jj], reinterpret_cast<f32x4*>(out + part_chunk_stride(a.group) * jj));
+                store_partial<D>(a.plan.o_part, size_t(orow), (16 * wave + col) & (a.group - 1), a.group, grp, acc,
+                                 l > 0.f ? 1.0f / l : 0.f);
                 if (grp == 0) *reinterpret_cast<f32x2*>(a.plan.l_part + 2 * size_t(orow)) = f32x2{m, l};
               }
               reset_state(ws);
@@ -1486,22 +1504,20 @@ __global__ __launch_bounds__(256) void merge_rows_kernel(AttnArgs a, int n_tok) 
   const int tok = a.plan.merge_tok[m];
   const size_t row0 = size_t(mh.base) * a.group + (qh & (a.group - 1));
   const size_t stride = size_t(a.group);  // rows between slots
-  // Chunks 4 blk + grp and 4 (blk + 1) + grp of the row in slot 0.
-  const float* op =
-      part_chunk0(a.plan.o_part, row0, qh & (a.group - 1), a.group, grp, D) + part_chunk_stride(a.group) * blk;
-  const int op1 = part_chunk_stride(a.group);
+  // Unit 4 (blk / 2) + grp of the row in slot 0: blocks blk and blk + 1.
+  const uint16_t* op =
+      part_unit0(a.plan.o_part, row0, qh & (a.group - 1), a.group, grp, D) + part_unit_stride(a.group) * (blk / 2);
   const f32x2* lp = reinterpret_cast<const f32x2*>(a.plan.l_part) + row0;
   f32x2 ml[kMergeBatch];
-  f32x4 ov[kMergeBatch][2];
+  u32x4 ov[kMergeBatch];
 #pragma unroll
   for (int k = 0; k < kMergeBatch; ++k) {
     if (k < mh.nparts) {
       ml[k] = lp[k * stride];
-      ov[k][0] = *reinterpret_cast<const f32x4*>(op + k * stride * D);
-      ov[k][1] = *reinterpret_cast<const f32x4*>(op + k * stride * D + op1);
+      ov[k] = *reinterpret_cast<const u32x4*>(op + k * stride * D);
     } else {
       ml[k] = f32x2{kNegBig, 0.f};
-      ov[k][0] = ov[k][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+      ov[k] = u32x4{0u, 0u, 0u, 0u};
     }
   }
   float mx = kNegBig;
@@ -1510,19 +1526,21 @@ __global__ __launch_bounds__(256) void merge_rows_kernel(AttnArgs a, int n_tok) 
   for (int k = kMergeBatch; k < mh.nparts; ++k) mx = fmaxf(mx, lp[k * stride][0]);
   float z = 0.f;
   f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+  // Part k weighs 2^(m_k - mx) l_k: its values are already divided by l_k.
 #pragma unroll
   for (int k = 0; k < kMergeBatch; ++k) {
-    const float w = fast_exp2(ml[k][0] - mx);  // 0 for unused slots and for pieces that saw no key
-    z += w * ml[k][1];
-    acc0 += w * ov[k][0];
-    acc1 += w * ov[k][1];
+    const float wl = fast_exp2(ml[k][0] - mx) * ml[k][1];  // 0 for unused slots and for pieces that saw no key
+    z += wl;
+    acc0 += wl * unpack_bf16x4(ov[k][0], ov[k][1]);
+    acc1 += wl * unpack_bf16x4(ov[k][2], ov[k][3]);
   }
   for (int k = kMergeBatch; k < mh.nparts; ++k) {
     const f32x2 x = lp[k * stride];
-    const float w = fast_exp2(x[0] - mx);
-    z += w * x[1];
-    acc0 += w * *reinterpret_cast<const f32x4*>(op + k * stride * D);
-    acc1 += w * *reinterpret_cast<const f32x4*>(op + k * stride * D + op1);
+    const float wl = fast_exp2(x[0] - mx) * x[1];
+    const u32x4 v = *reinterpret_cast<const u32x4*>(op + k * stride * D);
+    z += wl;
+    acc0 += wl * unpack_bf16x4(v[0], v[1]);
+    acc1 += wl * unpack_bf16x4(v[2], v[3]);
   }
   const float inv = 1.0f / z;
   uint16_t* out = a.o + (size_t(tok) * a.hq + qh) * D + 16 * blk + 4 * grp;

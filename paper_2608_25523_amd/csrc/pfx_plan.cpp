@@ -56,7 +56,7 @@ DevPlan dev_plan(const pfx_plan* p, void* ws) {
   d.segs = reinterpret_cast<const Seg*>(base + p->off_segs);
   d.merge_tok = reinterpret_cast<const int32_t*>(base + p->off_merge_tok);
   d.merge_head = reinterpret_cast<const MergeHead*>(base + p->off_merge_head);
-  d.o_part = reinterpret_cast<float*>(base + p->off_opart);
+  d.o_part = reinterpret_cast<uint16_t*>(base + p->off_opart);
   d.l_part = reinterpret_cast<float*>(base + p->off_lpart);
   return d;
 }
@@ -589,7 +589,7 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   p->off_merge_tok = off;  off = align256(off + p->merge_tok.size() * 4);
   p->off_merge_head = off; off = align256(off + p->merge_head.size() * sizeof(MergeHead));
   p->blob_bytes = off;
-  p->off_opart = off;      off = align256(off + size_t(p->num_part_rows) * p->d * 4);
+  p->off_opart = off;      off = align256(off + size_t(p->num_part_rows) * p->d * 2);
   p->off_lpart = off;      off = align256(off + size_t(p->num_part_rows) * 8);
   p->total_bytes = std::max<size_t>(off, 256);
 
