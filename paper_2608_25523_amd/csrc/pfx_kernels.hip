@@ -1470,7 +1470,7 @@ constexpr int kMergeBatch = 8;
 // after it, writes them into their pool slots (2 Hkv D / 8 chunks of 16
 // bytes per token, spread over the token's threads).
 template <int D, bool F>
-__global__ __launch_bounds__(256) void merge_rows_kernel(AttnArgs a, int n_tok) {
+__global__ __launch_bounds__(128) void merge_rows_kernel(AttnArgs a, int n_tok) {
   constexpr int CH = D / 16;
   constexpr int SL = D / 8;  // threads per row: 4 groups x CH/2 pairs
   const size_t t = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -1657,11 +1657,15 @@ static void launch_all(AttnArgs a, const pfx_plan* p, hipStream_t s) {
   }
   const int n_tok = static_cast<int>(p->merge_tok.size());
   if (n_tok) {
+    // Workgroups of 128 threads: a decode-8B merge (32768 threads) then
+    // spreads over every compute unit instead of half of them.
+    constexpr int kMergeThreads = 128;
     const size_t threads = size_t(n_tok) * p->hq * (D / 8);
+    const dim3 grid((threads + kMergeThreads - 1) / kMergeThreads);
     if (a.fuse_append)
-      hipLaunchKernelGGL((merge_rows_kernel<D, true>), dim3((threads + 255) / 256), dim3(256), 0, s, a, n_tok);
+      hipLaunchKernelGGL((merge_rows_kernel<D, true>), grid, dim3(kMergeThreads), 0, s, a, n_tok);
     else
-      hipLaunchKernelGGL((merge_rows_kernel<D, false>), dim3((threads + 255) / 256), dim3(256), 0, s, a, n_tok);
+      hipLaunchKernelGGL((merge_rows_kernel<D, false>), grid, dim3(kMergeThreads), 0, s, a, n_tok);
   }
 }
 
