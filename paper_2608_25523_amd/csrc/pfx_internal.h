@@ -141,6 +141,7 @@ struct pfx_plan {
   std::vector<int32_t> row_tok, row_out, page_list, tok_req, tok_slot;
   std::vector<pfx::ReqInfo> req;
   int32_t num_segs = 0;        // decode pieces (their records live in the blob at off_segs)
+  int32_t merge_parts = 0;     // P when every merged (row, KV head) has P parts at slots (row * Hkv + h) * P, else 0
   int64_t num_decode_steps = 0;
   std::vector<int32_t> merge_tok;
   std::vector<pfx::MergeHead> merge_head;

@@ -164,6 +164,9 @@ struct AttnArgs {
   // Decode launch: its first num_wide workgroups run the wide prefix blocks
   // items[wide_first ...], the others the decode pieces.
   int32_t num_wide, wide_first;
+  // Merge launch: P when every (merge row m, KV head h) has P parts from
+  // slot (m Hkv + h) P (then merge_head is not read), else 0.
+  int32_t merge_parts;
 };
 
 // Geometry of one 32-key step of an item.
@@ -1500,7 +1503,8 @@ __global__ __launch_bounds__(128) void merge_rows_kernel(AttnArgs a, int n_tok) 
       }
     }
   }
-  const MergeHead mh = a.plan.merge_head[size_t(m) * a.hkv + (qh >> a.group_shift)];
+  const size_t unit = size_t(m) * a.hkv + (qh >> a.group_shift);
+  const MergeHead mh = a.merge_parts ? MergeHead{int32_t(unit) * a.merge_parts, a.merge_parts} : a.plan.merge_head[unit];
   const int tok = a.plan.merge_tok[m];
   const size_t row0 = size_t(mh.base) * a.group + (qh & (a.group - 1));
   const size_t stride = size_t(a.group);  // rows between slots
@@ -1731,6 +1735,7 @@ static int launch_attention(const pfx_pool* pool, const pfx_plan* p, const DevPl
   a.num_workers = p->decode_workers > 0 ? p->decode_workers : p->num_segs;
   a.num_wide = p->num_wide;
   a.wide_first = p->num_items;
+  a.merge_parts = p->merge_parts;
   if (p->d == 128) launch_all<128>(a, p, s); else launch_all<64>(a, p, s);
   return check_launch(who);
 }

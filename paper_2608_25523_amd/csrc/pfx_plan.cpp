@@ -439,6 +439,17 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
   if (part_units * G > (int64_t(1) << 31) / std::max(1, p->d))
     return delete p, fail(PFX_ERANGE, "pfx_plan_create: too many partial rows");
   p->num_part_rows = part_units * G;
+  // When every (merge row, KV head) has the same number of parts P, its
+  // slots start at (row * Hkv + h) * P, and the merge launch computes that
+  // instead of loading merge_head (one dependent round trip less).
+  p->merge_parts = 0;
+  if (!p->merge_head.empty()) {
+    const int32_t P = p->merge_head[0].nparts;
+    bool uniform = P >= 1;
+    for (size_t i = 0; uniform && i < p->merge_head.size(); ++i)
+      uniform = p->merge_head[i].nparts == P && int64_t(p->merge_head[i].base) == int64_t(i) * P;
+    if (uniform) p->merge_parts = P;
+  }
 
   // Longest first: a prefix step multiplies 64 query columns, a suffix step
   // at most 16, so prefix steps weigh a little more (a wide prefix step,
