@@ -142,6 +142,7 @@ struct pfx_plan {
   std::vector<pfx::ReqInfo> req;
   int32_t num_segs = 0;        // decode pieces (their records live in the blob at off_segs)
   int32_t merge_parts = 0;     // P when every merged (row, KV head) has P parts at slots (row * Hkv + h) * P, else 0
+  int32_t merge_tok_is_row = 0;  // 1 when merge row m is decode token m for every m
   int64_t num_decode_steps = 0;
   std::vector<int32_t> merge_tok;
   std::vector<pfx::MergeHead> merge_head;

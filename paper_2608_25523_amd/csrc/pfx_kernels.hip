@@ -165,8 +165,12 @@ struct AttnArgs {
   // items[wide_first ...], the others the decode pieces.
   int32_t num_wide, wide_first;
   // Merge launch: P when every (merge row m, KV head h) has P parts from
-  // slot (m Hkv + h) P (then merge_head is not read), else 0.
-  int32_t merge_parts;
+  // slot (m Hkv + h) P (then merge_head is not read), else 0; and 1 when
+  // merge row m is token m for every m (then the merge with the append
+  // folded in reads no merge_tok: the append's chain of loads, merge_tok,
+  // then tok_slot and the new rows, loses a round trip.  Without the
+  // append the load stays: measured, skipping it there was no faster).
+  int32_t merge_parts, merge_tok_is_row;
 };
 
 // Geometry of one 32-key step of an item.
@@ -1488,7 +1492,7 @@ __global__ __launch_bounds__(128) void merge_rows_kernel(AttnArgs a, int n_tok) 
   u32x4 app_val[kAppendPerThread];
   uint16_t* app_dst[kAppendPerThread] = {nullptr, nullptr};
   if constexpr (F) {
-    const int tok = a.plan.merge_tok[m];
+    const int tok = a.merge_tok_is_row ? m : a.plan.merge_tok[m];
     const int slot = a.plan.tok_slot[tok];
     const int per = a.hkv * SL;  // chunks of K (or V) per token
 #pragma unroll
@@ -1505,7 +1509,7 @@ __global__ __launch_bounds__(128) void merge_rows_kernel(AttnArgs a, int n_tok) 
   }
   const size_t unit = size_t(m) * a.hkv + (qh >> a.group_shift);
   const MergeHead mh = a.merge_parts ? MergeHead{int32_t(unit) * a.merge_parts, a.merge_parts} : a.plan.merge_head[unit];
-  const int tok = a.plan.merge_tok[m];
+  const int tok = F && a.merge_tok_is_row ? m : a.plan.merge_tok[m];
   const size_t row0 = size_t(mh.base) * a.group + (qh & (a.group - 1));
   const size_t stride = size_t(a.group);  // rows between slots
   // Unit 4 (blk / 2) + grp of the row in slot 0: blocks blk and blk + 1.
@@ -1736,6 +1740,7 @@ static int launch_attention(const pfx_pool* pool, const pfx_plan* p, const DevPl
   a.num_wide = p->num_wide;
   a.wide_first = p->num_items;
   a.merge_parts = p->merge_parts;
+  a.merge_tok_is_row = p->merge_tok_is_row;
   if (p->d == 128) launch_all<128>(a, p, s); else launch_all<64>(a, p, s);
   return check_launch(who);
 }

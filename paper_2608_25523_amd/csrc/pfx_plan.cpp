@@ -450,6 +450,11 @@ extern "C" int pfx_plan_create(const pfx_pool* pool, const pfx_prefix_table* pt,
       uniform = p->merge_head[i].nparts == P && int64_t(p->merge_head[i].base) == int64_t(i) * P;
     if (uniform) p->merge_parts = P;
   }
+  // Merge row m is decode token m (a batch of decode rows only, in order):
+  // the merge launch then needs no merge_tok load either.
+  p->merge_tok_is_row = 1;
+  for (size_t m = 0; p->merge_tok_is_row && m < p->merge_tok.size(); ++m)
+    p->merge_tok_is_row = p->merge_tok[m] == int32_t(m);
 
   // Longest first: a prefix step multiplies 64 query columns, a suffix step
   // at most 16, so prefix steps weigh a little more (a wide prefix step,
