@@ -1148,7 +1148,8 @@ __device__ __forceinline__ void extend_block(const AttnArgs& a, const Item* itp,
       write_rows<D>(a, ws.acc[b], ws.m[b], ws.lv[b][0], orow[b], valid, grp);
     } else if (valid) {
       // A wide prefix block's state, as a decode piece leaves it:
-      // accumulator chunks in the partial layout, (m, l) once per column.
+      // the accumulators divided by l as bf16 units of the partial layout,
+      // (m, l) once per column.
       const float l = column_sum(ws.lv[b][0]);  // the column sum sits in the group-0 lanes
       store_partial<D>(a.plan.o_part, size_t(prow[b]), c & (G - 1), G, grp, ws.acc[b], l > 0.f ? 1.0f / l : 0.f);
       if (grp == 0) *reinterpret_cast<f32x2*>(a.plan.l_part + 2 * size_t(prow[b])) = f32x2{ws.m[b], l};
@@ -1434,8 +1435,8 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(AttnArgs a) {
             else
               attend_step<D, 1>(ws, stage, qf, lim, k0 + kStepKeys * k, kend, causal != 0, 1, lane, a.scale_log2);
             if (k == cnst - 1) {
-              // The piece's state goes out as it stands: each f32x4 of the
-              // accumulators as one chunk of the partial layout, (m, l) once
+              // The piece's state goes out as it stands: the accumulators
+              // divided by l as bf16 units of the partial layout, (m, l) once
               // per column.
               float l, m;
               f32x4 acc[CH];
