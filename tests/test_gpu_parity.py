@@ -189,6 +189,39 @@ def test_small_batches_valu_engine(case):
     assert ds.plan.stats().num_wide_blocks == 0
 
 
+def random_case(seed):
+    """A seeded random small batch: any group size, head dim 64 or 128, zero
+    to three agents, decode rows (one or a few per request), extend
+    requests and requests without a prefix, with short pieces or few
+    workers so that rows merge many parts."""
+    rng = np.random.Generator(np.random.PCG64(9000 + seed))
+    hq, hkv = [(8, 8), (16, 8), (16, 4), (32, 4), (16, 1), (32, 8)][int(rng.integers(0, 6))]
+    g = hq // hkv
+    d = int(rng.choice([64, 128]))
+    plen = [int(x) for x in rng.integers(0, 400, size=int(rng.integers(1, 4)))]
+    reqs = []
+    for _ in range(int(rng.integers(3, 13))):
+        agent = int(rng.integers(-1, len(plen)))
+        L = int(rng.integers(1, 300))
+        kind = rng.random()
+        n = 1 if kind < 0.5 else (min(L, max(1, 16 // g)) if kind < 0.75 else L)
+        reqs.append((agent, L, n))
+    opts = [{}, dict(piece_steps=1), dict(piece_steps=2), dict(piece_steps=5), dict(decode_workers=3)][int(rng.integers(0, 5))]
+    return (seed, hq, hkv, d, plen, reqs, opts)
+
+
+RANDOM_CASES = [random_case(i) for i in range(12)]
+
+
+@pytest.mark.parametrize("case", RANDOM_CASES, ids=[f"random{c[0]}" for c in RANDOM_CASES])
+def test_random_small_batches(case):
+    """Seeded random shapes (group size, head dim, prefixes, decode and extend
+    rows, piece lengths): every row against the oracle."""
+    b, opts = small_batch(case)
+    hv = W.host_values(b, 7000 + case[0])
+    run_and_check(b, hv, f"random{case[0]} Hq={case[1]} Hkv={case[2]} d={case[3]} prefixes={case[4]}", **opts)
+
+
 def small_batch(case):
     seed, hq, hkv, d, plen, reqs, opts = case
     need = sum((p + 15) // 16 for p in plen) + sum((r[1] + 15) // 16 for r in reqs)
